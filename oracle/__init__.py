@@ -1,0 +1,39 @@
+"""CPU oracle for block-sparse video self-attention -- TEST INFRASTRUCTURE ONLY.
+
+Only the tests, the smoke check and the benchmark's CPU-baseline leg may import
+this package.  The GPU library never calls it, and it shares no code with the
+GPU path: every function here is a plain, slow, float64 restatement of what the
+path computes, written for a reader to check by eye.
+
+What the paper fixes (Section 4.2.2, "Sparse Attention"; Appendix A.2.2, the
+LTX-2.3 pipeline): attention over the spatiotemporal token set is replaced by a
+block-sparse pattern; blocks are routed by a score ("score-based routing", a
+"block-wise similarity metric"); the blocks that are kept ("critical blocks")
+are computed exactly; block size 64 and density 0.1 in the LTX-2.3 setting; a
+dense FlashAttention fallback.  The paper prints no formula for the routing
+score or the selection rule, so this oracle takes the readings listed in the
+design notes (mean-pooled block summaries, scaled dot-product block score,
+top-k or cumulative-softmax-mass selection, non-kept blocks contribute nothing).
+
+Parity status per function:
+  blocks.pool_blocks          pinned (closed form on arithmetic progressions, brute force)
+  select.block_scores         pinned (brute force, transposition-sensitive)
+  select.select_topk          pinned (brute-force sort with index tie-break, hand-worked fixture)
+  select.select_cummass       pinned (independent cumsum search, closed forms, invariants)
+  attention.block_sparse_attention / dense_attention
+                              pinned (pure-Python brute force, torch SDPA in float64,
+                                      closed forms, invariants)
+  The paper's own routing rule and its Taylor remainder for non-kept blocks:
+                              parity unpinned (not defined in the paper's text).
+"""
+from .blocks import bf16_bits_to_f64, num_blocks, block_bounds, pool_blocks
+from .select import (block_scores, topk_count, select_topk, first_frame_blocks,
+                     mass_cap, select_cummass, kept_to_arrays, kept_to_mask)
+from .attention import block_sparse_attention, dense_attention
+
+__all__ = [
+    "bf16_bits_to_f64", "num_blocks", "block_bounds", "pool_blocks",
+    "block_scores", "topk_count", "select_topk", "first_frame_blocks", "mass_cap",
+    "select_cummass", "kept_to_arrays", "kept_to_mask",
+    "block_sparse_attention", "dense_attention",
+]

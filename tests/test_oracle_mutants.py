@@ -1,0 +1,119 @@
+"""Planted mistakes in the oracle must be caught by its pins.
+
+Each case swaps one oracle function for a plausibly wrong version (dropped term,
+wrong divisor, transposed operand, reversed tie-break, ...) on the CPU and runs
+the pins that should fail.  A pin set that let a mutant through would not pin
+the oracle.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import oracle.attention as oatt
+import oracle.blocks as oblk
+import oracle.select as osel
+
+from . import test_oracle_attention as TA
+from . import test_oracle_pool as TP
+from . import test_oracle_select as TS
+
+pytestmark = pytest.mark.cpu
+
+
+def _pool_div_by_block(x, block):
+    x = np.asarray(x, dtype=np.float64)
+    b = oblk.block_bounds(x.shape[-2], block)
+    out = np.empty(x.shape[:-2] + (len(b), x.shape[-1]))
+    for i, (a, e) in enumerate(b):
+        out[..., i, :] = x[..., a:e, :].sum(axis=-2) / block
+    return out
+
+
+def _scores_transposed(q, k, scale):
+    return scale * np.matmul(np.asarray(k, float), np.swapaxes(np.asarray(q, float), -1, -2))
+
+
+def _order_desc_high_index_wins(row, candidates):
+    cand = np.asarray(list(candidates), dtype=np.int64)
+    order = np.lexsort((-cand, -row[cand]))
+    return [int(j) for j in cand[order]]
+
+
+def _cummass_forced_mass_ignored(scores, tau, cap, forced=()):
+    scores = np.asarray(scores, float)
+    flat = scores.reshape(-1, scores.shape[-1])
+    forced = sorted(set(forced))
+    rows = []
+    for s in flat:
+        p = np.exp(s - s.max()); p /= p.sum()
+        kept, mass = list(forced), 0.0
+        for j in osel._order_desc(s, [j for j in range(len(s)) if j not in forced]):
+            if mass >= tau or len(kept) >= cap:
+                break
+            kept.append(j); mass += p[j]
+        rows.append(sorted(kept))
+    return osel._reshape_nested(rows, scores.shape[:-1])
+
+
+def _attend_no_max_in_lse(qrows, keys, vals, scale):
+    logits = scale * (qrows @ keys.T)
+    mx = logits.max(axis=1, keepdims=True)
+    w = np.exp(logits - mx)
+    return (w @ vals) / w.sum(1, keepdims=True), np.log(w.sum(1))
+
+
+def _attend_scale_dropped(qrows, keys, vals, scale):
+    logits = qrows @ keys.T
+    mx = logits.max(axis=1, keepdims=True)
+    w = np.exp(logits - mx)
+    return (w @ vals) / w.sum(1, keepdims=True), mx[:, 0] + np.log(w.sum(1))
+
+
+def _attend_values_unnormalised(qrows, keys, vals, scale):
+    logits = scale * (qrows @ keys.T)
+    mx = logits.max(axis=1, keepdims=True)
+    w = np.exp(logits - mx)
+    return w @ vals, mx[:, 0] + np.log(w.sum(1))
+
+
+def _bounds_off_by_one(seq_len, block):
+    nb = -(-seq_len // block)
+    return [(i * block, min((i + 1) * block, seq_len - 1)) for i in range(nb)]
+
+
+MUTANTS = [
+    ("pool divides by S", oblk, "pool_blocks", _pool_div_by_block,
+     [lambda g: TP.test_pool_arithmetic_progression_closed_form(),
+      lambda g: TS.test_golden_pool_then_topk(g)]),
+    ("scores transposed", osel, "block_scores", _scores_transposed,
+     [lambda g: TS.test_scores_bruteforce_and_orientation(), lambda g: TS.test_golden_pool_then_topk(g)]),
+    ("ties go to the higher index", osel, "_order_desc", _order_desc_high_index_wins,
+     [lambda g: TS.test_topk_bruteforce_random_and_ties(), lambda g: TS.test_golden_pool_then_topk(g),
+      lambda g: TS.test_golden_mass(g)]),
+    ("forced mass not counted", osel, "select_cummass", _cummass_forced_mass_ignored,
+     [lambda g: TS.test_golden_mass(g),
+      lambda g: TS.test_mass_matches_independent_search_and_invariants(0.9, 0.3, True)]),
+    ("LSE without the max", oatt, "_attend", _attend_no_max_in_lse,
+     [lambda g: TA.test_sparse_bruteforce_pure_python(), lambda g: TA.test_dense_matches_torch_sdpa_float64()]),
+    ("softmax scale dropped", oatt, "_attend", _attend_scale_dropped,
+     [lambda g: TA.test_sparse_bruteforce_pure_python(), lambda g: TA.test_scale_is_applied()]),
+    ("values not normalised", oatt, "_attend", _attend_values_unnormalised,
+     [lambda g: TA.test_constant_values_give_constant_output()]),
+    ("last token of the sequence dropped", oblk, "block_bounds", _bounds_off_by_one,
+     [lambda g: TP.test_num_blocks_closed_form(1000, 64)]),
+]
+
+
+@pytest.mark.parametrize("name,mod,attr,fn,pins", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(name, mod, attr, fn, pins, monkeypatch, golden_dir):
+    monkeypatch.setattr(mod, attr, fn)
+    # re-export through the package namespace the pins call
+    if hasattr(oracle, attr):
+        monkeypatch.setattr(oracle, attr, fn)
+    for mname in ("oracle.attention", "oracle.select", "oracle.blocks"):
+        m = __import__(mname, fromlist=["x"])
+        if hasattr(m, attr) and m is not mod:
+            monkeypatch.setattr(m, attr, fn)
+    for pin in pins:
+        with pytest.raises(AssertionError):
+            pin(golden_dir)
