@@ -1,0 +1,165 @@
+/*
+ * sva.h -- block-sparse spatiotemporal self-attention for video DiTs on
+ * AMD Instinct MI355X (gfx950).  C ABI of libsva.so.
+ *
+ * The operation (paper Section 4.2.2 "Sparse Attention"; Appendix A.2.2, the
+ * LTX-2.3 stage-2 setting: block size 64, density 0.1, score-based routing,
+ * dense FlashAttention fallback): dense self-attention over the T x H x W
+ * video-token grid is replaced by attention that visits, for each query block,
+ * only the key/value blocks a block-importance score selects.  The paper
+ * prints no formula for the score or the selection; this library implements
+ * the reading below, step by step:
+ *
+ *   blocks   the grid is flattened t-major (n = (t*H + y)*W + x) and cut into
+ *            nB = ceil(N/S) contiguous blocks of S tokens; the last block may
+ *            be partial.
+ *   pool     qbar_i = mean of Q over the valid tokens of block i; same for K.
+ *   score    s[i,j] = c * <qbar_i, kbar_j>, c = softmax scale.
+ *   select   top-k: the k blocks with the largest s[i,j] (ties: lower j wins),
+ *            or cumulative mass: forced first-frame blocks, then blocks by
+ *            descending score while the kept softmax mass over j is below tau
+ *            and fewer than `cap` blocks are kept.
+ *   attend   for each valid query n of block i: softmax(c * Q[n] . K[m]) V[m]
+ *            over the valid keys m of the kept blocks only.
+ *
+ * Conventions for every entry point:
+ *   - Tensors are row-major and contiguous: Q, K, V, O are [B, H, N, D]
+ *     (D fastest), pooled summaries [B, H, nB, D] float32, kv_idx
+ *     [B, H, nB, kmax] int32, kv_count [B, H, nB] int32, mask [B, H, nB, nB]
+ *     uint8, lse [B, H, N] float32.
+ *   - Q, K, V, O are bf16 (O may be float32, see sva_problem.out_dtype).  All
+ *     device pointers are device memory owned by the caller; the library never
+ *     allocates, frees or keeps them.  Q/K/V/O must be 16-byte aligned, the
+ *     other arrays 4-byte aligned (mask: any alignment).
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Work
+ *     is enqueued asynchronously; no call synchronizes the host.
+ *   - Every call returns an sva_status.  Arguments are validated on the host
+ *     before anything is launched; on any error nothing is launched and no
+ *     output is touched.  SVA_ERR_HIP reports a launch error from the runtime.
+ *   - The library keeps no state between calls and is safe to call from
+ *     several host threads.
+ */
+#ifndef SVA_H
+#define SVA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SVA_VERSION_MAJOR 0
+#define SVA_VERSION_MINOR 1
+
+typedef enum sva_status {
+  SVA_OK = 0,
+  SVA_ERR_INVALID_ARG = 1, /* null pointer, value out of range, bad enum          */
+  SVA_ERR_SHAPE = 2,       /* N != T*H*W, kmax too small, sizes overflow          */
+  SVA_ERR_ALIGNMENT = 3,   /* pointer not aligned as required                     */
+  SVA_ERR_UNSUPPORTED = 4, /* valid but not implemented (head_dim, block, nB)     */
+  SVA_ERR_HIP = 5          /* the HIP runtime reported an error at launch         */
+} sva_status;
+
+typedef enum sva_dtype { SVA_BF16 = 0, SVA_F32 = 1 } sva_dtype;
+
+typedef enum sva_select_mode {
+  SVA_SELECT_TOPK = 0,    /* keep k blocks per query block                         */
+  SVA_SELECT_CUMMASS = 1  /* keep blocks until the softmax mass reaches tau        */
+} sva_select_mode;
+
+/* One video self-attention problem. */
+typedef struct sva_problem {
+  int32_t batch;         /* B >= 1                                                 */
+  int32_t heads;         /* H >= 1                                                 */
+  int32_t seq_len;       /* N >= 1 tokens; must equal grid_t*grid_h*grid_w         */
+  int32_t head_dim;      /* D in {64, 112, 128}                                    */
+  int32_t grid_t;        /* latent frames T >= 1                                   */
+  int32_t grid_h;        /* latent height >= 1                                     */
+  int32_t grid_w;        /* latent width  >= 1                                     */
+  int32_t block_size;    /* S in {64, 128}: query block == key/value block         */
+  double softmax_scale;  /* c; <= 0 selects 1/sqrt(D)                              */
+  int32_t out_dtype;     /* sva_dtype of O: SVA_BF16 or SVA_F32                     */
+} sva_problem;
+
+/* Block-selection rule. */
+typedef struct sva_select_params {
+  int32_t mode;             /* sva_select_mode                                      */
+  double keep_ratio;        /* top-k: r in (0, 1]; k = clamp(ceil(r*nB - 1e-6), 1, nB) */
+  int32_t topk;             /* top-k: k > 0 overrides keep_ratio (clamped to nB)    */
+  double mass_threshold;    /* mass: tau in (0, 1]                                  */
+  double max_keep_ratio;    /* mass: rho in (0, 1]; cap = clamp(ceil(rho*nB - 1e-6), |F|, nB) */
+  int32_t force_first_frame;/* mass: nonzero keeps every block holding a token of
+                               frame t = 0 (blocks j with j*S < grid_h*grid_w)      */
+} sva_select_params;
+
+/* Largest nB that sva_select_blocks accepts (block rows are selected in LDS). */
+#define SVA_SELECT_MAX_BLOCKS 2048
+
+/* nB = ceil(N / S) for a validated problem.  Host only. */
+int sva_num_blocks(const sva_problem* prob, int32_t* n_blocks);
+
+/* Kept blocks per row that sva_select_blocks may write: k in top-k mode, cap in
+ * mass mode.  kv_idx needs at least this many columns.  Host only. */
+int sva_max_keep(const sva_problem* prob, const sva_select_params* sel, int32_t* kmax);
+
+/* Step 1: block mean-pooling of Q and K (Section 4.2.2: a block-wise summary
+ * is what the routing score compares).
+ *   q, k    : bf16 [B, H, N, D] device
+ *   q_pool  : float32 [B, H, nB, D] device, written
+ *   k_pool  : float32 [B, H, nB, D] device, written
+ * Each output is the mean over the block's valid tokens, accumulated in
+ * float64 and rounded once to float32. */
+int sva_pool_blocks(const sva_problem* prob, const void* q, const void* k,
+                    float* q_pool, float* k_pool, void* stream);
+
+/* Steps 2-3: block scores and block selection ("score-based routing",
+ * Appendix A.2.2).
+ *   q_pool, k_pool : float32 [B, H, nB, D] device (from sva_pool_blocks)
+ *   kmax           : columns of kv_idx, >= sva_max_keep(...)
+ *   kv_idx         : int32 [B, H, nB, kmax] device, written: kept KV blocks of
+ *                    each query block in ascending order, padded with -1
+ *   kv_count       : int32 [B, H, nB] device, written: number of kept blocks
+ *   mask           : uint8 [B, H, nB, nB] device or NULL; if given, written
+ *                    with 1 for kept (i, j) and 0 elsewhere
+ * Scores are accumulated in float64; ties in score are broken toward the lower
+ * block index.  Requires nB <= SVA_SELECT_MAX_BLOCKS. */
+int sva_select_blocks(const sva_problem* prob, const sva_select_params* sel,
+                      const float* q_pool, const float* k_pool, int32_t kmax,
+                      int32_t* kv_idx, int32_t* kv_count, uint8_t* mask,
+                      void* stream);
+
+/* Step 4: attention over the kept blocks only (Section 4.2.2: the kept blocks
+ * are computed exactly).
+ *   q, k, v   : bf16 [B, H, N, D] device
+ *   kv_idx    : int32 [B, H, nB, kmax] device; entries outside [0, nB) are
+ *               skipped, as are entries at or beyond kv_count
+ *   kv_count  : int32 [B, H, nB] device; values are clamped to [0, kmax]
+ *   out       : [B, H, N, D] device, bf16 or float32 per out_dtype, written for
+ *               every valid token; a query block with no valid kept block gets
+ *               zeros
+ *   lse       : float32 [B, H, N] device or NULL; natural-log log-sum-exp of
+ *               the scaled logits of each query (-inf for an empty row)
+ * bf16 MFMA products with float32 accumulation and an online softmax in
+ * float32.  Duplicate entries in a row are attended twice. */
+int sva_sparse_attention(const sva_problem* prob, const void* q, const void* k,
+                         const void* v, const int32_t* kv_idx,
+                         const int32_t* kv_count, int32_t kmax, void* out,
+                         float* lse, void* stream);
+
+/* The dense fallback (Appendix A.2.2 keeps layers 0-1 dense): step 4 with
+ * every block kept.  Arguments as for sva_sparse_attention. */
+int sva_dense_attention(const sva_problem* prob, const void* q, const void* k,
+                        const void* v, void* out, float* lse, void* stream);
+
+/* Static text for a status code. */
+const char* sva_status_string(int status);
+
+/* SVA_VERSION_MAJOR * 100 + SVA_VERSION_MINOR. */
+int sva_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SVA_H */

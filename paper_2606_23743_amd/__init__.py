@@ -1,0 +1,17 @@
+"""Block-sparse spatiotemporal self-attention for video DiTs on MI355X (gfx950).
+
+The compute path is libsva.so (HIP kernels behind the C ABI in include/sva.h);
+this package is its Python binding plus the synthetic-input generator and the
+workload shapes.  Importing the package does not load the library; the first
+call into it does, and raises if libsva.so has not been built.
+"""
+from . import workloads
+from ._lib import (SvaError, Problem, SelectParams, load, problem, problem_for, select_topk,
+                   select_mass, select_for, num_blocks, max_keep, pool_blocks, select_blocks,
+                   sparse_attention, dense_attention, status_string, LIB_PATH)
+
+__all__ = [
+    "workloads", "SvaError", "Problem", "SelectParams", "load", "problem", "problem_for",
+    "select_topk", "select_mass", "select_for", "num_blocks", "max_keep", "pool_blocks",
+    "select_blocks", "sparse_attention", "dense_attention", "status_string", "LIB_PATH",
+]

@@ -1,0 +1,259 @@
+"""ctypes binding of libsva.so (include/sva.h).  Argument marshalling only:
+every step of the path runs in the library's HIP kernels.  torch supplies device
+memory and the current stream; nothing here computes on the host, and there is
+no fallback -- a missing or unloadable library raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from typing import Optional, Tuple
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libsva.so")
+HEADER = os.path.join(os.path.dirname(HERE), "include", "sva.h")
+
+SVA_OK, SVA_ERR_INVALID_ARG, SVA_ERR_SHAPE, SVA_ERR_ALIGNMENT, SVA_ERR_UNSUPPORTED, SVA_ERR_HIP = range(6)
+SVA_BF16, SVA_F32 = 0, 1
+SVA_SELECT_TOPK, SVA_SELECT_CUMMASS = 0, 1
+SVA_SELECT_MAX_BLOCKS = 2048
+
+
+class SvaError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: status {status} ({status_string(status)})")
+
+
+class Problem(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("heads", ctypes.c_int32), ("seq_len", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("grid_t", ctypes.c_int32), ("grid_h", ctypes.c_int32),
+                ("grid_w", ctypes.c_int32), ("block_size", ctypes.c_int32),
+                ("softmax_scale", ctypes.c_double), ("out_dtype", ctypes.c_int32)]
+
+
+class SelectParams(ctypes.Structure):
+    _fields_ = [("mode", ctypes.c_int32), ("keep_ratio", ctypes.c_double), ("topk", ctypes.c_int32),
+                ("mass_threshold", ctypes.c_double), ("max_keep_ratio", ctypes.c_double),
+                ("force_first_frame", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libsva.so once; raise if it is missing (build it with
+    `python -m paper_2606_23743_amd.build`)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} not found: build the HIP library first "
+                           "(python -m paper_2606_23743_amd.build)")
+    lib = ctypes.CDLL(path)
+    P, S = ctypes.POINTER(Problem), ctypes.POINTER(SelectParams)
+    vp, i32p = ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32)
+    sig = {
+        "sva_num_blocks": [P, i32p],
+        "sva_max_keep": [P, S, i32p],
+        "sva_pool_blocks": [P, vp, vp, vp, vp, vp],
+        "sva_select_blocks": [P, S, vp, vp, ctypes.c_int32, vp, vp, vp, vp],
+        "sva_sparse_attention": [P, vp, vp, vp, vp, vp, ctypes.c_int32, vp, vp, vp],
+        "sva_dense_attention": [P, vp, vp, vp, vp, vp, vp],
+        "sva_status_string": [ctypes.c_int],
+        "sva_version": [],
+    }
+    for name, args in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_char_p if name == "sva_status_string" else ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def header_functions(header: str = HEADER):
+    """Names of the functions include/sva.h declares."""
+    text = open(header).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+char\*|int)\s+(sva_\w+)\s*\(", text, re.M)))
+
+
+def status_string(status: int) -> str:
+    try:
+        return load().sva_status_string(int(status)).decode()
+    except Exception:  # pragma: no cover - only while reporting another error
+        return "?"
+
+
+def _check(status: int, what: str):
+    if status != SVA_OK:
+        raise SvaError(status, what)
+
+
+# ----------------------------------------------------------------- parameters
+
+def problem(batch, heads, seq_len, head_dim, grid, block_size, softmax_scale=0.0,
+            out_dtype="bf16") -> Problem:
+    t, h, w = grid
+    return Problem(batch, heads, seq_len, head_dim, t, h, w, block_size, float(softmax_scale),
+                   SVA_F32 if out_dtype in ("f32", "float32", SVA_F32) else SVA_BF16)
+
+
+def problem_for(wl, out_dtype="bf16", softmax_scale=0.0) -> Problem:
+    return problem(wl.batch, wl.heads, wl.seq_len, wl.head_dim, (wl.grid_t, wl.grid_h, wl.grid_w),
+                   wl.block, softmax_scale, out_dtype)
+
+
+def select_topk(keep_ratio: float = 0.0, topk: int = 0) -> SelectParams:
+    return SelectParams(SVA_SELECT_TOPK, float(keep_ratio), int(topk), 0.0, 0.0, 0)
+
+
+def select_mass(tau: float, max_keep_ratio: float, force_first_frame: bool) -> SelectParams:
+    return SelectParams(SVA_SELECT_CUMMASS, 0.0, 0, float(tau), float(max_keep_ratio),
+                        1 if force_first_frame else 0)
+
+
+def select_for(wl, keep_ratio: Optional[float] = None) -> SelectParams:
+    if wl.mode == "mass":
+        return select_mass(wl.mass_threshold, wl.max_keep_ratio, wl.force_first_frame)
+    if keep_ratio is not None:
+        return select_topk(keep_ratio, 0)
+    return select_topk(wl.keep_ratio, wl.topk)
+
+
+def num_blocks(prob: Problem) -> int:
+    out = ctypes.c_int32()
+    _check(load().sva_num_blocks(ctypes.byref(prob), ctypes.byref(out)), "sva_num_blocks")
+    return out.value
+
+
+def max_keep(prob: Problem, sel: SelectParams) -> int:
+    out = ctypes.c_int32()
+    _check(load().sva_max_keep(ctypes.byref(prob), ctypes.byref(sel), ctypes.byref(out)), "sva_max_keep")
+    return out.value
+
+
+# ------------------------------------------------------------- device calls
+
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _need(t, dtype, shape, name):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _qkv_shape(prob):
+    return (prob.batch, prob.heads, prob.seq_len, prob.head_dim)
+
+
+def pool_blocks(prob: Problem, q, k, q_pool=None, k_pool=None, stream=None) -> Tuple:
+    torch = _torch()
+    nb = num_blocks(prob)
+    shp = _qkv_shape(prob)
+    _need(q, torch.bfloat16, shp, "q")
+    _need(k, torch.bfloat16, shp, "k")
+    pshape = (prob.batch, prob.heads, nb, prob.head_dim)
+    if q_pool is None:
+        q_pool = torch.empty(pshape, dtype=torch.float32, device=q.device)
+    if k_pool is None:
+        k_pool = torch.empty(pshape, dtype=torch.float32, device=q.device)
+    _need(q_pool, torch.float32, pshape, "q_pool")
+    _need(k_pool, torch.float32, pshape, "k_pool")
+    _check(load().sva_pool_blocks(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(q_pool), _ptr(k_pool),
+                                  _stream(stream)), "sva_pool_blocks")
+    return q_pool, k_pool
+
+
+def select_blocks(prob: Problem, sel: SelectParams, q_pool, k_pool, kmax: Optional[int] = None,
+                  kv_idx=None, kv_count=None, want_mask: bool = False, mask=None, stream=None) -> Tuple:
+    torch = _torch()
+    nb = num_blocks(prob)
+    pshape = (prob.batch, prob.heads, nb, prob.head_dim)
+    _need(q_pool, torch.float32, pshape, "q_pool")
+    _need(k_pool, torch.float32, pshape, "k_pool")
+    if kmax is None:
+        kmax = max_keep(prob, sel)
+    dev = q_pool.device
+    if kv_idx is None:
+        kv_idx = torch.empty((prob.batch, prob.heads, nb, kmax), dtype=torch.int32, device=dev)
+    if kv_count is None:
+        kv_count = torch.empty((prob.batch, prob.heads, nb), dtype=torch.int32, device=dev)
+    _need(kv_idx, torch.int32, (prob.batch, prob.heads, nb, kmax), "kv_idx")
+    _need(kv_count, torch.int32, (prob.batch, prob.heads, nb), "kv_count")
+    if want_mask and mask is None:
+        mask = torch.empty((prob.batch, prob.heads, nb, nb), dtype=torch.uint8, device=dev)
+    if mask is not None:
+        _need(mask, torch.uint8, (prob.batch, prob.heads, nb, nb), "mask")
+    _check(load().sva_select_blocks(ctypes.byref(prob), ctypes.byref(sel), _ptr(q_pool), _ptr(k_pool),
+                                    int(kmax), _ptr(kv_idx), _ptr(kv_count), _ptr(mask), _stream(stream)),
+           "sva_select_blocks")
+    return kv_idx, kv_count, mask
+
+
+def _out_tensor(prob, like, out):
+    torch = _torch()
+    dt = torch.float32 if prob.out_dtype == SVA_F32 else torch.bfloat16
+    if out is None:
+        out = torch.empty(_qkv_shape(prob), dtype=dt, device=like.device)
+    _need(out, dt, _qkv_shape(prob), "out")
+    return out
+
+
+def sparse_attention(prob: Problem, q, k, v, kv_idx, kv_count, out=None, want_lse: bool = False,
+                     lse=None, stream=None) -> Tuple:
+    torch = _torch()
+    nb = num_blocks(prob)
+    shp = _qkv_shape(prob)
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        _need(t, torch.bfloat16, shp, n)
+    kmax = kv_idx.shape[-1]
+    _need(kv_idx, torch.int32, (prob.batch, prob.heads, nb, kmax), "kv_idx")
+    _need(kv_count, torch.int32, (prob.batch, prob.heads, nb), "kv_count")
+    out = _out_tensor(prob, q, out)
+    if want_lse and lse is None:
+        lse = torch.empty(shp[:3], dtype=torch.float32, device=q.device)
+    if lse is not None:
+        _need(lse, torch.float32, shp[:3], "lse")
+    _check(load().sva_sparse_attention(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(kv_idx),
+                                       _ptr(kv_count), int(kmax), _ptr(out), _ptr(lse), _stream(stream)),
+           "sva_sparse_attention")
+    return out, lse
+
+
+def dense_attention(prob: Problem, q, k, v, out=None, want_lse: bool = False, lse=None,
+                    stream=None) -> Tuple:
+    torch = _torch()
+    shp = _qkv_shape(prob)
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        _need(t, torch.bfloat16, shp, n)
+    out = _out_tensor(prob, q, out)
+    if want_lse and lse is None:
+        lse = torch.empty(shp[:3], dtype=torch.float32, device=q.device)
+    if lse is not None:
+        _need(lse, torch.float32, shp[:3], "lse")
+    _check(load().sva_dense_attention(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(out),
+                                      _ptr(lse), _stream(stream)), "sva_dense_attention")
+    return out, lse

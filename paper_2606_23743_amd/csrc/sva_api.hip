@@ -1,0 +1,197 @@
+// Host side of the C ABI declared in include/sva.h: argument validation and
+// dispatch.  Every check runs before any HIP call, so invalid arguments return
+// a status without touching the device.
+#include <math.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/sva.h"
+#include "sva_internal.h"
+
+namespace {
+
+using sva::Dims;
+using sva::SelectRule;
+
+constexpr double kCountEps = 1e-6;   // guards ceil() against ratio*nB landing a hair above an integer
+
+bool aligned(const void* p, size_t n) { return (reinterpret_cast<uintptr_t>(p) % n) == 0; }
+
+int check_problem(const sva_problem* p, Dims* d) {
+  if (!p) return SVA_ERR_INVALID_ARG;
+  if (p->batch < 1 || p->heads < 1 || p->seq_len < 1 || p->head_dim < 1 || p->block_size < 1)
+    return SVA_ERR_INVALID_ARG;
+  if (p->grid_t < 1 || p->grid_h < 1 || p->grid_w < 1) return SVA_ERR_INVALID_ARG;
+  if (p->out_dtype != SVA_BF16 && p->out_dtype != SVA_F32) return SVA_ERR_INVALID_ARG;
+  if (!(p->softmax_scale == p->softmax_scale) || isinf(p->softmax_scale)) return SVA_ERR_INVALID_ARG;
+  const int64_t thw = (int64_t)p->grid_t * p->grid_h * p->grid_w;
+  if (thw != (int64_t)p->seq_len) return SVA_ERR_SHAPE;
+  if (p->head_dim != 64 && p->head_dim != 112 && p->head_dim != 128) return SVA_ERR_UNSUPPORTED;
+  if (p->block_size != 64 && p->block_size != 128) return SVA_ERR_UNSUPPORTED;
+  const int64_t nB = ((int64_t)p->seq_len + p->block_size - 1) / p->block_size;
+  const int64_t rows = (int64_t)p->batch * p->heads * nB;
+  if (rows > INT32_MAX) return SVA_ERR_SHAPE;
+  // element offsets are formed in 64-bit; the per-head offset bh*N*D must fit too
+  const int64_t elems = (int64_t)p->batch * p->heads * p->seq_len * p->head_dim;
+  if (elems / p->head_dim / p->seq_len != (int64_t)p->batch * p->heads) return SVA_ERR_SHAPE;
+  if ((int64_t)p->batch * p->heads * p->seq_len > INT32_MAX) return SVA_ERR_SHAPE;
+  if (d) {
+    d->B = p->batch;
+    d->H = p->heads;
+    d->N = p->seq_len;
+    d->D = p->head_dim;
+    d->S = p->block_size;
+    d->nB = (int)nB;
+    d->frame_tokens = (int)((int64_t)p->grid_h * p->grid_w > INT32_MAX ? INT32_MAX
+                                                                        : (int64_t)p->grid_h * p->grid_w);
+    d->scale = p->softmax_scale > 0.0 ? p->softmax_scale : 1.0 / sqrt((double)p->head_dim);
+    d->out_f32 = p->out_dtype == SVA_F32;
+  }
+  return SVA_OK;
+}
+
+int check_select(const sva_select_params* s, const Dims& d, SelectRule* r) {
+  if (!s) return SVA_ERR_INVALID_ARG;
+  SelectRule out{};
+  out.mode = s->mode;
+  if (s->mode == SVA_SELECT_TOPK) {
+    if (s->topk < 0) return SVA_ERR_INVALID_ARG;
+    int64_t k;
+    if (s->topk > 0) {
+      k = s->topk;
+    } else {
+      if (!(s->keep_ratio > 0.0 && s->keep_ratio <= 1.0)) return SVA_ERR_INVALID_ARG;
+      k = (int64_t)ceil(s->keep_ratio * d.nB - kCountEps);
+    }
+    if (k < 1) k = 1;
+    if (k > d.nB) k = d.nB;
+    out.k = (int)k;
+    out.cap = out.k;
+  } else if (s->mode == SVA_SELECT_CUMMASS) {
+    if (!(s->mass_threshold > 0.0 && s->mass_threshold <= 1.0)) return SVA_ERR_INVALID_ARG;
+    if (!(s->max_keep_ratio > 0.0 && s->max_keep_ratio <= 1.0)) return SVA_ERR_INVALID_ARG;
+    int nf = 0;
+    if (s->force_first_frame) {
+      const int64_t f = ((int64_t)d.frame_tokens + d.S - 1) / d.S;
+      nf = (int)(f < d.nB ? f : d.nB);
+    }
+    int64_t cap = (int64_t)ceil(s->max_keep_ratio * d.nB - kCountEps);
+    if (cap > d.nB) cap = d.nB;
+    if (cap < nf) cap = nf;
+    if (cap < 1) cap = 1;
+    out.cap = (int)cap;
+    out.n_forced = nf;
+    out.tau = s->mass_threshold;
+  } else {
+    return SVA_ERR_INVALID_ARG;
+  }
+  if (r) *r = out;
+  return SVA_OK;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? SVA_OK : SVA_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+int sva_version(void) { return SVA_VERSION_MAJOR * 100 + SVA_VERSION_MINOR; }
+
+const char* sva_status_string(int status) {
+  switch (status) {
+    case SVA_OK: return "ok";
+    case SVA_ERR_INVALID_ARG: return "invalid argument";
+    case SVA_ERR_SHAPE: return "inconsistent or oversized shape";
+    case SVA_ERR_ALIGNMENT: return "misaligned pointer";
+    case SVA_ERR_UNSUPPORTED: return "unsupported head_dim, block_size or block count";
+    case SVA_ERR_HIP: return "HIP runtime error at launch";
+    default: return "unknown status";
+  }
+}
+
+int sva_num_blocks(const sva_problem* prob, int32_t* n_blocks) {
+  if (!n_blocks) return SVA_ERR_INVALID_ARG;
+  Dims d;
+  const int st = check_problem(prob, &d);
+  if (st != SVA_OK) return st;
+  *n_blocks = d.nB;
+  return SVA_OK;
+}
+
+int sva_max_keep(const sva_problem* prob, const sva_select_params* sel, int32_t* kmax) {
+  if (!kmax) return SVA_ERR_INVALID_ARG;
+  Dims d;
+  int st = check_problem(prob, &d);
+  if (st != SVA_OK) return st;
+  SelectRule r;
+  st = check_select(sel, d, &r);
+  if (st != SVA_OK) return st;
+  *kmax = r.cap;
+  return SVA_OK;
+}
+
+int sva_pool_blocks(const sva_problem* prob, const void* q, const void* k, float* q_pool,
+                    float* k_pool, void* stream) {
+  Dims d;
+  const int st = check_problem(prob, &d);
+  if (st != SVA_OK) return st;
+  if (!q || !k || !q_pool || !k_pool) return SVA_ERR_INVALID_ARG;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(q_pool, 4) || !aligned(k_pool, 4))
+    return SVA_ERR_ALIGNMENT;
+  return hip_status(sva::launch_pool(d, static_cast<const uint16_t*>(q),
+                                     static_cast<const uint16_t*>(k), q_pool, k_pool,
+                                     static_cast<hipStream_t>(stream)));
+}
+
+int sva_select_blocks(const sva_problem* prob, const sva_select_params* sel, const float* q_pool,
+                      const float* k_pool, int32_t kmax, int32_t* kv_idx, int32_t* kv_count,
+                      uint8_t* mask, void* stream) {
+  Dims d;
+  int st = check_problem(prob, &d);
+  if (st != SVA_OK) return st;
+  SelectRule r;
+  st = check_select(sel, d, &r);
+  if (st != SVA_OK) return st;
+  if (!q_pool || !k_pool || !kv_idx || !kv_count) return SVA_ERR_INVALID_ARG;
+  if (!aligned(q_pool, 4) || !aligned(k_pool, 4) || !aligned(kv_idx, 4) || !aligned(kv_count, 4))
+    return SVA_ERR_ALIGNMENT;
+  if (d.nB > SVA_SELECT_MAX_BLOCKS) return SVA_ERR_UNSUPPORTED;
+  if (kmax < r.cap) return SVA_ERR_SHAPE;
+  return hip_status(sva::launch_select(d, r, q_pool, k_pool, kmax, kv_idx, kv_count, mask,
+                                       static_cast<hipStream_t>(stream)));
+}
+
+int sva_sparse_attention(const sva_problem* prob, const void* q, const void* k, const void* v,
+                         const int32_t* kv_idx, const int32_t* kv_count, int32_t kmax, void* out,
+                         float* lse, void* stream) {
+  Dims d;
+  const int st = check_problem(prob, &d);
+  if (st != SVA_OK) return st;
+  if (!q || !k || !v || !kv_idx || !kv_count || !out) return SVA_ERR_INVALID_ARG;
+  if (kmax < 1) return SVA_ERR_SHAPE;
+  if ((int64_t)d.B * d.H * d.nB * kmax > ((int64_t)1 << 40)) return SVA_ERR_SHAPE;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
+      !aligned(kv_idx, 4) || !aligned(kv_count, 4) || (lse && !aligned(lse, 4)))
+    return SVA_ERR_ALIGNMENT;
+  return hip_status(sva::launch_attention(
+      d, true, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+      static_cast<const uint16_t*>(v), kv_idx, kv_count, kmax, out, lse,
+      static_cast<hipStream_t>(stream)));
+}
+
+int sva_dense_attention(const sva_problem* prob, const void* q, const void* k, const void* v,
+                        void* out, float* lse, void* stream) {
+  Dims d;
+  const int st = check_problem(prob, &d);
+  if (st != SVA_OK) return st;
+  if (!q || !k || !v || !out) return SVA_ERR_INVALID_ARG;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
+      (lse && !aligned(lse, 4)))
+    return SVA_ERR_ALIGNMENT;
+  return hip_status(sva::launch_attention(
+      d, false, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+      static_cast<const uint16_t*>(v), nullptr, nullptr, 1, out, lse,
+      static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

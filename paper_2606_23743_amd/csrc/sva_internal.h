@@ -1,0 +1,53 @@
+// Internal declarations shared by the HIP translation units of libsva.so.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sva {
+
+// Problem sizes after host validation.
+struct Dims {
+  int B, H, N, D, S, nB;
+  int frame_tokens;   // grid_h * grid_w
+  double scale;       // softmax scale c (resolved, > 0)
+  bool out_f32;
+};
+
+// Selection rule after host validation (counts already derived).
+struct SelectRule {
+  int mode;     // 0 top-k, 1 cumulative mass
+  int k;        // top-k: blocks kept per row
+  double tau;   // mass: threshold
+  int cap;      // mass: most blocks kept per row
+  int n_forced; // mass: forced first-frame blocks 0 .. n_forced-1
+};
+
+hipError_t launch_pool(const Dims& d, const uint16_t* q, const uint16_t* k, float* q_pool,
+                       float* k_pool, hipStream_t stream);
+
+hipError_t launch_select(const Dims& d, const SelectRule& r, const float* q_pool,
+                         const float* k_pool, int kmax, int32_t* kv_idx, int32_t* kv_count,
+                         uint8_t* mask, hipStream_t stream);
+
+hipError_t launch_attention(const Dims& d, bool sparse, const uint16_t* q, const uint16_t* k,
+                            const uint16_t* v, const int32_t* kv_idx, const int32_t* kv_count,
+                            int kmax, void* out, float* lse, hipStream_t stream);
+
+// Workgroup order: the hardware hands consecutive workgroup ids to the 8 XCDs
+// round-robin.  Mapping id -> (id % 8) * ceil(n/8) + id / 8 gives each XCD a
+// contiguous range of logical work items, so neighbouring query blocks of a
+// head (which read overlapping key/value blocks) share one XCD's L2.
+__device__ __forceinline__ int xcd_remap(int id, int n) {
+  constexpr int kXcd = 8;
+  const int per = (n + kXcd - 1) / kXcd;
+  const int xcd = id % kXcd;
+  const int slot = id / kXcd;
+  // the first (n % 8) XCDs (or all, if n is a multiple of 8) own `per` items,
+  // the rest own per-1; compute the start of this XCD's range accordingly
+  const int full = (n % kXcd == 0) ? kXcd : (n % kXcd);
+  const int start = (xcd < full) ? xcd * per : full * per + (xcd - full) * (per - 1);
+  return start + slot;
+}
+
+}  // namespace sva

@@ -1,0 +1,101 @@
+"""Comparison rules between the HIP path and the oracle (test helpers).
+
+Masks: rows must agree on every block whose oracle score is more than EPS away
+from the row's oracle boundary scores (the lowest kept and the highest dropped
+non-forced score).  Top-k counts must be exactly k; forced blocks must be
+present; in mass mode the count may differ by one only when the oracle's kept
+mass at count-1 or count is within EPS of tau, and then only the boundary block
+may differ.
+
+Attention: max |dO| <= 2e-2 and mean |dO| <= 2e-3 over valid elements (bf16
+inputs, fp32 accumulation); LSE within LSE_TOL (bf16 rounding of the
+probabilities bounds the relative error of the row sum by 2^-9, so ln(sum) by
+about 2e-3).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+EPS = 1e-5
+MAX_ABS = 2e-2
+MEAN_ABS = 2e-3
+LSE_TOL = 3e-3
+
+
+def gpu_rows(kv_idx: np.ndarray, kv_count: np.ndarray):
+    """Flatten GPU outputs into a list of kept lists (row-major over B, H, nB)."""
+    idx = kv_idx.reshape(-1, kv_idx.shape[-1])
+    cnt = kv_count.reshape(-1)
+    return [idx[r, : cnt[r]].tolist() for r in range(idx.shape[0])]
+
+
+def check_idx_layout(kv_idx: np.ndarray, kv_count: np.ndarray, n_blocks: int):
+    """Ascending, in range, -1 padded: exact structural checks on every row."""
+    idx = kv_idx.reshape(-1, kv_idx.shape[-1])
+    cnt = kv_count.reshape(-1)
+    for r in range(idx.shape[0]):
+        c = int(cnt[r])
+        row = idx[r]
+        assert 0 <= c <= row.size, (r, c)
+        kept = row[:c]
+        assert np.all(kept >= 0) and np.all(kept < n_blocks), (r, kept)
+        assert np.all(np.diff(kept) > 0), (r, kept)
+        assert np.all(row[c:] == -1), (r, row[c:])
+
+
+def _softmax(s):
+    w = np.exp(s - s.max())
+    return w / w.sum()
+
+
+def compare_masks(oracle_rows, gpu_rows_, scores: np.ndarray, mode: str, k: int = 0,
+                  tau: float = 0.0, forced=(), eps: float = EPS):
+    """Return (n_rows, n_identical, problems) where problems lists failing rows."""
+    flat_scores = scores.reshape(-1, scores.shape[-1])
+    forced = set(int(j) for j in forced)
+    problems = []
+    identical = 0
+    for r, (ko, kg) in enumerate(zip(oracle_rows, gpu_rows_)):
+        so, sg = set(ko), set(kg)
+        if so == sg:
+            identical += 1
+            continue
+        s = flat_scores[r]
+        if mode == "topk" and len(kg) != k:
+            problems.append((r, "count", len(kg), k))
+            continue
+        if not forced <= sg:
+            problems.append((r, "forced missing"))
+            continue
+        free_kept = [j for j in ko if j not in forced]
+        dropped = [j for j in range(s.size) if j not in so]
+        lo = min(s[j] for j in free_kept) if free_kept else np.inf
+        hi = max(s[j] for j in dropped) if dropped else -np.inf
+        diff = so ^ sg
+        if mode == "mass" and len(kg) != len(ko):
+            if abs(len(kg) - len(ko)) != 1:
+                problems.append((r, "mass count", len(kg), len(ko)))
+                continue
+            p = _softmax(s)
+            order = sorted(free_kept, key=lambda j: (-s[j], j))
+            m_forced = sum(p[j] for j in forced)
+            m_all = m_forced + sum(p[j] for j in order)
+            m_less = m_all - (p[order[-1]] if order else 0.0)
+            if not (abs(m_all - tau) <= eps or abs(m_less - tau) <= eps):
+                problems.append((r, "mass count not near tau", len(kg), len(ko), m_less, m_all))
+                continue
+            if len(diff) != 1:
+                problems.append((r, "mass diff > 1 block", sorted(diff)))
+                continue
+            continue
+        bad = [j for j in diff if abs(s[j] - lo) > eps and abs(s[j] - hi) > eps]
+        if bad:
+            problems.append((r, "blocks differ away from the boundary", bad[:5], lo, hi))
+    return len(oracle_rows), identical, problems
+
+
+def attention_errors(gpu_out: np.ndarray, ref: np.ndarray, valid: np.ndarray):
+    """max and mean |gpu - ref| over the elements selected by `valid` (bool, same
+    leading shape as ref without D)."""
+    d = np.abs(gpu_out.astype(np.float64) - ref)[valid]
+    return float(d.max()) if d.size else 0.0, float(d.mean()) if d.size else 0.0
