@@ -1,0 +1,245 @@
+"""Benchmark: block-sparse video self-attention on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                    [--no-cpu-baseline] [--no-dense] [--cpu-seconds S]
+
+One step = the whole sparse path on one synthetic layer already resident in
+HBM: block pooling -> block selection -> sparse attention (the dense fallback
+is timed separately as the speedup denominator).  Prints one JSON line.
+
+value        kept-block attention FLOPs / step time (pool + select + attend)
+roofline     the sparse-attention kernel alone: kept FLOPs per launch / mean
+             launch time (HIP events on the stream the kernel runs on),
+             against the bf16 dense MFMA peak
+cpu_baseline the float64 oracle on a bounded sample of the same workload (one
+             head's pooling and selection plus as many query blocks as fit the
+             time budget), in the same unit
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "effective TFLOP/s of sparse attention (kept blocks) + % bf16 MFMA peak"
+BF16_PEAK_TFLOPS = 2516.6   # 256 CU x 2.4 GHz x 4096 dense bf16 flop/clk/CU
+HBM_PEAK_GBS = 8000.0
+
+
+def kept_flops(idx: np.ndarray, cnt: np.ndarray, N: int, S: int, D: int):
+    """(valid-token FLOPs, full-block FLOPs, kept pairs): 4*D*n_i*n_j per kept
+    (query block i, key block j) pair; n = valid tokens of the block."""
+    nb = cnt.shape[-1]
+    ntok = np.full(nb + 1, S, dtype=np.int64)
+    ntok[nb - 1] = N - (nb - 1) * S
+    ntok[nb] = 0
+    kmax = idx.shape[-1]
+    col = np.arange(kmax)[None, None, None, :]
+    live = col < cnt[..., None]
+    j = np.where(live & (idx >= 0) & (idx < nb), idx, nb)
+    kept_tok = ntok[j].sum(axis=-1)                  # [B, H, nB]
+    flops = 4 * D * float((ntok[None, None, :nb] * kept_tok).sum())
+    pairs = int(cnt.sum())
+    return flops, 4.0 * D * S * S * pairs, pairs
+
+
+def cpu_baseline(wl, bits, budget_s: float):
+    """Time the oracle on a bounded sample: head (0, 0) pooling + selection,
+    then block-sparse attention on query blocks until the budget is spent."""
+    import oracle
+    from threadpoolctl import threadpool_info
+
+    t0 = time.perf_counter()
+    f = {n: oracle.bf16_bits_to_f64(bits[n][0, 0]) for n in ("q", "k", "v")}
+    c = 1.0 / np.sqrt(wl.head_dim)
+    qp = oracle.pool_blocks(f["q"], wl.block)
+    kp = oracle.pool_blocks(f["k"], wl.block)
+    s = oracle.block_scores(qp, kp, c)
+    nb = s.shape[-1]
+    # BLAS registers its thread pool once numpy has called into it (the matmul above)
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    if wl.mode == "mass":
+        forced = oracle.first_frame_blocks(wl.grid_h, wl.grid_w, wl.block, nb) if wl.force_first_frame else []
+        kept = oracle.select_cummass(s, wl.mass_threshold, oracle.mass_cap(nb, wl.max_keep_ratio, len(forced)),
+                                     forced)
+    else:
+        kept = oracle.select_topk(s, oracle.topk_count(nb, wl.keep_ratio, wl.topk))
+    t_select = time.perf_counter() - t0
+    q4, k4, v4 = (f[n][None, None] for n in ("q", "k", "v"))
+    rng = np.random.default_rng(0)
+    order = rng.permutation(nb)
+    flops = 0.0
+    done = 0
+    t1 = time.perf_counter()
+    ntok = [min(wl.block, wl.seq_len - i * wl.block) for i in range(nb)]
+    for i in order:
+        oracle.block_sparse_attention(q4, k4, v4, [[kept]], wl.block, c, rows=[(0, 0, int(i))])
+        flops += 4.0 * wl.head_dim * ntok[i] * sum(ntok[j] for j in kept[i])
+        done += 1
+        if time.perf_counter() - t1 > budget_s:
+            break
+    t_attn = time.perf_counter() - t1
+    total = t_select + t_attn
+    return {
+        "value": flops / total / 1e12,
+        "unit": "TFLOP/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": (f"head (b=0,h=0) of {wl.name}: float64 pooling + scores + selection over all "
+                   f"{nb} query blocks ({t_select:.2f} s), then block-sparse attention on {done} "
+                   f"random query blocks ({t_attn:.2f} s); value = kept FLOPs of those blocks / "
+                   f"total seconds"),
+        "attention_only_tflops": flops / t_attn / 1e12,
+        "seconds": total,
+    }
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="large_64b_b1h48d128_n111600_s128")
+    ap.add_argument("--keep-ratio", type=float, default=None, help="override the top-k keep ratio")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+              "the path shards over (batch, head) with no communication, but no multi-GPU "
+              "launcher is built.", file=sys.stderr)
+        return 2
+
+    import torch
+
+    import paper_2606_23743_amd as sva
+    from paper_2606_23743_amd import inputs, workloads
+
+    wl = workloads.find(args.workload)
+    if wl is None:
+        print(f"unknown workload {args.workload}; one of {list(workloads.BY_NAME)}", file=sys.stderr)
+        return 2
+    if args.keep_ratio is not None:
+        wl = wl.with_ratio(args.keep_ratio)
+    print(f"[bench] generating {wl.name}", file=sys.stderr, flush=True)
+    bits = inputs.generate(wl)
+    dev = {n: inputs.to_device(bits[n]) for n in ("q", "k", "v")}
+    prob = sva.problem_for(wl)
+    sel = sva.select_for(wl)
+    nb = sva.num_blocks(prob)
+    kmax = sva.max_keep(prob, sel)
+    B, H, N, D, S = wl.batch, wl.heads, wl.seq_len, wl.head_dim, wl.block
+    f32, i32 = torch.float32, torch.int32
+    qp = torch.empty((B, H, nb, D), dtype=f32, device="cuda")
+    kp = torch.empty_like(qp)
+    idx = torch.empty((B, H, nb, kmax), dtype=i32, device="cuda")
+    cnt = torch.empty((B, H, nb), dtype=i32, device="cuda")
+    out = torch.empty((B, H, N, D), dtype=torch.bfloat16, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    ev = lambda: torch.cuda.Event(enable_timing=True)   # noqa: E731
+    pool_ev = [(ev(), ev()) for _ in range(args.steps)]
+    sel_ev = [(ev(), ev()) for _ in range(args.steps)]
+    att_ev = [(ev(), ev()) for _ in range(args.steps)]
+
+    def step(k=None):
+        if k is not None:
+            pool_ev[k][0].record(stream)
+        sva.pool_blocks(prob, dev["q"], dev["k"], qp, kp, stream=stream)
+        if k is not None:
+            pool_ev[k][1].record(stream)
+            sel_ev[k][0].record(stream)
+        sva.select_blocks(prob, sel, qp, kp, kmax, idx, cnt, stream=stream)
+        if k is not None:
+            sel_ev[k][1].record(stream)
+            att_ev[k][0].record(stream)
+        sva.sparse_attention(prob, dev["q"], dev["k"], dev["v"], idx, cnt, out=out, stream=stream)
+        if k is not None:
+            att_ev[k][1].record(stream)
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t_start, t_end = ev(), ev()
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for k in range(args.steps):
+        step(k)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    ms_step = t_start.elapsed_time(t_end) / args.steps
+    pool_ms = float(np.mean([a.elapsed_time(b) for a, b in pool_ev]))
+    sel_ms = float(np.mean([a.elapsed_time(b) for a, b in sel_ev]))
+    att_ms = float(np.mean([a.elapsed_time(b) for a, b in att_ev]))
+    print(f"[bench] step {ms_step:.3f} ms (pool {pool_ms:.3f}, select {sel_ms:.3f}, attention {att_ms:.3f})",
+          file=sys.stderr, flush=True)
+
+    flops, flops_full, pairs = kept_flops(idx.cpu().numpy(), cnt.cpu().numpy(), N, S, D)
+    att_tflops = flops / (att_ms * 1e-3) / 1e12
+    value = flops / (ms_step * 1e-3) / 1e12
+    pool_bytes = 2 * B * H * N * D * 2 + 2 * B * H * nb * D * 4
+
+    extra = {}
+    if not args.no_dense:
+        dout = torch.empty_like(out)
+        sva.dense_attention(prob, dev["q"], dev["k"], dev["v"], out=dout, stream=stream)
+        a, b = ev(), ev()
+        a.record(stream)
+        sva.dense_attention(prob, dev["q"], dev["k"], dev["v"], out=dout, stream=stream)
+        b.record(stream)
+        torch.cuda.synchronize()
+        dense_ms = a.elapsed_time(b)
+        dense_flops = 4.0 * D * B * H * float(N) * N
+        extra["dense_attention"] = {"ms": dense_ms, "tflops": dense_flops / (dense_ms * 1e-3) / 1e12,
+                                    "sparse_path_speedup": dense_ms / ms_step}
+        del dout
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        print(f"[bench] cpu baseline (~{args.cpu_seconds:.0f} s)", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(wl, bits, args.cpu_seconds)
+
+    sel_desc = (f"cumulative mass tau={wl.mass_threshold} cap={kmax}" if wl.mode == "mass"
+                else f"top-k k={kmax} (r={wl.keep_ratio})" if not wl.topk else f"top-k k={wl.topk}")
+    rec = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "batch": B, "heads": H, "seq_len": N, "head_dim": D,
+                   "grid": [wl.grid_t, wl.grid_h, wl.grid_w], "block": S, "selection": sel_desc,
+                   "kept_pairs": pairs, "kept_flops": flops, "kept_flops_full_blocks": flops_full},
+        "pct_of_bf16_peak": round(100.0 * value / BF16_PEAK_TFLOPS, 2),
+        "roofline": {"bound": "mfma", "kernel": "sparse attention", "achieved": round(att_tflops, 2),
+                     "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(att_tflops / BF16_PEAK_TFLOPS, 4), "traffic": None},
+        "stages_ms": {"pool": round(pool_ms, 4), "select": round(sel_ms, 4), "attention": round(att_ms, 4)},
+        "pool_hbm_gbs": round(pool_bytes / (pool_ms * 1e-3) / 1e9, 1),
+        "cpu_baseline": cpu,
+    }
+    rec.update(extra)
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

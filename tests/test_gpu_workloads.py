@@ -1,0 +1,118 @@
+"""GPU parity at the five workload shapes, in the launch configuration the
+benchmark times.  Pooled summaries are checked on every head, block masks on
+every row (near-tie rule), attention on sampled query blocks (first, last
+partial, and random ones) that the oracle computes one by one -- both with the
+oracle's own index lists and end to end with the GPU's.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2606_23743_amd as sva
+from paper_2606_23743_amd import inputs, workloads
+
+from . import parity
+from .gpu_cases import flat_rows, oracle_select, say
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+torch = pytest.importorskip("torch")
+
+SAMPLE_BLOCKS = 6
+
+
+def _sample_rows(wl, nb, rng):
+    rows = {(0, 0, 0), (wl.batch - 1, wl.heads - 1, nb - 1)}
+    while len(rows) < SAMPLE_BLOCKS:
+        rows.add((int(rng.integers(wl.batch)), int(rng.integers(wl.heads)), int(rng.integers(nb))))
+    return sorted(rows)
+
+
+def _run(wl, ratios):
+    say(f"[workload {wl.name}] generating B={wl.batch} H={wl.heads} N={wl.seq_len} D={wl.head_dim}")
+    bits = inputs.generate(wl)
+    dev = {n: inputs.to_device(bits[n]) for n in ("q", "k", "v")}
+    prob = sva.problem_for(wl)
+    nb = sva.num_blocks(prob)
+    c = 1.0 / math.sqrt(wl.head_dim)
+    qp, kp = sva.pool_blocks(prob, dev["q"], dev["k"])
+    torch.cuda.synchronize()
+    gqp, gkp = qp.cpu().numpy(), kp.cpu().numpy()
+
+    # pooled summaries and scores, every head
+    say(f"[workload {wl.name}] oracle pooling")
+    oqp = np.empty(gqp.shape)
+    okp = np.empty(gkp.shape)
+    for b in range(wl.batch):
+        for h in range(wl.heads):
+            oqp[b, h] = oracle.pool_blocks(oracle.bf16_bits_to_f64(bits["q"][b, h]), wl.block)
+            okp[b, h] = oracle.pool_blocks(oracle.bf16_bits_to_f64(bits["k"][b, h]), wl.block)
+    assert np.array_equal(gqp, oqp.astype(np.float32))
+    assert np.array_equal(gkp, okp.astype(np.float32))
+    scores = oracle.block_scores(oqp, okp, c)
+
+    rng = np.random.default_rng(wl.seed)
+    rows = _sample_rows(wl, nb, rng)
+    f64 = {}
+    for n in ("q", "k", "v"):
+        f64[n] = {}
+        for (b, h, _) in rows:
+            f64[n][(b, h)] = oracle.bf16_bits_to_f64(bits[n][b, h])
+
+    for r in ratios:
+        sel = sva.select_for(wl, r)
+        kmax = sva.max_keep(prob, sel)
+        idx, cnt, _ = sva.select_blocks(prob, sel, qp, kp, kmax)
+        out, lse = sva.sparse_attention(prob, dev["q"], dev["k"], dev["v"], idx, cnt, want_lse=True)
+        torch.cuda.synchronize()
+        gidx, gcnt = idx.cpu().numpy(), cnt.cpu().numpy()
+        parity.check_idx_layout(gidx, gcnt, nb)
+        say(f"[workload {wl.name} r={r}] oracle selection")
+        kept, info = oracle_select(wl, scores, r)
+        rows_o = flat_rows(kept)
+        rows_g = parity.gpu_rows(gidx, gcnt)
+        n, same, problems = parity.compare_masks(rows_o, rows_g, scores, info["mode"], k=info["k"],
+                                                 tau=info["tau"], forced=info["forced"])
+        say(f"[workload {wl.name} r={r}] mask rows={n} identical={same} problems={len(problems)}")
+        assert not problems, problems[:5]
+
+        # attention with the oracle's own index lists, sampled query blocks
+        oidx, ocnt = oracle.kept_to_arrays(kept, nb, kmax)
+        oout, olse = sva.sparse_attention(prob, dev["q"], dev["k"], dev["v"], torch.from_numpy(oidx).cuda(),
+                                          torch.from_numpy(ocnt).cuda(), want_lse=True)
+        torch.cuda.synchronize()
+        for (b, h, i) in rows:
+            sub_kept = [[kept[b][h]]]
+            q4, k4, v4 = (f64[n][(b, h)][None, None] for n in ("q", "k", "v"))
+            ref, rlse = oracle.block_sparse_attention(q4, k4, v4, sub_kept, wl.block, c, rows=[(0, 0, i)])
+            a, e = i * wl.block, min((i + 1) * wl.block, wl.seq_len)
+            got = oout[b, h, a:e].float().cpu().numpy()
+            mx, mean = parity.attention_errors(got, ref[0, 0, a:e], np.ones(got.shape, dtype=bool))
+            assert mx <= parity.MAX_ABS and mean <= parity.MEAN_ABS, ((b, h, i), mx, mean)
+            assert np.max(np.abs(olse[b, h, a:e].cpu().numpy() - rlse[0, 0, a:e])) <= parity.LSE_TOL
+            # end to end: the GPU's own selection, where it matches the oracle's row
+            row_id = (b * wl.heads + h) * nb + i
+            if set(rows_g[row_id]) == set(rows_o[row_id]):
+                got2 = out[b, h, a:e].float().cpu().numpy()
+                mx2, mean2 = parity.attention_errors(got2, ref[0, 0, a:e], np.ones(got2.shape, dtype=bool))
+                assert mx2 <= parity.MAX_ABS and mean2 <= parity.MEAN_ABS, ((b, h, i), mx2, mean2)
+        say(f"[workload {wl.name} r={r}] attention ok on {len(rows)} sampled query blocks")
+        if r == 1.0:
+            dout, _ = sva.dense_attention(prob, dev["q"], dev["k"], dev["v"])
+            torch.cuda.synchronize()
+            assert torch.equal(dout, out), "keep-all sparse must equal the dense kernel"
+        del idx, cnt, out, lse, oout, olse
+    del dev
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("wl", [workloads.TINY, workloads.SMALL_2B, workloads.MID_22B,
+                                workloads.LARGE_64B], ids=lambda w: w.name)
+def test_workload(wl):
+    _run(wl, [None])
+
+
+def test_cfg_sweep_all_ratios():
+    _run(workloads.CFG_SWEEP, list(workloads.CFG_SWEEP.ratios))
