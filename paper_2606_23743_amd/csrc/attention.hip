@@ -36,17 +36,6 @@ typedef __attribute__((ext_vector_type(2))) float f32x2;
 
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
-struct AttnArgs {
-  const uint16_t* q;
-  const uint16_t* k;
-  const uint16_t* v;
-  const int32_t* kv_idx;
-  const int32_t* kv_count;
-  void* out;
-  float* lse;
-  int N, nB, kmax, n_rows;
-  float scale_log2;   // c * log2(e)
-};
 
 // ds_read_b64_tr_b16 on an LDS address (the pointer must point into __shared__).
 __device__ __forceinline__ i16x4 lds_read_tr16(const uint16_t* p) {
@@ -86,6 +75,13 @@ __global__ __launch_bounds__(S * 2) void attn_kernel(AttnArgs a) {
   const int bh = row / nB;
   const int i = row - bh * nB;
   const size_t head = (size_t)bh * N * D;
+  if (a.only_marked) {
+    // recompute only blocks the fixed-max kernel marked (NaN first element)
+    const size_t first = head + (size_t)i * S * D;
+    const bool marked = OUT_F32 ? __builtin_isnan(static_cast<const float*>(a.out)[first])
+                                : ((static_cast<const uint16_t*>(a.out)[first] & 0x7FFF) > 0x7F80);
+    if (!marked) return;
+  }
   const uint16_t* Qh = a.q + head;
   const uint16_t* Kh = a.k + head;
   const uint16_t* Vh = a.v + head;
@@ -298,6 +294,18 @@ hipError_t launch_ds(const Dims& d, bool sparse, const AttnArgs& a, hipStream_t 
 
 }  // namespace
 
+hipError_t launch_attention_rescaling(const Dims& d, bool sparse, const AttnArgs& a, hipStream_t stream) {
+  switch (d.D * 1000 + d.S) {
+    case 64064: return launch_ds<64, 64>(d, sparse, a, stream);
+    case 64128: return launch_ds<64, 128>(d, sparse, a, stream);
+    case 112064: return launch_ds<112, 64>(d, sparse, a, stream);
+    case 112128: return launch_ds<112, 128>(d, sparse, a, stream);
+    case 128064: return launch_ds<128, 64>(d, sparse, a, stream);
+    case 128128: return launch_ds<128, 128>(d, sparse, a, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 hipError_t launch_attention(const Dims& d, bool sparse, const uint16_t* q, const uint16_t* k,
                             const uint16_t* v, const int32_t* kv_idx, const int32_t* kv_count,
                             int kmax, void* out, float* lse, hipStream_t stream) {
@@ -314,16 +322,15 @@ hipError_t launch_attention(const Dims& d, bool sparse, const uint16_t* q, const
   a.kmax = kmax;
   a.n_rows = d.B * d.H * d.nB;
   a.scale_log2 = (float)(d.scale * 1.4426950408889634);
-  const int key = d.D * 1000 + d.S;
-  switch (key) {
-    case 64064: return launch_ds<64, 64>(d, sparse, a, stream);
-    case 64128: return launch_ds<64, 128>(d, sparse, a, stream);
-    case 112064: return launch_ds<112, 64>(d, sparse, a, stream);
-    case 112128: return launch_ds<112, 128>(d, sparse, a, stream);
-    case 128064: return launch_ds<128, 64>(d, sparse, a, stream);
-    case 128128: return launch_ds<128, 128>(d, sparse, a, stream);
-    default: return hipErrorInvalidValue;
+  a.only_marked = 0;
+  if (d.S == 128) {
+    // fixed-max kernel, then the rescaling kernel for any block it marked
+    hipError_t e = launch_attention_q64(d, sparse, a, stream);
+    if (e != hipSuccess) return e;
+    a.only_marked = 1;
+    return launch_attention_rescaling(d, sparse, a, stream);
   }
+  return launch_attention_rescaling(d, sparse, a, stream);
 }
 
 }  // namespace sva

@@ -23,6 +23,27 @@ struct SelectRule {
   int n_forced; // mass: forced first-frame blocks 0 .. n_forced-1
 };
 
+// Arguments shared by the attention kernels.
+struct AttnArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  const int32_t* kv_idx;
+  const int32_t* kv_count;
+  void* out;
+  float* lse;
+  int N, nB, kmax, n_rows;
+  float scale_log2;   // c * log2(e)
+  int only_marked;    // rescaling kernel: recompute only query blocks whose first
+                      // output element holds the NaN mark of the fixed-max kernel
+};
+
+// The rescaling (per-iteration online softmax) kernel; attention.hip.
+hipError_t launch_attention_rescaling(const Dims& d, bool sparse, const AttnArgs& a, hipStream_t stream);
+
+// 64-queries-per-wave attention with a fixed reference max; attention_q64.hip.
+hipError_t launch_attention_q64(const Dims& d, bool sparse, const AttnArgs& a, hipStream_t stream);
+
 hipError_t launch_pool(const Dims& d, const uint16_t* q, const uint16_t* k, float* q_pool,
                        float* k_pool, hipStream_t stream);
 

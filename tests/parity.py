@@ -8,9 +8,11 @@ mass at count-1 or count is within EPS of tau, and then only the boundary block
 may differ.
 
 Attention: max |dO| <= 2e-2 and mean |dO| <= 2e-3 over valid elements (bf16
-inputs, fp32 accumulation); LSE within LSE_TOL (bf16 rounding of the
-probabilities bounds the relative error of the row sum by 2^-9, so ln(sum) by
-about 2e-3).
+inputs, fp32 accumulation); LSE within LSE_TOL.  The row sum adds the
+probabilities after rounding to bf16 (8 significant bits, so each has a
+relative error of at most 2^-8); when every probability rounds the same way
+(identical keys) the sum is off by up to 2^-8 relative, i.e. ln(sum) by up to
+ln(1 + 2^-8) = 3.9e-3.
 """
 from __future__ import annotations
 
@@ -19,7 +21,7 @@ import numpy as np
 EPS = 1e-5
 MAX_ABS = 2e-2
 MEAN_ABS = 2e-3
-LSE_TOL = 3e-3
+LSE_TOL = 4e-3
 
 
 def gpu_rows(kv_idx: np.ndarray, kv_count: np.ndarray):

@@ -256,3 +256,39 @@ def test_select_ties_go_to_lower_index():
         want = oracle.select_topk(s, k)[0][0]
         assert parity.gpu_rows(idx.cpu().numpy(), cnt.cpu().numpy()) == want, k
         assert want[2][:1] == [3]        # of the tied 3/9/12 the lowest index comes first
+
+
+@pytest.mark.parametrize("S,D", [(128, 128), (128, 112), (128, 64)])
+def test_logit_growth_beyond_fixed_reference_is_exact(S, D):
+    """Block-size-128 kernels fix the softmax reference max from the first key
+    chunk.  Here a later kept block's logits exceed it by about 1000 (log2
+    units), which overflows that reference; the block must be recomputed with
+    per-iteration rescaling and still match the oracle, while other query
+    blocks keep their normal results."""
+    B, H, grid = 1, 1, (4, 8, 16)           # N = 512, 4 blocks of 128
+    wl = SC(f"overflow_{S}_{D}", B, H, D, grid, S, "topk", topk=2, seed=31)
+    bits = inputs.generate(wl)
+    N = wl.seq_len
+    # block 0 keys ~0 (logits ~0 for every query), block 3 keys large and aligned with queries 128..255
+    f = {n: inputs.bf16_bits_to_f32(bits[n]).copy() for n in ("q", "k", "v")}
+    f["k"][0, 0, 0:128] *= 1e-3
+    f["q"][0, 0, 128:256] = 8.0
+    f["k"][0, 0, 384:512] = 8.0
+    new_bits = {n: inputs._round_bf16(f[n]) for n in f}
+    dev = device_inputs(new_bits)
+    prob = sva.problem_for(wl)
+    rows = [[0, 1], [0, 3], [1, 2], [2, 3]]          # query block 1: first block 0, then the huge block 3
+    idx = np.array(rows, dtype=np.int32).reshape(1, 1, 4, 2)
+    cnt = np.full((1, 1, 4), 2, dtype=np.int32)
+    out, lse = sva.sparse_attention(prob, dev["q"], dev["k"], dev["v"], torch.from_numpy(idx).cuda(),
+                                    torch.from_numpy(cnt).cuda(), want_lse=True)
+    torch.cuda.synchronize()
+    f64 = {n: oracle.bf16_bits_to_f64(new_bits[n]) for n in ("q", "k", "v")}
+    ref, rlse = oracle.block_sparse_attention(f64["q"], f64["k"], f64["v"], [[rows]], S, scale_of(wl))
+    o = out.float().cpu().numpy()
+    assert np.isfinite(o).all()
+    mx, mean = parity.attention_errors(o, ref, np.ones(ref.shape, dtype=bool))
+    assert mx <= parity.MAX_ABS and mean <= parity.MEAN_ABS, (mx, mean)
+    # absolute bf16-probability bound plus float32 relative error of a ~700 LSE
+    err = np.abs(lse.cpu().numpy() - rlse)
+    assert np.all(err <= parity.LSE_TOL + 1e-5 * np.abs(rlse)), err.max()
