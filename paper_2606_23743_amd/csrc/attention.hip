@@ -322,14 +322,11 @@ hipError_t launch_attention(const Dims& d, bool sparse, const uint16_t* q, const
   a.kmax = kmax;
   a.n_rows = d.B * d.H * d.nB;
   a.scale_log2 = (float)(d.scale * 1.4426950408889634);
+  // fixed-reference-max kernel, then the rescaling kernel for any block it marked
   a.only_marked = 0;
-  if (d.S == 128) {
-    // fixed-max kernel, then the rescaling kernel for any block it marked
-    hipError_t e = launch_attention_q64(d, sparse, a, stream);
-    if (e != hipSuccess) return e;
-    a.only_marked = 1;
-    return launch_attention_rescaling(d, sparse, a, stream);
-  }
+  hipError_t e = launch_attention_q32(d, sparse, a, stream);
+  if (e != hipSuccess) return e;
+  a.only_marked = 1;
   return launch_attention_rescaling(d, sparse, a, stream);
 }
 

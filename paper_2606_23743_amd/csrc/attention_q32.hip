@@ -1,0 +1,371 @@
+// Block-sparse (and dense) flash attention, 32 queries per wave, two waves per
+// SIMD (Section 4.2.2: kept blocks computed exactly; Appendix A.2.2: dense
+// FlashAttention fallback).
+//
+// A workgroup is one query block of S tokens with S/32 waves of 32 queries.
+// Each wave's state (O^T 64 registers, Q^T 32, one key chunk of S^T and P)
+// fits in 256 registers, so two workgroups share a CU with two waves on every
+// SIMD: while one wave runs its MFMAs the other runs its softmax, which the
+// hardware overlaps without any in-wave software pipelining.
+//
+// Keys are processed in 32-key chunks staged in LDS with two stages: the next chunk's K and V tiles are fetched with
+// buffer_load ... lds straight into the other stage while this one computes.
+// Tiles are unpadded and XOR-swizzled on 16-byte pieces (K: c ^ (row & 7),
+// conflict-free for the ds_read_b128 operand reads; V: c ^ 2(row & 7),
+// conflict-free for the ds_read_b64_tr_b16 transpose reads).
+//
+// Per 32-key sub-chunk (lane = one query; its 16 S^T registers are keys
+// (r/4)*8 + half*4 + r%4):
+//   S^T = K Q^T                mfma_f32_32x32x16_bf16, Q^T in registers
+//   p   = exp2(c*log2e*s - m)  m is the reference maximum fixed from the first
+//                              chunk of the row, so O is never rescaled here
+//   l  += sum of the bf16 p    v_dot2 with (1, 1)
+//   O^T += V^T P^T             P^T from the S^T registers, V^T by transpose reads
+// A row whose logits outgrow the first chunk's maximum by ~100 (log2 units)
+// could overflow: such query blocks are marked (NaN first element) and the
+// per-iteration rescaling kernel that runs next recomputes them.
+#include "attn_common.h"
+
+namespace sva {
+namespace {
+
+using namespace attn;
+
+template <int D, int S, bool SPARSE, bool OUT_F32>
+__global__ __launch_bounds__(2 * S) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void attn_q32_kernel(AttnArgs a) {
+  using G = Geo<D>;
+  constexpr int NW = S / 32;                 // waves per workgroup
+  constexpr int CK = 32;                     // keys per staged chunk
+  constexpr int NSC = CK / 32;               // 32-key sub-chunks per chunk
+  constexpr int NCK = S / CK;                // chunks per block
+  constexpr int CT = CK * G::RB;             // bytes of one chunk tile (K or V)
+  constexpr int NUW = CT / 1024 / NW;        // direct-load pieces per wave per tile
+  static_assert(NUW >= 1 && (NUW % 2 == 0 || G::RPI == 8), "piece parity");
+
+  __shared__ __attribute__((aligned(1024))) unsigned char Ks[2][CT];
+  __shared__ __attribute__((aligned(1024))) unsigned char Vs[2][CT];
+  __shared__ int wg_bad;
+
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int hf = lane >> 5;
+  const int l32 = lane & 31;
+  const int g16 = lane >> 4;
+  const int n16 = lane & 15;
+  const int N = a.N, nB = a.nB;
+  const float sl2 = a.scale_log2;
+
+  const int row = __builtin_amdgcn_readfirstlane(xcd_remap(blockIdx.x, a.n_rows));  // (b*H + h)*nB + i
+  const int bh = row / nB;
+  const int i = row - bh * nB;
+  const size_t head = (size_t)bh * N * D;
+  const uint16_t* Qh = a.q + head;
+  const uint16_t* Kh = a.k + head;
+  const uint16_t* Vh = a.v + head;
+
+  // ---- Q^T operand: query i*S + w*32 + l32, d = s*16 + hf*8 + 0..7 ----
+  const int qr = i * S + w * 32 + l32;
+  bf16x8 qop[G::DQ];
+#pragma unroll
+  for (int s = 0; s < G::DQ; ++s) {
+    if (qr < N) qop[s] = *reinterpret_cast<const bf16x8*>(Qh + (size_t)qr * D + s * 16 + hf * 8);
+    else qop[s] = bf16x8{};
+  }
+
+  // index list through the constant address space: uniform reads become
+  // scalar loads (lgkmcnt), so they never wait on the in-flight tile loads
+  int count;
+  const_i32* idxrow = nullptr;
+  if constexpr (SPARSE) {
+    count = __builtin_amdgcn_readfirstlane(min(max(((const_i32*)a.kv_count)[row], 0), a.kmax));
+    idxrow = (const_i32*)a.kv_idx + (size_t)row * a.kmax;
+  } else {
+    count = nB;
+  }
+  auto block_at = [&](int it) -> int {
+    return __builtin_amdgcn_readfirstlane(SPARSE ? idxrow[it] : it);
+  };
+  auto next_valid = [&](int it) -> int {
+    while (it < count) {
+      const int j = block_at(it);
+      if (j >= 0 && j < nB) break;
+      ++it;
+    }
+    return it;
+  };
+  // position in the flattened (kept block, chunk) sequence; chunks wholly past
+  // the end of the sequence are skipped
+  struct Pos { int it, ch, key0; };
+  auto make = [&](int it, int ch) -> Pos {
+    return Pos{it, ch, it < count ? block_at(it) * S + ch * CK : 0};
+  };
+  auto advance = [&](const Pos& p) -> Pos {
+    if (p.ch + 1 < NCK && p.key0 + CK < N) return make(p.it, p.ch + 1);
+    return make(next_valid(p.it + 1), 0);
+  };
+
+  // ---- direct global -> LDS fetch of one chunk (this wave's 1 KB pieces) ----
+  // Piece u covers chunk rows u*RPI .. u*RPI + RPI - 1; lane L fills row
+  // u*RPI + L/NCH at position L % NCH, i.e. global piece (L % NCH) ^ swizzle(row).
+  // (row & 7) depends on u only through its parity (RPI = 4) or not at all
+  // (RPI = 8), so two per-lane byte offsets per tensor serve every full chunk;
+  // the uniform part is the scalar offset.  Every address formed lies inside
+  // the head's rows (full chunks by construction, the last by clamping).
+  const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc((void*)Kh, (short)0, N * D * 2, 0x00020000);
+  const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc((void*)Vh, (short)0, N * D * 2, 0x00020000);
+  int kgo[2], vgo[2];
+  {
+    const int p = lane % G::NCH;
+    const int rl = lane / G::NCH;
+#pragma unroll
+    for (int par = 0; par < 2; ++par) {
+      const int r = par * G::RPI + rl;
+      int ck = swz_k(r, p), cv = swz_v<G::NCH>(r, p);   // the swizzle is an involution
+      if (ck >= G::DCH) ck = 0;                          // padding pieces: any in-row address
+      if (cv >= G::DCH) cv = 0;
+      kgo[par] = (rl * D + ck * 8) * 2;
+      vgo[par] = (rl * D + cv * 8) * 2;
+    }
+  }
+  // LDS byte addresses of the tiles, computed once (M0 is then scalar adds)
+  typedef __attribute__((address_space(3))) unsigned char lds_u8;
+  const unsigned ks_base = __builtin_amdgcn_readfirstlane((unsigned)(size_t)(lds_u8*)&Ks[0][0]);
+  const unsigned vs_base = __builtin_amdgcn_readfirstlane((unsigned)(size_t)(lds_u8*)&Vs[0][0]);
+  auto bll = [&](const __amdgpu_buffer_rsrc_t& rs, unsigned lds_addr, int voff, int soff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_u8*)(size_t)__builtin_amdgcn_readfirstlane(lds_addr), 16,
+                                             voff, __builtin_amdgcn_readfirstlane(soff), 0, 0);
+  };
+  auto fetch = [&](int st, int key0) {
+    st = __builtin_amdgcn_readfirstlane(st);
+    key0 = __builtin_amdgcn_readfirstlane(key0);
+    const int base = key0 * D * 2;
+    const int valid = N - key0;
+    if (valid >= CK) {
+#pragma unroll
+      for (int v = 0; v < NUW; ++v) {
+        const int u = w * NUW + v;
+        bll(krs, ks_base + st * CT + u * 1024, kgo[u & 1], base + u * G::RPI * D * 2);
+        bll(vrs, vs_base + st * CT + u * 1024, vgo[u & 1], base + u * G::RPI * D * 2);
+      }
+    } else {
+      // last, partial chunk: rows past the sequence read row 0 of the chunk
+      // (finite data; those keys are masked out of the softmax).  The lane id
+      // goes through an empty asm so this rare path's per-lane values are
+      // recomputed here rather than hoisted (and kept live) across the loop.
+      int ln = lane;
+      asm volatile("" : "+v"(ln));
+      const int p = ln % G::NCH;
+#pragma unroll
+      for (int v = 0; v < NUW; ++v) {
+        const int u = w * NUW + v;
+        const int r = u * G::RPI + ln / G::NCH;
+        const int rs = r < valid ? r : 0;
+        int ck = swz_k(r, p), cv = swz_v<G::NCH>(r, p);
+        if (ck >= G::DCH) ck = 0;
+        if (cv >= G::DCH) cv = 0;
+        bll(krs, ks_base + st * CT + u * 1024, (rs * D + ck * 8) * 2, base);
+        bll(vrs, vs_base + st * CT + u * 1024, (rs * D + cv * 8) * 2, base);
+      }
+    }
+  };
+
+  // Per-lane LDS offsets.  K operand, step s: row (sc*32 + l32), piece 2s + hf
+  // at position (2s + hf) ^ (l32 & 7); positions of steps s and s + 4 differ by
+  // exactly 8 pieces, so four offsets cover all steps and the rest is an
+  // immediate.  V transpose reads: row (sc*32 + kk*16 + hf*4 + n16/4 [+8]),
+  // piece dt*4 + (g16&1)*2 + (n16&3)/2; only dt interacts with the swizzle.
+  int koff[4];
+#pragma unroll
+  for (int s = 0; s < 4; ++s) koff[s] = l32 * G::RB + (swz_k(l32, 2 * s + hf) << 4);
+  int voff[G::DT];
+  {
+    const int vr = hf * 4 + (n16 >> 2);
+#pragma unroll
+    for (int dt = 0; dt < G::DT; ++dt) {
+      const int c = dt * 4 + (g16 & 1) * 2 + ((n16 & 3) >> 1);
+      voff[dt] = vr * G::RB + (swz_v<G::NCH>(vr, c) << 4) + (n16 & 1) * 8;
+    }
+  }
+
+  float m_ref = 0.0f;        // reference max (log2 units), fixed by the first chunk
+  float l_part = 0.0f;       // this lane's half of the row sum
+  f32x16 oacc[G::DT];
+#pragma unroll
+  for (int dt = 0; dt < G::DT; ++dt) oacc[dt] = f32x16{};
+
+  auto qk = [&](f32x16& sacc, const unsigned char* kt, int sc) {
+    sacc = f32x16{};
+#pragma unroll
+    for (int s = 0; s < G::DQ; ++s) {
+      const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kt + koff[s & 3] + (s >> 2) * 128 + sc * 32 * G::RB);
+      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[s], sacc, 0, 0, 0);
+    }
+  };
+  auto mask_tail = [&](f32x16& sacc, int sc, int valid) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int key = sc * 32 + (r >> 2) * 8 + hf * 4 + (r & 3);
+      if (key >= valid) sacc[r] = -INFINITY;
+    }
+  };
+  auto softmax = [&](const f32x16& sacc, bf16x8 (&pop)[2]) {
+    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+    float lsum = l_part;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      u32x4 wv;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kk * 8 + 2 * e], sl2, -m_ref));
+        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kk * 8 + 2 * e + 1], sl2, -m_ref));
+        const bf16x2 pb = cvt2(p0, p1);
+        lsum = __builtin_amdgcn_fdot2_f32_bf16(pb, ones, lsum, false);
+        wv[e] = __builtin_bit_cast(unsigned, pb);
+      }
+      pop[kk] = __builtin_bit_cast(bf16x8, wv);
+    }
+    l_part = lsum;
+  };
+  auto pv = [&](const bf16x8 (&pop)[2], const unsigned char* vt, int sc) {
+#pragma unroll
+    for (int dt = 0; dt < G::DT; ++dt) {
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        // rows r and r + 8 share (r & 7), hence the swizzle
+        const unsigned char* p = vt + voff[dt] + (sc * 32 + kk * 16) * G::RB;
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p));
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 8 * G::RB));
+        const u32x2 lw = __builtin_bit_cast(u32x2, lo);
+        const u32x2 hw = __builtin_bit_cast(u32x2, hi);
+        const u32x4 vw = {lw[0], lw[1], hw[0], hw[1]};
+        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vw), pop[kk], oacc[dt], 0, 0, 0);
+      }
+    }
+  };
+
+  // One body for every chunk: the tail mask and the reference maximum are
+  // small uniform branches that touch only S and m, never O, so the O
+  // registers carry through the loop without copies.
+  auto chunk = [&](const unsigned char* kt, const unsigned char* vt, int valid, bool first) {
+    f32x16 sacc[NSC];
+    bf16x8 pop[NSC][2];
+#pragma unroll
+    for (int sc = 0; sc < NSC; ++sc) qk(sacc[sc], kt, sc);
+    if (valid < CK) {
+      asm volatile("");          // keep this a real (rarely taken) branch, not select code
+#pragma unroll
+      for (int sc = 0; sc < NSC; ++sc) mask_tail(sacc[sc], sc, valid);
+    }
+    if (first) {
+      // the first chunk holds at least one valid key, so the maximum is finite
+      float mx = sacc[0][0];
+#pragma unroll
+      for (int sc = 0; sc < NSC; ++sc)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[sc][r]);
+      m_ref = swap_halves_max(mx) * sl2;
+    }
+#pragma unroll
+    for (int sc = 0; sc < NSC; ++sc) {
+      softmax(sacc[sc], pop[sc]);
+      pv(pop[sc], vt, sc);
+    }
+  };
+
+  Pos cur = make(next_valid(0), 0);
+  if (cur.it < count) fetch(0, cur.key0);
+  int st = 0;
+  bool first = true;
+  while (cur.it < count) {
+    const Pos nxt = advance(cur);
+    const bool more = nxt.it < count;
+    if (more) {
+      fetch(st ^ 1, nxt.key0);   // that stage was released by the last iteration's barrier
+      wait_vmcnt<2 * NUW>();     // this chunk landed; the next one may still be in flight
+    } else {
+      wait_vmcnt<0>();
+    }
+    wg_barrier();
+    st = __builtin_amdgcn_readfirstlane(st);
+    const int valid = __builtin_amdgcn_readfirstlane(N - cur.key0);
+    chunk(Ks[st], Vs[st], valid, first);
+    first = false;
+    wg_barrier();                // every wave is done with this stage
+    st ^= 1;
+    cur = nxt;
+  }
+
+  // ---- epilogue: overflow check, then O = O^T / l and LSE ----
+  if (threadIdx.x == 0) wg_bad = 0;
+  const float l_tot = swap_halves_sum(l_part);
+  bool bad = !(l_tot < 0x1p100f);
+#pragma unroll
+  for (int dt = 0; dt < G::DT; ++dt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) bad |= !__builtin_isfinite(oacc[dt][r]);
+  __syncthreads();
+  if (__builtin_amdgcn_ballot_w64(bad) != 0 && lane == 0) atomicOr(&wg_bad, 1);
+  __syncthreads();
+  if (wg_bad) {
+    if (threadIdx.x == 0 && i * S < N) {
+      if constexpr (OUT_F32) static_cast<float*>(a.out)[head + (size_t)i * S * D] = __builtin_nanf("");
+      else static_cast<uint16_t*>(a.out)[head + (size_t)i * S * D] = 0x7FC0;
+    }
+    return;
+  }
+  const bool has = count > 0 && l_tot > 0.0f;
+  const float inv = has ? 1.0f / l_tot : 0.0f;
+  if (qr < N) {
+    const size_t obase = head + (size_t)qr * D;
+#pragma unroll
+    for (int dt = 0; dt < G::DT; ++dt)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int d = dt * 32 + r4 * 8 + hf * 4;
+        if (d < D) {
+          const float o0 = oacc[dt][r4 * 4 + 0] * inv, o1 = oacc[dt][r4 * 4 + 1] * inv;
+          const float o2 = oacc[dt][r4 * 4 + 2] * inv, o3 = oacc[dt][r4 * 4 + 3] * inv;
+          if constexpr (OUT_F32) {
+            *reinterpret_cast<float4*>(static_cast<float*>(a.out) + obase + d) = make_float4(o0, o1, o2, o3);
+          } else {
+            const bf16x2 x = cvt2(o0, o1), y = cvt2(o2, o3);
+            const bf16x4 o = {x[0], x[1], y[0], y[1]};
+            *reinterpret_cast<bf16x4*>(static_cast<uint16_t*>(a.out) + obase + d) = o;
+          }
+        }
+      }
+    if (a.lse && hf == 0) {
+      a.lse[(size_t)bh * N + qr] = has ? (m_ref + __log2f(l_tot)) * 0.69314718055994530942f : -INFINITY;
+    }
+  }
+}
+
+template <int D, int S>
+hipError_t launch_q32(const Dims& d, bool sparse, const AttnArgs& a, hipStream_t stream) {
+  dim3 grid(a.n_rows), block(2 * S);
+  if (sparse) {
+    if (d.out_f32) hipLaunchKernelGGL((attn_q32_kernel<D, S, true, true>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((attn_q32_kernel<D, S, true, false>), grid, block, 0, stream, a);
+  } else {
+    if (d.out_f32) hipLaunchKernelGGL((attn_q32_kernel<D, S, false, true>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((attn_q32_kernel<D, S, false, false>), grid, block, 0, stream, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attention_q32(const Dims& d, bool sparse, const AttnArgs& a, hipStream_t stream) {
+  switch (d.D * 1000 + d.S) {
+    case 64128: return launch_q32<64, 128>(d, sparse, a, stream);
+    case 112128: return launch_q32<112, 128>(d, sparse, a, stream);
+    case 128128: return launch_q32<128, 128>(d, sparse, a, stream);
+    case 64064: return launch_q32<64, 64>(d, sparse, a, stream);
+    case 112064: return launch_q32<112, 64>(d, sparse, a, stream);
+    case 128064: return launch_q32<128, 64>(d, sparse, a, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace sva

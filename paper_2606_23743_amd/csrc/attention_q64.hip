@@ -32,66 +32,12 @@
 // chunk c+1, PV of chunk c-1) so the scheduler can overlap VALU and MFMA.
 #include <type_traits>
 
-#include "sva_internal.h"
+#include "attn_common.h"
 
 namespace sva {
 namespace {
 
-typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
-typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
-typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
-typedef __attribute__((ext_vector_type(16))) float f32x16;
-typedef __attribute__((ext_vector_type(2))) float f32x2;
-typedef __attribute__((ext_vector_type(4))) short i16x4;
-typedef __attribute__((ext_vector_type(2))) unsigned u32x2;
-typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-typedef __attribute__((address_space(4))) const int32_t const_i32;
-
-
-template <int D>
-struct Geo {
-  static constexpr int RB = (D > 64) ? 256 : 128;   // LDS row pitch, bytes
-  static constexpr int NCH = RB / 16;               // 16-byte chunks per LDS row
-  static constexpr int DCH = D / 8;                 // chunks that hold data
-  static constexpr int RPI = 1024 / RB;             // rows per 1 KB direct load
-  static constexpr int DQ = D / 16;                 // k-steps of QK^T
-  static constexpr int DP = (D + 31) / 32 * 32;     // head dim padded to PV tiles
-  static constexpr int DT = DP / 32;                // 32-row d tiles of O^T
-};
-
-__device__ __forceinline__ int swz_k(int r, int c) { return c ^ (r & 7); }
-template <int NCH>
-__device__ __forceinline__ int swz_v(int r, int c) { return c ^ ((2 * (r & 7)) & (NCH - 1)); }
-
-__device__ __forceinline__ bf16x2 cvt2(float a, float b) {
-  f32x2 f = {a, b};
-  return __builtin_convertvector(f, bf16x2);
-}
-
-__device__ __forceinline__ float swap_halves_max(float x) {
-  const u32x2 r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-
-__device__ __forceinline__ float swap_halves_sum(float x) {
-  const u32x2 r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-
-// s_waitcnt vmcnt(n) leaving the other counters alone (gfx9 encoding).
-template <int n>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(n >= 0 && n < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14));
-  asm volatile("" ::: "memory");
-}
-
-// Workgroup barrier without the release/acquire fences of __syncthreads (which
-// would wait for every in-flight direct load); LDS visibility is handled by the
-// explicit vmcnt waits and by MFMAs having consumed their LDS operands.
-__device__ __forceinline__ void wg_barrier() {
-  asm volatile("s_barrier" ::: "memory");
-}
+using namespace attn;
 
 template <int D, int S, bool SPARSE, bool OUT_F32>
 __global__ __launch_bounds__(S) __attribute__((amdgpu_waves_per_eu(1, 1)))
@@ -314,17 +260,18 @@ void attn_q64_kernel(AttnArgs a) {
       float lsum = l_part[t];
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
-        bf16x8 pv;
+        // the operand is built as four packed dwords so each v_cvt_pk_bf16_f32
+        // can write its final register directly
+        u32x4 w;
 #pragma unroll
-        for (int e = 0; e < 8; e += 2) {
-          const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[t][kk * 8 + e], sl2, -m_ref[t]));
-          const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[t][kk * 8 + e + 1], sl2, -m_ref[t]));
+        for (int e = 0; e < 4; ++e) {
+          const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[t][kk * 8 + 2 * e], sl2, -m_ref[t]));
+          const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[t][kk * 8 + 2 * e + 1], sl2, -m_ref[t]));
           const bf16x2 pb = cvt2(p0, p1);
           lsum = __builtin_amdgcn_fdot2_f32_bf16(pb, ones, lsum, false);
-          pv[e] = pb[0];
-          pv[e + 1] = pb[1];
+          w[e] = __builtin_bit_cast(unsigned, pb);
         }
-        pop[t][kk] = pv;
+        pop[t][kk] = __builtin_bit_cast(bf16x8, w);
       }
       l_part[t] = lsum;
     }
@@ -340,9 +287,10 @@ void attn_q64_kernel(AttnArgs a) {
         const unsigned char* p = vt + voff[dt] + (sc * 32 + kk * 16) * G::RB;
         const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p));
         const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 8 * G::RB));
-        const bf16x4 lb = __builtin_bit_cast(bf16x4, lo);
-        const bf16x4 hb4 = __builtin_bit_cast(bf16x4, hi);
-        const bf16x8 vop = {lb[0], lb[1], lb[2], lb[3], hb4[0], hb4[1], hb4[2], hb4[3]};
+        const u32x2 lw = __builtin_bit_cast(u32x2, lo);
+        const u32x2 hw = __builtin_bit_cast(u32x2, hi);
+        const u32x4 vw = {lw[0], lw[1], hw[0], hw[1]};
+        const bf16x8 vop = __builtin_bit_cast(bf16x8, vw);
 #pragma unroll
         for (int t = 0; t < 2; ++t)
           oacc[t][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pop[t][kk], oacc[t][dt], 0, 0, 0);
@@ -402,6 +350,17 @@ void attn_q64_kernel(AttnArgs a) {
   // rescaling kernel that runs next on the same stream.
   __shared__ int wg_bad;
   if (threadIdx.x == 0) wg_bad = 0;
+  // O is read out of the accumulation registers (AGPRs) explicitly: with every
+  // use of O being an MFMA or this read, O stays in AGPRs for the whole loop
+  // instead of being copied in and out around each PV step.
+  float ov[2][G::DT][16];
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int dt = 0; dt < G::DT; ++dt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(ov[t][dt][r]) : "a"(oacc[t][dt][r]));
   float l_tot[2];
   bool bad = false;
 #pragma unroll
@@ -411,7 +370,7 @@ void attn_q64_kernel(AttnArgs a) {
 #pragma unroll
     for (int dt = 0; dt < G::DT; ++dt)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) bad |= !__builtin_isfinite(oacc[t][dt][r]);
+      for (int r = 0; r < 16; ++r) bad |= !__builtin_isfinite(ov[t][dt][r]);
   }
   __syncthreads();
   if (__builtin_amdgcn_ballot_w64(bad) != 0 && lane == 0) atomicOr(&wg_bad, 1);
@@ -436,8 +395,8 @@ void attn_q64_kernel(AttnArgs a) {
         for (int r4 = 0; r4 < 4; ++r4) {
           const int d = dt * 32 + r4 * 8 + hf * 4;
           if (d < D) {
-            const float o0 = oacc[t][dt][r4 * 4 + 0] * inv, o1 = oacc[t][dt][r4 * 4 + 1] * inv;
-            const float o2 = oacc[t][dt][r4 * 4 + 2] * inv, o3 = oacc[t][dt][r4 * 4 + 3] * inv;
+            const float o0 = ov[t][dt][r4 * 4 + 0] * inv, o1 = ov[t][dt][r4 * 4 + 1] * inv;
+            const float o2 = ov[t][dt][r4 * 4 + 2] * inv, o3 = ov[t][dt][r4 * 4 + 3] * inv;
             if constexpr (OUT_F32) {
               *reinterpret_cast<float4*>(static_cast<float*>(a.out) + obase + d) = make_float4(o0, o1, o2, o3);
             } else {

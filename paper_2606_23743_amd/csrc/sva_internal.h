@@ -43,6 +43,9 @@ hipError_t launch_attention_rescaling(const Dims& d, bool sparse, const AttnArgs
 
 // 64-queries-per-wave attention with a fixed reference max; attention_q64.hip.
 hipError_t launch_attention_q64(const Dims& d, bool sparse, const AttnArgs& a, hipStream_t stream);
+// 32-queries-per-wave, two-waves-per-SIMD attention with a fixed reference max;
+// attention_q32.hip.
+hipError_t launch_attention_q32(const Dims& d, bool sparse, const AttnArgs& a, hipStream_t stream);
 
 hipError_t launch_pool(const Dims& d, const uint16_t* q, const uint16_t* k, float* q_pool,
                        float* k_pool, hipStream_t stream);
