@@ -37,18 +37,19 @@ void attn_q32_kernel(AttnArgs a) {
   using G = Geo<D>;
   constexpr int NW = S / 32;                 // waves per workgroup
   constexpr int CK = 32;                     // keys per staged chunk
-  constexpr int NSC = CK / 32;               // 32-key sub-chunks per chunk
   constexpr int NCK = S / CK;                // chunks per block
+  constexpr int NST = NCK;                   // LDS stages: chunk c of a block in stage c
+  constexpr int PD = NST - 1;                // prefetch distance, in chunks
   constexpr int CT = CK * G::RB;             // bytes of one chunk tile (K or V)
   constexpr int NUW = CT / 1024 / NW;        // direct-load pieces per wave per tile
-  static_assert(NUW >= 1 && (NUW % 2 == 0 || G::RPI == 8), "piece parity");
+  static_assert(NUW >= 1 && PD >= 1, "tile split");
 
-  __shared__ __attribute__((aligned(1024))) unsigned char Ks[2][CT];
-  __shared__ __attribute__((aligned(1024))) unsigned char Vs[2][CT];
+  __shared__ __attribute__((aligned(1024))) unsigned char Ks[NST][CT];
+  __shared__ __attribute__((aligned(1024))) unsigned char Vs[NST][CT];
   __shared__ int wg_bad;
 
   const int lane = threadIdx.x & 63;
-  const int w = threadIdx.x >> 6;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int hf = lane >> 5;
   const int l32 = lane & 31;
   const int g16 = lane >> 4;
@@ -73,8 +74,9 @@ void attn_q32_kernel(AttnArgs a) {
     else qop[s] = bf16x8{};
   }
 
-  // index list through the constant address space: uniform reads become
-  // scalar loads (lgkmcnt), so they never wait on the in-flight tile loads
+  // ---- the kept-block list ----
+  // Read through the constant address space: uniform reads become scalar
+  // loads (lgkmcnt), so they never wait on the in-flight tile loads.
   int count;
   const_i32* idxrow = nullptr;
   if constexpr (SPARSE) {
@@ -83,52 +85,37 @@ void attn_q32_kernel(AttnArgs a) {
   } else {
     count = nB;
   }
-  auto block_at = [&](int it) -> int {
+  auto raw_at = [&](int it) -> int {
     return __builtin_amdgcn_readfirstlane(SPARSE ? idxrow[it] : it);
   };
-  auto next_valid = [&](int it) -> int {
-    while (it < count) {
-      const int j = block_at(it);
-      if (j >= 0 && j < nB) break;
-      ++it;
-    }
+  auto in_range = [&](int j) -> bool { return j >= 0 && j < nB; };
+  auto seek = [&](int it) -> int {         // first usable entry at or after it
+    while (it < count && !in_range(raw_at(it))) ++it;
     return it;
-  };
-  // position in the flattened (kept block, chunk) sequence; chunks wholly past
-  // the end of the sequence are skipped
-  struct Pos { int it, ch, key0; };
-  auto make = [&](int it, int ch) -> Pos {
-    return Pos{it, ch, it < count ? block_at(it) * S + ch * CK : 0};
-  };
-  auto advance = [&](const Pos& p) -> Pos {
-    if (p.ch + 1 < NCK && p.key0 + CK < N) return make(p.it, p.ch + 1);
-    return make(next_valid(p.it + 1), 0);
   };
 
   // ---- direct global -> LDS fetch of one chunk (this wave's 1 KB pieces) ----
   // Piece u covers chunk rows u*RPI .. u*RPI + RPI - 1; lane L fills row
   // u*RPI + L/NCH at position L % NCH, i.e. global piece (L % NCH) ^ swizzle(row).
-  // (row & 7) depends on u only through its parity (RPI = 4) or not at all
-  // (RPI = 8), so two per-lane byte offsets per tensor serve every full chunk;
-  // the uniform part is the scalar offset.  Every address formed lies inside
-  // the head's rows (full chunks by construction, the last by clamping).
+  // A wave always loads the same pieces, so its per-lane byte offsets are
+  // fixed and the chunk's key offset is the scalar offset.  Every address
+  // formed lies inside the head's rows: full chunks by construction, the
+  // sequence's last partial chunk by clamping rows past the end to its first
+  // row, and a chunk wholly past the end (the rest of a partial block, or a
+  // pipeline slot with nothing left to load) by reading chunk 0 instead.
   const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc((void*)Kh, (short)0, N * D * 2, 0x00020000);
   const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc((void*)Vh, (short)0, N * D * 2, 0x00020000);
-  int kgo[2], vgo[2];
-  {
-    const int p = lane % G::NCH;
-    const int rl = lane / G::NCH;
+  int kgv[NUW], vgv[NUW];
 #pragma unroll
-    for (int par = 0; par < 2; ++par) {
-      const int r = par * G::RPI + rl;
-      int ck = swz_k(r, p), cv = swz_v<G::NCH>(r, p);   // the swizzle is an involution
-      if (ck >= G::DCH) ck = 0;                          // padding pieces: any in-row address
-      if (cv >= G::DCH) cv = 0;
-      kgo[par] = (rl * D + ck * 8) * 2;
-      vgo[par] = (rl * D + cv * 8) * 2;
-    }
+  for (int v = 0; v < NUW; ++v) {
+    const int r = (w * NUW + v) * G::RPI + lane / G::NCH;
+    const int p = lane % G::NCH;
+    int ck = swz_k<G::NCH>(r, p), cv = swz_v<G::NCH>(r, p);
+    if (ck >= G::DCH) ck = 0;                        // padding pieces: any in-row address
+    if (cv >= G::DCH) cv = 0;
+    kgv[v] = (r * D + ck * 8) * 2;
+    vgv[v] = (r * D + cv * 8) * 2;
   }
-  // LDS byte addresses of the tiles, computed once (M0 is then scalar adds)
   typedef __attribute__((address_space(3))) unsigned char lds_u8;
   const unsigned ks_base = __builtin_amdgcn_readfirstlane((unsigned)(size_t)(lds_u8*)&Ks[0][0]);
   const unsigned vs_base = __builtin_amdgcn_readfirstlane((unsigned)(size_t)(lds_u8*)&Vs[0][0]);
@@ -137,22 +124,19 @@ void attn_q32_kernel(AttnArgs a) {
                                              voff, __builtin_amdgcn_readfirstlane(soff), 0, 0);
   };
   auto fetch = [&](int st, int key0) {
-    st = __builtin_amdgcn_readfirstlane(st);
     key0 = __builtin_amdgcn_readfirstlane(key0);
-    const int base = key0 * D * 2;
-    const int valid = N - key0;
-    if (valid >= CK) {
+    if (key0 + CK <= N) {
 #pragma unroll
       for (int v = 0; v < NUW; ++v) {
         const int u = w * NUW + v;
-        bll(krs, ks_base + st * CT + u * 1024, kgo[u & 1], base + u * G::RPI * D * 2);
-        bll(vrs, vs_base + st * CT + u * 1024, vgo[u & 1], base + u * G::RPI * D * 2);
+        bll(krs, ks_base + st * CT + u * 1024, kgv[v], key0 * D * 2);
+        bll(vrs, vs_base + st * CT + u * 1024, vgv[v], key0 * D * 2);
       }
     } else {
-      // last, partial chunk: rows past the sequence read row 0 of the chunk
-      // (finite data; those keys are masked out of the softmax).  The lane id
-      // goes through an empty asm so this rare path's per-lane values are
-      // recomputed here rather than hoisted (and kept live) across the loop.
+      // The lane id goes through an empty asm so this rare path's per-lane
+      // values are recomputed here rather than hoisted and kept live.
+      if (key0 >= N) key0 = 0;
+      const int valid = N - key0;
       int ln = lane;
       asm volatile("" : "+v"(ln));
       const int p = ln % G::NCH;
@@ -161,23 +145,22 @@ void attn_q32_kernel(AttnArgs a) {
         const int u = w * NUW + v;
         const int r = u * G::RPI + ln / G::NCH;
         const int rs = r < valid ? r : 0;
-        int ck = swz_k(r, p), cv = swz_v<G::NCH>(r, p);
+        int ck = swz_k<G::NCH>(r, p), cv = swz_v<G::NCH>(r, p);
         if (ck >= G::DCH) ck = 0;
         if (cv >= G::DCH) cv = 0;
-        bll(krs, ks_base + st * CT + u * 1024, (rs * D + ck * 8) * 2, base);
-        bll(vrs, vs_base + st * CT + u * 1024, (rs * D + cv * 8) * 2, base);
+        bll(krs, ks_base + st * CT + u * 1024, (rs * D + ck * 8) * 2, key0 * D * 2);
+        bll(vrs, vs_base + st * CT + u * 1024, (rs * D + cv * 8) * 2, key0 * D * 2);
       }
     }
   };
 
-  // Per-lane LDS offsets.  K operand, step s: row (sc*32 + l32), piece 2s + hf
-  // at position (2s + hf) ^ (l32 & 7); positions of steps s and s + 4 differ by
-  // exactly 8 pieces, so four offsets cover all steps and the rest is an
-  // immediate.  V transpose reads: row (sc*32 + kk*16 + hf*4 + n16/4 [+8]),
-  // piece dt*4 + (g16&1)*2 + (n16&3)/2; only dt interacts with the swizzle.
-  int koff[4];
+  // Per-lane LDS offsets.  K operand, step s: row l32 of the tile, piece
+  // 2s + hf.  V transpose reads: row (kk*16 + hf*4 + n16/4 [+8]), piece
+  // dt*4 + (g16&1)*2 + (n16&3)/2; only dt interacts with the swizzle.  The
+  // stage and the kk / +8 row offsets are immediates.
+  int koff[G::DQ];
 #pragma unroll
-  for (int s = 0; s < 4; ++s) koff[s] = l32 * G::RB + (swz_k(l32, 2 * s + hf) << 4);
+  for (int s = 0; s < G::DQ; ++s) koff[s] = l32 * G::RB + (swz_k<G::NCH>(l32, 2 * s + hf) << 4);
   int voff[G::DT];
   {
     const int vr = hf * 4 + (n16 >> 2);
@@ -194,18 +177,18 @@ void attn_q32_kernel(AttnArgs a) {
 #pragma unroll
   for (int dt = 0; dt < G::DT; ++dt) oacc[dt] = f32x16{};
 
-  auto qk = [&](f32x16& sacc, const unsigned char* kt, int sc) {
+  auto qk = [&](f32x16& sacc, const unsigned char* kt) {
     sacc = f32x16{};
 #pragma unroll
     for (int s = 0; s < G::DQ; ++s) {
-      const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kt + koff[s & 3] + (s >> 2) * 128 + sc * 32 * G::RB);
+      const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kt + koff[s]);
       sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[s], sacc, 0, 0, 0);
     }
   };
-  auto mask_tail = [&](f32x16& sacc, int sc, int valid) {
+  auto mask_tail = [&](f32x16& sacc, int valid) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int key = sc * 32 + (r >> 2) * 8 + hf * 4 + (r & 3);
+      const int key = (r >> 2) * 8 + hf * 4 + (r & 3);
       if (key >= valid) sacc[r] = -INFINITY;
     }
   };
@@ -227,13 +210,13 @@ void attn_q32_kernel(AttnArgs a) {
     }
     l_part = lsum;
   };
-  auto pv = [&](const bf16x8 (&pop)[2], const unsigned char* vt, int sc) {
+  auto pv = [&](const bf16x8 (&pop)[2], const unsigned char* vt) {
 #pragma unroll
     for (int dt = 0; dt < G::DT; ++dt) {
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
-        // rows r and r + 8 share (r & 7), hence the swizzle
-        const unsigned char* p = vt + voff[dt] + (sc * 32 + kk * 16) * G::RB;
+        // rows r and r + 8 have the same swizzle, so one offset serves both
+        const unsigned char* p = vt + voff[dt] + kk * 16 * G::RB;
         const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p));
         const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 8 * G::RB));
         const u32x2 lw = __builtin_bit_cast(u32x2, lo);
@@ -244,57 +227,74 @@ void attn_q32_kernel(AttnArgs a) {
     }
   };
 
-  // One body for every chunk: the tail mask and the reference maximum are
-  // small uniform branches that touch only S and m, never O, so the O
-  // registers carry through the loop without copies.
-  auto chunk = [&](const unsigned char* kt, const unsigned char* vt, int valid, bool first) {
-    f32x16 sacc[NSC];
-    bf16x8 pop[NSC][2];
-#pragma unroll
-    for (int sc = 0; sc < NSC; ++sc) qk(sacc[sc], kt, sc);
+  // One chunk: the tail mask and the reference maximum are small uniform
+  // branches that touch only S and m, never O, so the O registers carry
+  // through every copy of the body without moves.
+  auto chunk = [&](const unsigned char* kt, const unsigned char* vt, int key0, bool first) {
+    f32x16 sacc;
+    bf16x8 pop[2];
+    qk(sacc, kt);
+    const int valid = __builtin_amdgcn_readfirstlane(N - key0);
     if (valid < CK) {
       asm volatile("");          // keep this a real (rarely taken) branch, not select code
-#pragma unroll
-      for (int sc = 0; sc < NSC; ++sc) mask_tail(sacc[sc], sc, valid);
+      mask_tail(sacc, valid);
     }
     if (first) {
       // the first chunk holds at least one valid key, so the maximum is finite
-      float mx = sacc[0][0];
+      float mx = sacc[0];
 #pragma unroll
-      for (int sc = 0; sc < NSC; ++sc)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[sc][r]);
+      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[r]);
       m_ref = swap_halves_max(mx) * sl2;
     }
-#pragma unroll
-    for (int sc = 0; sc < NSC; ++sc) {
-      softmax(sacc[sc], pop[sc]);
-      pv(pop[sc], vt, sc);
-    }
+    softmax(sacc, pop);
+    pv(pop, vt);
   };
 
-  Pos cur = make(next_valid(0), 0);
-  if (cur.it < count) fetch(0, cur.key0);
-  int st = 0;
-  bool first = true;
-  while (cur.it < count) {
-    const Pos nxt = advance(cur);
-    const bool more = nxt.it < count;
-    if (more) {
-      fetch(st ^ 1, nxt.key0);   // that stage was released by the last iteration's barrier
-      wait_vmcnt<2 * NUW>();     // this chunk landed; the next one may still be in flight
-    } else {
-      wait_vmcnt<0>();
-    }
-    wg_barrier();
-    st = __builtin_amdgcn_readfirstlane(st);
-    const int valid = __builtin_amdgcn_readfirstlane(N - cur.key0);
-    chunk(Ks[st], Vs[st], valid, first);
-    first = false;
-    wg_barrier();                // every wave is done with this stage
-    st ^= 1;
-    cur = nxt;
+  // ---- pipeline over (kept block, chunk) ----
+  // Chunk c of every block lives in stage c (NST = NCK stages), so stages and
+  // LDS offsets are compile-time in the unrolled chunk loop.  At chunk c a
+  // wave waits for its own loads of that chunk and for its own LDS reads of
+  // chunk c-1 (the compiler may leave the last V reads in flight, their MFMAs
+  // sunk below the barrier); after the barrier every wave's loads have landed
+  // and every wave is done reading chunk c-1, so the loads of the chunk
+  // PD = NST-1 positions ahead go into chunk c-1's stage.  Each chunk issues
+  // exactly one load group (a dummy past the end of the list), so the wait
+  // count is a constant.  The block index after the next is read one block
+  // ahead, after chunk 0's barrier so that its scalar load has a whole chunk
+  // to land before the next LDS-idle wait.
+  int it = seek(0);
+  int j = it < count ? raw_at(it) : 0;
+  int itn = it < count ? seek(it + 1) : count;
+  int jn = itn < count ? raw_at(itn) : -1;
+  if (it < count) {
+#pragma unroll
+    for (int c = 0; c < PD; ++c) fetch(c, j * S + c * CK);
   }
+  bool first = true;
+  while (it < count) {
+    const int itnn = itn + 1;
+    int jnn = -1;
+#pragma unroll
+    for (int c = 0; c < NCK; ++c) {
+      wait_vmcnt_lds_idle<2 * NUW * (PD - 1)>();
+      wg_barrier();
+      if (c + PD < NCK) fetch((c + PD) % NST, j * S + (c + PD) * CK);
+      else fetch((c + PD) % NST, jn >= 0 ? jn * S + (c + PD - NCK) * CK : 0);
+      if (c == 0) jnn = itnn < count ? raw_at(itnn) : -1;
+      chunk(&Ks[c][0], &Vs[c][0], j * S + c * CK, c == 0 && first);
+    }
+    first = false;
+    it = itn;
+    j = jn;
+    if (itnn >= count || in_range(jnn)) {
+      itn = itnn;
+      jn = jnn;
+    } else {
+      itn = seek(itnn + 1);
+      jn = itn < count ? raw_at(itn) : -1;
+    }
+  }
+  wait_vmcnt<0>();           // no load may still target this workgroup's LDS
 
   // ---- epilogue: overflow check, then O = O^T / l and LSE ----
   if (threadIdx.x == 0) wg_bad = 0;

@@ -30,9 +30,21 @@ struct Geo {
   static constexpr int DT = DP / 32;                // 32-row d tiles of O^T
 };
 
-__device__ __forceinline__ int swz_k(int r, int c) { return c ^ (r & 7); }
+// LDS position of 16-byte piece c of tile row r.  LDS serves 256 bytes per
+// clock from 64 four-byte banks: a b128 read in groups of 16 consecutive lanes,
+// a b64 (transpose) read in groups of 32.  K operand reads put 16 consecutive
+// rows at one piece in a group, so the K swizzle spreads any 16 consecutive
+// rows over all 64 banks; V transpose reads put 4 consecutive rows x 4 pieces
+// in a group, so the V swizzle moves those 4 rows to disjoint 4-piece groups.
+// Both are XORs (involutions): the same function maps position to piece.
 template <int NCH>
-__device__ __forceinline__ int swz_v(int r, int c) { return c ^ ((2 * (r & 7)) & (NCH - 1)); }
+__device__ __forceinline__ int swz_k(int r, int c) {
+  return NCH == 16 ? c ^ (r & 15) : c ^ ((r >> 1) & 7);
+}
+template <int NCH>
+__device__ __forceinline__ int swz_v(int r, int c) {
+  return NCH == 16 ? c ^ (4 * (r & 3)) : c ^ (4 * ((r >> 1) & 1));
+}
 
 __device__ __forceinline__ bf16x2 cvt2(float a, float b) {
   f32x2 f = {a, b};
@@ -54,6 +66,16 @@ template <int n>
 __device__ __forceinline__ void wait_vmcnt() {
   static_assert(n >= 0 && n < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14));
+  asm volatile("" ::: "memory");
+}
+
+// s_waitcnt vmcnt(n) lgkmcnt(0): also every LDS read of this wave has returned
+// (and any scalar load), so a stage it was reading may be refilled once every
+// wave has passed the following barrier.
+template <int n>
+__device__ __forceinline__ void wait_vmcnt_lds_idle() {
+  static_assert(n >= 0 && n < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((n & 15) | (7 << 4) | (0 << 8) | ((n >> 4) << 14));
   asm volatile("" ::: "memory");
 }
 
