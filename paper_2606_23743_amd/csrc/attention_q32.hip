@@ -40,6 +40,7 @@ void attn_q32_kernel(AttnArgs a) {
   constexpr int NCK = S / CK;                // chunks per block
   constexpr int NST = NCK;                   // LDS stages: chunk c of a block in stage c
   constexpr int PD = NST - 1;                // prefetch distance, in chunks
+  constexpr bool PIPE = NST >= 4;            // S of chunk c+1 overlaps chunk c's softmax
   constexpr int CT = CK * G::RB;             // bytes of one chunk tile (K or V)
   constexpr int NUW = CT / 1024 / NW;        // direct-load pieces per wave per tile
   static_assert(NUW >= 1 && PD >= 1, "tile split");
@@ -270,20 +271,7 @@ void attn_q32_kernel(AttnArgs a) {
 #pragma unroll
     for (int c = 0; c < PD; ++c) fetch(c, j * S + c * CK);
   }
-  bool first = true;
-  while (it < count) {
-    const int itnn = itn + 1;
-    int jnn = -1;
-#pragma unroll
-    for (int c = 0; c < NCK; ++c) {
-      wait_vmcnt_lds_idle<2 * NUW * (PD - 1)>();
-      wg_barrier();
-      if (c + PD < NCK) fetch((c + PD) % NST, j * S + (c + PD) * CK);
-      else fetch((c + PD) % NST, jn >= 0 ? jn * S + (c + PD - NCK) * CK : 0);
-      if (c == 0) jnn = itnn < count ? raw_at(itnn) : -1;
-      chunk(&Ks[c][0], &Vs[c][0], j * S + c * CK, c == 0 && first);
-    }
-    first = false;
+  auto advance_block = [&](int itnn, int jnn) {
     it = itn;
     j = jn;
     if (itnn >= count || in_range(jnn)) {
@@ -292,6 +280,69 @@ void attn_q32_kernel(AttnArgs a) {
     } else {
       itn = seek(itnn + 1);
       jn = itn < count ? raw_at(itn) : -1;
+    }
+  };
+  if constexpr (PIPE) {
+    // Software pipeline inside the wave: the S MFMAs of the next chunk are
+    // issued alongside the softmax of this one, then this chunk's PV.  At
+    // iteration c the wave needs K of chunk c+1 and V of chunk c; after
+    // iteration c's barrier chunk c-1's stage is free (its K was read at
+    // iteration c-2, its V at c-1), and it receives chunk c+PD.  The last
+    // chunk of the list computes S for a dummy next chunk (stage 0 holds
+    // in-bounds data then), which is dropped.
+    f32x16 sacc = f32x16{};
+    if (it < count) {
+      wait_vmcnt<2 * NUW * (PD - 1)>();
+      wg_barrier();
+      qk(sacc, &Ks[0][0]);
+      const int valid = __builtin_amdgcn_readfirstlane(N - j * S);
+      if (valid < CK) mask_tail(sacc, valid);
+      float mx = sacc[0];                 // chunk 0 holds a valid key: finite
+#pragma unroll
+      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[r]);
+      m_ref = swap_halves_max(mx) * sl2;
+    }
+    while (it < count) {
+      const int itnn = itn + 1;
+      int jnn = -1;
+#pragma unroll
+      for (int c = 0; c < NCK; ++c) {
+        wait_vmcnt_lds_idle<2 * NUW * (PD - 2)>();     // chunk c+1 landed
+        wg_barrier();
+        if (c + PD < NCK) fetch((c + PD) % NST, j * S + (c + PD) * CK);
+        else fetch((c + PD) % NST, jn >= 0 ? jn * S + (c + PD - NCK) * CK : 0);
+        if (c == 0) jnn = itnn < count ? raw_at(itnn) : -1;
+        const int nkey0 = c + 1 < NCK ? j * S + (c + 1) * CK : (jn >= 0 ? jn * S : 0);
+        f32x16 snext;
+        bf16x8 pop[2];
+        qk(snext, &Ks[(c + 1) % NST][0]);
+        softmax(sacc, pop);
+        pv(pop, &Vs[c][0]);
+        const int nvalid = __builtin_amdgcn_readfirstlane(N - nkey0);
+        if (nvalid < CK) {
+          asm volatile("");        // keep this a real (rarely taken) branch, not select code
+          mask_tail(snext, nvalid);
+        }
+        sacc = snext;
+      }
+      advance_block(itnn, jnn);
+    }
+  } else {
+    bool first = true;
+    while (it < count) {
+      const int itnn = itn + 1;
+      int jnn = -1;
+#pragma unroll
+      for (int c = 0; c < NCK; ++c) {
+        wait_vmcnt_lds_idle<2 * NUW * (PD - 1)>();
+        wg_barrier();
+        if (c + PD < NCK) fetch((c + PD) % NST, j * S + (c + PD) * CK);
+        else fetch((c + PD) % NST, jn >= 0 ? jn * S + (c + PD - NCK) * CK : 0);
+        if (c == 0) jnn = itnn < count ? raw_at(itnn) : -1;
+        chunk(&Ks[c][0], &Vs[c][0], j * S + c * CK, c == 0 && first);
+      }
+      first = false;
+      advance_block(itnn, jnn);
     }
   }
   wait_vmcnt<0>();           // no load may still target this workgroup's LDS
