@@ -47,8 +47,9 @@ __device__ __forceinline__ bf16x2 cvt2(float a, float b) {
   return __builtin_convertvector(f, bf16x2);
 }
 
+// One query block (row = (b*H + h)*nB + i), computed by the whole workgroup.
 template <int D, int S, bool SPARSE, bool OUT_F32>
-__global__ __launch_bounds__(S * 2) void attn_kernel(AttnArgs a) {
+__device__ __forceinline__ void attn_row(const AttnArgs& a, const int row) {
   constexpr int NW = S / 32;             // waves per workgroup
   constexpr int NT = NW * 64;            // threads
   constexpr int DP = (D + 31) / 32 * 32; // head dim padded to the 32-wide PV tiles
@@ -71,17 +72,9 @@ __global__ __launch_bounds__(S * 2) void attn_kernel(AttnArgs a) {
   const int l32 = lane & 31;
   const int N = a.N, nB = a.nB;
 
-  const int row = xcd_remap(blockIdx.x, a.n_rows);   // (b*H + h)*nB + i
   const int bh = row / nB;
   const int i = row - bh * nB;
   const size_t head = (size_t)bh * N * D;
-  if (a.only_marked) {
-    // recompute only blocks the fixed-max kernel marked (NaN first element)
-    const size_t first = head + (size_t)i * S * D;
-    const bool marked = OUT_F32 ? __builtin_isnan(static_cast<const float*>(a.out)[first])
-                                : ((static_cast<const uint16_t*>(a.out)[first] & 0x7FFF) > 0x7F80);
-    if (!marked) return;
-  }
   const uint16_t* Qh = a.q + head;
   const uint16_t* Kh = a.k + head;
   const uint16_t* Vh = a.v + head;
@@ -279,15 +272,45 @@ __global__ __launch_bounds__(S * 2) void attn_kernel(AttnArgs a) {
   }
 }
 
+// Recomputes the query blocks the fixed-reference kernel marked (NaN first
+// output element).  A small grid scans the marks 64 rows at a time (one row
+// per lane, one ballot) and runs the per-block body only for marked rows, so
+// the common case (nothing marked) costs a few microseconds.
+template <int D, int S, bool SPARSE, bool OUT_F32>
+__global__ __launch_bounds__(S * 2) void attn_marked_kernel(AttnArgs a) {
+  const int lane = threadIdx.x & 63;
+  for (int base = blockIdx.x * 64; base < a.n_rows; base += gridDim.x * 64) {
+    const int r = base + lane;
+    bool marked = false;
+    if (r < a.n_rows) {
+      const int bh = r / a.nB;
+      const size_t first = (size_t)bh * a.N * D + (size_t)(r - bh * a.nB) * S * D;
+      marked = OUT_F32 ? __builtin_isnan(static_cast<const float*>(a.out)[first])
+                       : ((static_cast<const uint16_t*>(a.out)[first] & 0x7FFF) > 0x7F80);
+    }
+    uint64_t mask = __builtin_amdgcn_ballot_w64(marked);
+    // every wave holds the same mask before any marked row is rewritten, so
+    // all waves run the same rows (and barriers) below
+    __syncthreads();
+    while (mask != 0) {
+      const int b = __builtin_ctzll(mask);
+      mask &= mask - 1;
+      attn_row<D, S, SPARSE, OUT_F32>(a, base + b);
+      __syncthreads();                   // LDS tiles are reused by the next row
+    }
+  }
+}
+
 template <int D, int S>
 hipError_t launch_ds(const Dims& d, bool sparse, const AttnArgs& a, hipStream_t stream) {
-  dim3 grid(a.n_rows), block(S * 2);
+  const int groups = (a.n_rows + 63) / 64;
+  dim3 grid(groups < 2048 ? groups : 2048), block(S * 2);
   if (sparse) {
-    if (d.out_f32) hipLaunchKernelGGL((attn_kernel<D, S, true, true>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((attn_kernel<D, S, true, false>), grid, block, 0, stream, a);
+    if (d.out_f32) hipLaunchKernelGGL((attn_marked_kernel<D, S, true, true>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((attn_marked_kernel<D, S, true, false>), grid, block, 0, stream, a);
   } else {
-    if (d.out_f32) hipLaunchKernelGGL((attn_kernel<D, S, false, true>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((attn_kernel<D, S, false, false>), grid, block, 0, stream, a);
+    if (d.out_f32) hipLaunchKernelGGL((attn_marked_kernel<D, S, false, true>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((attn_marked_kernel<D, S, false, false>), grid, block, 0, stream, a);
   }
   return hipGetLastError();
 }
@@ -323,10 +346,8 @@ hipError_t launch_attention(const Dims& d, bool sparse, const uint16_t* q, const
   a.n_rows = d.B * d.H * d.nB;
   a.scale_log2 = (float)(d.scale * 1.4426950408889634);
   // fixed-reference-max kernel, then the rescaling kernel for any block it marked
-  a.only_marked = 0;
   hipError_t e = launch_attention_q32(d, sparse, a, stream);
   if (e != hipSuccess) return e;
-  a.only_marked = 1;
   return launch_attention_rescaling(d, sparse, a, stream);
 }
 

@@ -3,27 +3,29 @@
 // FlashAttention fallback).
 //
 // A workgroup is one query block of S tokens with S/32 waves of 32 queries.
-// Each wave's state (O^T 64 registers, Q^T 32, one key chunk of S^T and P)
-// fits in 256 registers, so two workgroups share a CU with two waves on every
-// SIMD: while one wave runs its MFMAs the other runs its softmax, which the
-// hardware overlaps without any in-wave software pipelining.
+// Each wave's state (O^T 64 registers, Q^T 32, S^T and P of a key chunk) fits
+// in 256 registers, so two workgroups share a CU with two waves on every SIMD.
 //
-// Keys are processed in 32-key chunks staged in LDS with two stages: the next chunk's K and V tiles are fetched with
-// buffer_load ... lds straight into the other stage while this one computes.
-// Tiles are unpadded and XOR-swizzled on 16-byte pieces (K: c ^ (row & 7),
-// conflict-free for the ds_read_b128 operand reads; V: c ^ 2(row & 7),
-// conflict-free for the ds_read_b64_tr_b16 transpose reads).
+// Keys are processed in 32-key chunks staged in LDS, chunk c of a kept block
+// in stage c (S/32 stages), filled by buffer_load ... lds straight from global
+// memory S/32 - 1 chunks ahead.  Tiles are unpadded and XOR-swizzled on
+// 16-byte pieces so that both the ds_read_b128 K operand reads and the
+// ds_read_b64_tr_b16 V transpose reads are free of bank conflicts.  With
+// S = 128 each wave also overlaps the next chunk's S^T MFMAs with the current
+// chunk's softmax.
 //
 // Per 32-key sub-chunk (lane = one query; its 16 S^T registers are keys
 // (r/4)*8 + half*4 + r%4):
 //   S^T = K Q^T                mfma_f32_32x32x16_bf16, Q^T in registers
-//   p   = exp2(c*log2e*s - m)  m is the reference maximum fixed from the first
-//                              chunk of the row, so O is never rescaled here
+//   p   = exp2(c*log2e*s - m)  m is the reference maximum taken from the first
+//                              chunk of the row, so O is not rescaled per chunk
 //   l  += sum of the bf16 p    v_dot2 with (1, 1)
 //   O^T += V^T P^T             P^T from the S^T registers, V^T by transpose reads
-// A row whose logits outgrow the first chunk's maximum by ~100 (log2 units)
-// could overflow: such query blocks are marked (NaN first element) and the
-// per-iteration rescaling kernel that runs next recomputes them.
+// After each kept block a row whose sum has passed 2^64 moves its reference up
+// by a power of two (O and l scaled exactly).  A row that still overflows (its
+// logits jump by more than ~2^63 over the running sum inside one block) is
+// marked (NaN first element) and recomputed by the per-iteration rescaling
+// kernel that runs next.
 #include "attn_common.h"
 
 namespace sva {
@@ -251,6 +253,28 @@ void attn_q32_kernel(AttnArgs a) {
     pv(pop, vt);
   };
 
+  // After every kept block: if a row sum has grown past 2^64 (the reference
+  // maximum was far below this row's logits), move the reference up by the
+  // sum's binary exponent and scale that query's O and l by the same power of
+  // two (exact).  p = exp2(s - m) can then only overflow if one block raises
+  // the logits by more than ~2^63 over the running sum; that rare case is
+  // caught by the final check.  Rows never come near 2^64 in practice, so this
+  // is one compare and a branch per block.
+  auto rescale_if_large = [&]() {
+    if (__builtin_amdgcn_ballot_w64(l_part > 0x1p64f) != 0) {
+      asm volatile("");
+      const float l_tot = swap_halves_sum(l_part);
+      const int e = l_tot > 0x1p64f ? __builtin_amdgcn_frexp_expf(l_tot) : 0;
+      const float f = __builtin_amdgcn_ldexpf(1.0f, -e);
+      l_part *= f;
+#pragma unroll
+      for (int dt = 0; dt < G::DT; ++dt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[dt][r] *= f;
+      m_ref += (float)e;
+    }
+  };
+
   // ---- pipeline over (kept block, chunk) ----
   // Chunk c of every block lives in stage c (NST = NCK stages), so stages and
   // LDS offsets are compile-time in the unrolled chunk loop.  At chunk c a
@@ -325,6 +349,7 @@ void attn_q32_kernel(AttnArgs a) {
         }
         sacc = snext;
       }
+      rescale_if_large();
       advance_block(itnn, jnn);
     }
   } else {
@@ -342,6 +367,7 @@ void attn_q32_kernel(AttnArgs a) {
         chunk(&Ks[c][0], &Vs[c][0], j * S + c * CK, c == 0 && first);
       }
       first = false;
+      rescale_if_large();
       advance_block(itnn, jnn);
     }
   }

@@ -34,8 +34,6 @@ struct AttnArgs {
   float* lse;
   int N, nB, kmax, n_rows;
   float scale_log2;   // c * log2(e)
-  int only_marked;    // rescaling kernel: recompute only query blocks whose first
-                      // output element holds the NaN mark of the fixed-max kernel
 };
 
 // The rescaling (per-iteration online softmax) kernel; attention.hip.

@@ -258,6 +258,46 @@ def test_select_ties_go_to_lower_index():
         assert want[2][:1] == [3]        # of the tied 3/9/12 the lowest index comes first
 
 
+@pytest.mark.parametrize("S,D", [(128, 128), (64, 128), (128, 112)])
+def test_gradual_logit_growth_is_exact(S, D):
+    """Logits rise by ~40 (log2 units) from one kept block to the next, so the
+    row sum relative to the first chunk's maximum passes 2^64 after a few
+    blocks and would reach ~2^127 by the last: the kernel must move its
+    reference between blocks and still match the oracle."""
+    B, H = 1, 1
+    nblk = 5
+    grid = (1, nblk * S // 16, 16)
+    wl = SC(f"growth_{S}_{D}", B, H, D, grid, S, "topk", topk=nblk, seed=37)
+    bits = inputs.generate(wl)
+    f = {n: inputs.bf16_bits_to_f32(bits[n]).copy() for n in ("q", "k", "v")}
+    c = scale_of(wl)
+    f["q"][0, 0] = 1.0
+    # key block b: every element equal, logits q.k * c = 40*b / log2(e)
+    for b in range(nblk):
+        val = 40.0 * b / (math.log2(math.e) * c * D) + 0.01
+        f["k"][0, 0, b * S:(b + 1) * S] = val + 0.02 * f["k"][0, 0, b * S:(b + 1) * S]
+    new_bits = {n: inputs._round_bf16(f[n]) for n in f}
+    dev = device_inputs(new_bits)
+    prob = sva.problem_for(wl)
+    rows = [list(range(nblk)) for _ in range(nblk)]
+    idx = np.array(rows, dtype=np.int32).reshape(1, 1, nblk, nblk)
+    cnt = np.full((1, 1, nblk), nblk, dtype=np.int32)
+    out, lse = sva.sparse_attention(prob, dev["q"], dev["k"], dev["v"], torch.from_numpy(idx).cuda(),
+                                    torch.from_numpy(cnt).cuda(), want_lse=True)
+    dout, dlse = sva.dense_attention(prob, dev["q"], dev["k"], dev["v"], want_lse=True)
+    torch.cuda.synchronize()
+    f64 = {n: oracle.bf16_bits_to_f64(new_bits[n]) for n in ("q", "k", "v")}
+    ref, rlse = oracle.block_sparse_attention(f64["q"], f64["k"], f64["v"], [[rows]], S, c)
+    assert rlse.max() > 100.0                      # the regime this test is about
+    for o_, l_ in ((out, lse), (dout, dlse)):
+        o = o_.float().cpu().numpy()
+        assert np.isfinite(o).all()
+        mx, mean = parity.attention_errors(o, ref, np.ones(ref.shape, dtype=bool))
+        assert mx <= parity.MAX_ABS and mean <= parity.MEAN_ABS, (mx, mean)
+        err = np.abs(l_.cpu().numpy() - rlse)
+        assert np.all(err <= parity.LSE_TOL + 1e-5 * np.abs(rlse)), err.max()
+
+
 @pytest.mark.parametrize("S,D", [(128, 128), (128, 112), (128, 64)])
 def test_logit_growth_beyond_fixed_reference_is_exact(S, D):
     """Block-size-128 kernels fix the softmax reference max from the first key
