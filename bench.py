@@ -10,7 +10,9 @@ is timed separately as the speedup denominator).  Prints one JSON line.
 value        kept-block attention FLOPs / step time (pool + select + attend)
 roofline     the sparse-attention kernel alone: kept FLOPs per launch / mean
              launch time (HIP events on the stream the kernel runs on),
-             against the bf16 dense MFMA peak
+             against the bf16 dense MFMA peak; traffic = HBM bytes per launch
+             from the committed rocprofv3 counter record while the kernel
+             sources still match it (else null)
 cpu_baseline the float64 oracle on a bounded sample of the same workload (one
              head's pooling and selection plus as many query blocks as fit the
              time budget), in the same unit
@@ -32,6 +34,30 @@ if ROOT not in sys.path:
 METRIC = "effective TFLOP/s of sparse attention (kept blocks) + % bf16 MFMA peak"
 BF16_PEAK_TFLOPS = 2516.6   # 256 CU x 2.4 GHz x 4096 dense bf16 flop/clk/CU
 HBM_PEAK_GBS = 8000.0
+
+
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "attention_traffic_large_64b.json")
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per sparse-attention launch from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE record, or None when the record is for another
+    workload or the kernel sources changed since it was taken."""
+    import hashlib
+    try:
+        with open(TRAFFIC_RECORD) as f:
+            rec = json.load(f)
+        if rec.get("workload") != workload:
+            return None
+        h = hashlib.sha256()
+        for rel in rec["sources"]:
+            with open(os.path.join(ROOT, rel), "rb") as f:
+                h.update(f.read())
+        if h.hexdigest() != rec["sources_sha256"]:
+            return None
+        return int(rec["hbm_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
 
 
 def kept_flops(idx: np.ndarray, cnt: np.ndarray, N: int, S: int, D: int):
@@ -243,7 +269,9 @@ def main(argv=None):
         "pct_of_bf16_peak": round(100.0 * value / BF16_PEAK_TFLOPS, 2),
         "roofline": {"bound": "mfma", "kernel": "sparse attention", "achieved": round(att_tflops, 2),
                      "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(att_tflops / BF16_PEAK_TFLOPS, 4), "traffic": None},
+                     "frac": round(att_tflops / BF16_PEAK_TFLOPS, 4),
+                     "traffic": measured_traffic(wl.name),
+                     "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, calibrated)"},
         "stages_ms": {"pool": round(pool_ms, 4), "select": round(sel_ms, 4), "attention": round(att_ms, 4)},
         "pool_hbm_gbs": round(pool_bytes / (pool_ms * 1e-3) / 1e9, 1),
         "cpu_baseline": cpu,
