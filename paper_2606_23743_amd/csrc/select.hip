@@ -301,6 +301,148 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Top-k with the scores in registers.  A workgroup (4 waves) takes R = 4*RW
+// query-block rows of one (b, h); each wave owns RW of them, and lane l holds
+// the float64 scores of blocks j = t*64 + l (t < NT) for each of its rows.
+// kbar is staged through LDS 64 blocks at a time (the next chunk is loaded
+// into registers while this one is used), so every kbar row is read once per
+// R query rows; each score is the same sequential float64 fma chain over d as
+// in select_kernel, so both give identical bits.
+// The k-th largest order key T is found bit by bit from the top: a candidate
+// bit stays set when at least k keys are >= the candidate (counted with one
+// ballot per register).  Keys above T are kept, and of the keys equal to T the
+// k - #above lowest block indices; the kept indices are written in ascending
+// order from ballots.
+template <int NT, int RW>
+__global__ __launch_bounds__(kThreads) void topk_kernel(SelectArgs a) {
+  constexpr int R = 4 * RW;
+  constexpr int KP = 132;            // kbar row pitch in LDS (floats): conflict-free b128 reads
+  constexpr int QP = 128;            // qbar row pitch in LDS (doubles)
+  __shared__ __attribute__((aligned(16))) double qs[R * QP];
+  __shared__ __attribute__((aligned(16))) float ks[64 * KP];
+
+  const int nB = a.nB, D = a.D;
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int work = xcd_remap(blockIdx.x, a.n_work);
+  const int bh = work / a.n_groups;
+  const int i0 = (work - bh * a.n_groups) * R;
+  const float* qsrc = a.q_pool + (size_t)bh * nB * D;
+  const float* ksrc = a.k_pool + (size_t)bh * nB * D;
+
+  for (int t = threadIdx.x; t < R * D; t += kThreads) {
+    const int g = t / D, d = t - g * D;
+    qs[g * QP + d] = (i0 + g < nB) ? (double)qsrc[(size_t)(i0 + g) * D + d] : 0.0;
+  }
+
+  // kbar chunk: 64 rows x D floats = 16*D float4, at most 8 per thread (D <= 128)
+  const int nf4 = 16 * D;
+  const int d4 = D / 4;
+  float4 pre[8];
+  auto load_chunk = [&](int c) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = threadIdx.x + u * kThreads;
+      const int r = e / d4, c4 = e - r * d4;
+      const int j = c * 64 + r;
+      pre[u] = (e < nf4 && j < nB) ? *reinterpret_cast<const float4*>(ksrc + (size_t)j * D + c4 * 4)
+                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+  auto store_chunk = [&]() {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = threadIdx.x + u * kThreads;
+      const int r = e / d4, c4 = e - r * d4;
+      if (e < nf4) *reinterpret_cast<float4*>(ks + r * KP + c4 * 4) = pre[u];
+    }
+  };
+
+  double sc[RW][NT];
+  load_chunk(0);
+#pragma unroll
+  for (int c = 0; c < NT; ++c) {
+    __syncthreads();                   // the previous chunk is consumed (q rows written)
+    store_chunk();
+    __syncthreads();
+    if (c + 1 < NT && (c + 1) * 64 < nB) load_chunk(c + 1);
+    double acc[RW];
+#pragma unroll
+    for (int r = 0; r < RW; ++r) acc[r] = 0.0;
+    if (c * 64 < nB) {
+      const float* krow = ks + lane * KP;
+      const double* qrow = qs + (w * RW) * QP;
+      for (int d = 0; d < D; d += 4) {
+        const float4 kv = *reinterpret_cast<const float4*>(krow + d);
+        const double k0 = kv.x, k1 = kv.y, k2 = kv.z, k3 = kv.w;
+#pragma unroll
+        for (int r = 0; r < RW; ++r) {
+          const double2 qa = *reinterpret_cast<const double2*>(qrow + r * QP + d);
+          const double2 qb = *reinterpret_cast<const double2*>(qrow + r * QP + d + 2);
+          double x = fma(qa.x, k0, acc[r]);
+          x = fma(qa.y, k1, x);
+          x = fma(qb.x, k2, x);
+          acc[r] = fma(qb.y, k3, x);
+        }
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < RW; ++r) sc[r][c] = a.scale * acc[r];
+  }
+
+  const uint32_t k = (uint32_t)a.k;
+#pragma unroll
+  for (int r = 0; r < RW; ++r) {
+    const int i = i0 + w * RW + r;
+    if (i >= nB) break;                // uniform: rows past the head's last block
+    const size_t row = (size_t)bh * nB + i;
+    uint64_t key[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) key[t] = (t * 64 + lane < nB) ? order_key(sc[r][t]) : 0ull;
+    // every valid key is > 0 (order_key maps -inf to 0x000F...), so T > 0
+    uint64_t T = 0;
+    for (int b = 63; b >= 0; --b) {
+      const uint64_t cand = T | (1ull << b);
+      uint32_t cnt = 0;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) cnt += __builtin_popcountll(__builtin_amdgcn_ballot_w64(key[t] >= cand));
+      if (cnt >= k) T = cand;
+    }
+    uint32_t above = 0;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) above += __builtin_popcountll(__builtin_amdgcn_ballot_w64(key[t] > T));
+    const uint32_t need = k - above;   // keys equal to T still to take, lowest indices first
+    int32_t* out = a.kv_idx + row * (size_t)a.kmax;
+    uint8_t* mrow = a.mask ? a.mask + row * (size_t)nB : nullptr;
+    uint32_t base = 0, ties = 0;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const int j = t * 64 + lane;
+      const bool eq = key[t] == T;
+      const uint64_t em = __builtin_amdgcn_ballot_w64(eq);
+      const uint32_t my_tie = ties + __builtin_amdgcn_mbcnt_hi((uint32_t)(em >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)em, 0u));
+      const bool kp = key[t] > T || (eq && my_tie < need);
+      const uint64_t km = __builtin_amdgcn_ballot_w64(kp);
+      const uint32_t pos = base + __builtin_amdgcn_mbcnt_hi((uint32_t)(km >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)km, 0u));
+      if (kp && pos < (uint32_t)a.kmax) out[pos] = j;
+      if (mrow && j < nB) mrow[j] = kp ? 1 : 0;
+      base += __builtin_popcountll(km);
+      ties += __builtin_popcountll(em);
+    }
+    for (int p = (int)base + lane; p < a.kmax; p += 64) out[p] = -1;
+    if (lane == 0) a.kv_count[row] = (int32_t)min(base, (uint32_t)a.kmax);
+  }
+}
+
+template <int NT, int RW>
+hipError_t launch_topk(SelectArgs a, int B, int H, hipStream_t stream) {
+  a.n_groups = (a.nB + 4 * RW - 1) / (4 * RW);
+  a.n_work = B * H * a.n_groups;
+  hipLaunchKernelGGL((topk_kernel<NT, RW>), dim3(a.n_work), dim3(kThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 size_t select_smem_bytes(int nB, int D, int mode, int sort_n) {
@@ -339,6 +481,16 @@ hipError_t launch_select(const Dims& d, const SelectRule& r, const float* q_pool
   int p = 1;
   while (p < m) p <<= 1;
   a.sort_n = (r.mode == 1) ? p : 0;
+  if (r.mode == 0 && d.D <= 128) {
+    const int nt = (d.nB + 63) / 64;
+    if (nt <= 1) return launch_topk<1, 4>(a, d.B, d.H, stream);
+    if (nt <= 2) return launch_topk<2, 4>(a, d.B, d.H, stream);
+    if (nt <= 4) return launch_topk<4, 4>(a, d.B, d.H, stream);
+    if (nt <= 8) return launch_topk<8, 4>(a, d.B, d.H, stream);
+    if (nt <= 16) return launch_topk<16, 4>(a, d.B, d.H, stream);
+    if (nt <= 24) return launch_topk<24, 2>(a, d.B, d.H, stream);
+    if (nt <= 32) return launch_topk<32, 2>(a, d.B, d.H, stream);
+  }
   const size_t smem = select_smem_bytes(d.nB, d.D, r.mode, a.sort_n);
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(select_kernel),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
