@@ -309,11 +309,12 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
 // into registers while this one is used), so every kbar row is read once per
 // R query rows; each score is the same sequential float64 fma chain over d as
 // in select_kernel, so both give identical bits.
-// The k-th largest order key T is found bit by bit from the top: a candidate
-// bit stays set when at least k keys are >= the candidate (counted with one
-// ballot per register).  Keys above T are kept, and of the keys equal to T the
-// k - #above lowest block indices; the kept indices are written in ascending
-// order from ballots.
+// The threshold T is found bit by bit from the top: a candidate bit stays set
+// when at least k keys are >= the candidate (counted with one ballot per
+// register); the search ends at the k-th largest key, or earlier once exactly
+// k keys are >= the candidate.  Keys above T are kept, and of the keys equal to
+// T the k - #above lowest block indices; the kept indices are written in
+// ascending order from ballots.
 template <int NT, int RW>
 __global__ __launch_bounds__(kThreads) void topk_kernel(SelectArgs a) {
   constexpr int R = 4 * RW;
@@ -400,7 +401,9 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(SelectArgs a) {
     uint64_t key[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) key[t] = (t * 64 + lane < nB) ? order_key(sc[r][t]) : 0ull;
-    // every valid key is > 0 (order_key maps -inf to 0x000F...), so T > 0
+    // every valid key is > 0 (order_key maps -inf to 0x000F...), so T > 0.
+    // Once exactly k keys are >= the candidate they are the top k (equal keys
+    // cannot straddle it) and the search stops with T = candidate.
     uint64_t T = 0;
     for (int b = 63; b >= 0; --b) {
       const uint64_t cand = T | (1ull << b);
@@ -408,6 +411,7 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(SelectArgs a) {
 #pragma unroll
       for (int t = 0; t < NT; ++t) cnt += __builtin_popcountll(__builtin_amdgcn_ballot_w64(key[t] >= cand));
       if (cnt >= k) T = cand;
+      if (cnt == k) break;
     }
     uint32_t above = 0;
 #pragma unroll
