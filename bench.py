@@ -1,7 +1,7 @@
 """Benchmark: block-sparse video self-attention on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-                    [--no-cpu-baseline] [--no-dense] [--cpu-seconds S]
+                    [--no-cpu-baseline] [--no-dense] [--cpu-seconds S] [--all-workloads]
 
 One step = the whole sparse path on one synthetic layer already resident in
 HBM: block pooling -> block selection -> sparse attention (the dense fallback
@@ -125,7 +125,19 @@ def cpu_baseline(wl, bits, budget_s: float):
                    f"total seconds"),
         "attention_only_tflops": flops / t_attn / 1e12,
         "seconds": total,
+        "cpu_model": _cpu_model(),
     }
+
+
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def main(argv=None):
@@ -141,6 +153,9 @@ def main(argv=None):
     ap.add_argument("--calib-copy-mb", type=int, default=0,
                     help="first run a plain device copy of this many MiB (a known-size kernel "
                          "for scaling the FETCH_SIZE/WRITE_SIZE counters)")
+    ap.add_argument("--all-workloads", action="store_true",
+                    help="one JSON line per workload (and per keep ratio of the sweep), "
+                         "without the CPU baseline; not the headline line")
     args = ap.parse_args(argv)
 
     if args.gpus != 1:
@@ -149,10 +164,17 @@ def main(argv=None):
               "launcher is built.", file=sys.stderr)
         return 2
 
-    import torch
+    from paper_2606_23743_amd import workloads
 
-    import paper_2606_23743_amd as sva
-    from paper_2606_23743_amd import inputs, workloads
+    if args.all_workloads:
+        import torch
+        for base in workloads.ALL:
+            for r in (base.ratios or (None,)):
+                wl = base.with_ratio(r) if r is not None else base
+                rec = measure(args, wl, with_cpu=False)
+                print(json.dumps(rec), flush=True)
+                torch.cuda.empty_cache()
+        return 0
 
     wl = workloads.find(args.workload)
     if wl is None:
@@ -160,6 +182,18 @@ def main(argv=None):
         return 2
     if args.keep_ratio is not None:
         wl = wl.with_ratio(args.keep_ratio)
+    rec = measure(args, wl, with_cpu=not args.no_cpu_baseline)
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
+def measure(args, wl, with_cpu: bool):
+    """Run the timed steps on one workload and return the JSON record."""
+    import torch
+
+    import paper_2606_23743_amd as sva
+    from paper_2606_23743_amd import inputs
+
     print(f"[bench] generating {wl.name}", file=sys.stderr, flush=True)
     bits = inputs.generate(wl)
     dev = {n: inputs.to_device(bits[n]) for n in ("q", "k", "v")}
@@ -217,9 +251,10 @@ def main(argv=None):
     t_end.record(stream)
     torch.cuda.synchronize()
     ms_step = t_start.elapsed_time(t_end) / args.steps
-    pool_ms = float(np.mean([a.elapsed_time(b) for a, b in pool_ev]))
-    sel_ms = float(np.mean([a.elapsed_time(b) for a, b in sel_ev]))
-    att_ms = float(np.mean([a.elapsed_time(b) for a, b in att_ev]))
+    pool_t = [a.elapsed_time(b) for a, b in pool_ev]
+    sel_t = [a.elapsed_time(b) for a, b in sel_ev]
+    att_t = [a.elapsed_time(b) for a, b in att_ev]
+    pool_ms, sel_ms, att_ms = float(np.mean(pool_t)), float(np.mean(sel_t)), float(np.mean(att_t))
     print(f"[bench] step {ms_step:.3f} ms (pool {pool_ms:.3f}, select {sel_ms:.3f}, attention {att_ms:.3f})",
           file=sys.stderr, flush=True)
 
@@ -227,6 +262,8 @@ def main(argv=None):
     att_tflops = flops / (att_ms * 1e-3) / 1e12
     value = flops / (ms_step * 1e-3) / 1e12
     pool_bytes = 2 * B * H * N * D * 2 + 2 * B * H * nb * D * 4
+    # select reads both pooled tensors and writes the index lists and counts
+    select_bytes = 2 * B * H * nb * D * 4 + B * H * nb * kmax * 4 + B * H * nb * 4
 
     extra = {}
     if not args.no_dense:
@@ -244,7 +281,7 @@ def main(argv=None):
         del dout
 
     cpu = None
-    if not args.no_cpu_baseline:
+    if with_cpu:
         print(f"[bench] cpu baseline (~{args.cpu_seconds:.0f} s)", file=sys.stderr, flush=True)
         cpu = cpu_baseline(wl, bits, args.cpu_seconds)
 
@@ -273,12 +310,16 @@ def main(argv=None):
                      "traffic": measured_traffic(wl.name),
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, calibrated)"},
         "stages_ms": {"pool": round(pool_ms, 4), "select": round(sel_ms, 4), "attention": round(att_ms, 4)},
+        "stages_ms_median": {"pool": round(float(np.median(pool_t)), 4),
+                             "select": round(float(np.median(sel_t)), 4),
+                             "attention": round(float(np.median(att_t)), 4)},
+        "pool_select_hbm_gbs": round((pool_bytes + select_bytes) / ((pool_ms + sel_ms) * 1e-3) / 1e9, 1),
         "pool_hbm_gbs": round(pool_bytes / (pool_ms * 1e-3) / 1e9, 1),
         "cpu_baseline": cpu,
     }
     rec.update(extra)
-    print(json.dumps(rec), flush=True)
-    return 0
+    del dev, qp, kp, idx, cnt, out
+    return rec
 
 
 if __name__ == "__main__":
