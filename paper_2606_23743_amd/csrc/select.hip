@@ -1,83 +1,18 @@
 // Block scores and block selection ("score-based routing", Appendix A.2.2;
 // the block-wise similarity of Section 4.2.2).
-//
-// One workgroup of 4 waves handles 4 consecutive query-block rows of one
-// (b, h).  Phase 1 computes the 4 x nB score tile s[i, j] = c * <qbar_i, kbar_j>
-// in float64 into LDS: kbar is streamed through LDS in chunks of 64 blocks with
-// coalesced loads, so each kbar row is read once per 4 query rows.  The fp32
-// products are exact in float64, so only the float64 sum rounds.
-//
-// Phase 2 gives each wave one row:
-//   top-k: a radix select over order-preserving 64-bit keys of the float64
-//          scores (8 passes of 8-bit digits, histogram in LDS) finds the k-th
-//          largest key T and how many elements equal to T are still needed;
-//          those ties are taken in ascending block order.
-//   mass : softmax weights in float64; the non-forced blocks are sorted by
-//          (score desc, index asc) with a bitonic network in LDS; a prefix sum
-//          over that order finds the first point where the forced mass plus the
-//          added mass reaches tau, bounded by the cap.
-// Both finish with an ordered compaction (wave prefix sums) that writes the
-// kept indices in ascending order, pads with -1, and writes the optional mask.
+#include <type_traits>
+
 #include "sva_internal.h"
 
 namespace sva {
 namespace {
 
-constexpr int kRows = 4;          // query-block rows per workgroup (one per wave)
 constexpr int kThreads = 256;
-constexpr int kChunkJ = 64;       // kbar rows staged per phase-1 chunk
 
 __device__ __forceinline__ uint64_t order_key(double s) {
   if (s == 0.0) s = 0.0;          // -0 and +0 compare equal: give them one key
   const uint64_t b = (uint64_t)__double_as_longlong(s);
   return (b >> 63) ? ~b : (b | 0x8000000000000000ull);
-}
-
-__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const uint32_t o = __shfl_up(v, off, 64);
-    if (lane >= off) v += o;
-  }
-  return v;
-}
-
-__device__ __forceinline__ double wave_incl_scan_f64(double v) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const double o = __shfl_up(v, off, 64);
-    if (lane >= off) v += o;
-  }
-  return v;
-}
-
-__device__ __forceinline__ double wave_max_f64(double v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v = fmax(v, __shfl_xor(v, off, 64));
-  return v;
-}
-
-__device__ __forceinline__ double wave_sum_f64(double v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-  return v;
-}
-
-__device__ __forceinline__ int wave_min_i32(int v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v = min(v, __shfl_xor(v, off, 64));
-  return v;
-}
-
-// Orders this wave's LDS writes before its later LDS reads of other lanes'
-// data (LDS requests of one wave are served in issue order; this keeps the
-// compiler from moving the reads up).
-__device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
 struct SelectArgs {
@@ -88,235 +23,73 @@ struct SelectArgs {
   uint8_t* mask;
   int nB, D, kmax, n_groups, n_work;
   double scale;
-  int mode, k, cap, n_forced, sort_n;  // sort_n: power of two >= nB - n_forced
+  int mode, k, cap, n_forced;
   double tau;
 };
 
-// Writes one row's kept flags (given by keep(j)) in ascending order.
-template <typename KeepFn>
-__device__ void compact_row(const SelectArgs& a, size_t row, int lane, KeepFn keep) {
-  const int nB = a.nB;
-  const int per = (nB + 63) / 64;
-  const int j0 = min(nB, lane * per);
-  const int j1 = min(nB, j0 + per);
-  uint32_t n = 0;
-  for (int j = j0; j < j1; ++j) n += keep(j) ? 1u : 0u;
-  const uint32_t incl = wave_incl_scan(n);
-  uint32_t pos = incl - n;
-  const uint32_t total = __shfl(incl, 63, 64);
-  int32_t* out = a.kv_idx + row * (size_t)a.kmax;
-  uint8_t* mrow = a.mask ? a.mask + row * (size_t)nB : nullptr;
-  for (int j = j0; j < j1; ++j) {
-    const bool kp = keep(j);
-    if (kp) {
-      if (pos < (uint32_t)a.kmax) out[pos] = j;   // never past the row, whatever the flags say
-      ++pos;
-    }
-    if (mrow) mrow[j] = kp ? 1 : 0;
-  }
-  for (int p = (int)total + lane; p < a.kmax; p += 64) out[p] = -1;
-  if (lane == 0) a.kv_count[row] = (int32_t)min(total, (uint32_t)a.kmax);
-}
-
-__global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  const int nB = a.nB, D = a.D;
-  double* scores = reinterpret_cast<double*>(smem);                 // [kRows][nB]
-  unsigned char* area = smem + (size_t)kRows * nB * sizeof(double);  // phase scratch
-
-  const int work = xcd_remap(blockIdx.x, a.n_work);
-  const int bh = work / a.n_groups;
-  const int i0 = (work - bh * a.n_groups) * kRows;
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int w = tid >> 6;
-
-  // ---------------- phase 1: score tile ----------------
-  {
-    float* qt = reinterpret_cast<float*>(area);                      // [kRows][D]
-    float* kt = qt + kRows * D;                                      // [kChunkJ][D+1]
-    const float* qsrc = a.q_pool + ((size_t)bh * nB) * D;
-    const float* ksrc = a.k_pool + ((size_t)bh * nB) * D;
-    for (int t = tid; t < kRows * D; t += kThreads) {
-      const int g = t / D, d = t - g * D;
-      qt[t] = (i0 + g < nB) ? qsrc[(size_t)(i0 + g) * D + d] : 0.0f;
-    }
-    const int g = tid / kChunkJ;
-    const int jj = tid - g * kChunkJ;
-    for (int j0 = 0; j0 < nB; j0 += kChunkJ) {
-      __syncthreads();
-      const int rows = min(kChunkJ, nB - j0);
-      for (int t = tid; t < rows * D; t += kThreads) {
-        const int r = t / D, d = t - r * D;
-        kt[r * (D + 1) + d] = ksrc[(size_t)(j0 + r) * D + d];
-      }
-      __syncthreads();
-      if (jj < rows) {
-        const float* qa = qt + g * D;
-        const float* ka = kt + jj * (D + 1);
-        double acc = 0.0;
-        for (int d = 0; d < D; ++d) acc = fma((double)qa[d], (double)ka[d], acc);
-        scores[g * nB + j0 + jj] = a.scale * acc;
-      }
-    }
-    __syncthreads();
-  }
-
-  const int i = i0 + w;
-  const bool row_ok = i < nB;
-  const size_t row = (size_t)bh * nB + (row_ok ? i : 0);
-  const double* sc = scores + w * nB;
-
-  if (a.mode == 0) {
-    // ---------------- top-k: radix select ----------------
-    uint32_t* hist = reinterpret_cast<uint32_t*>(area) + w * 256;
-    uint64_t prefix = 0;
-    uint32_t need = (uint32_t)a.k;   // rank (1-based) of the wanted key among the rest
-    for (int pass = 0; pass < 8; ++pass) {
-      const int shift = 56 - 8 * pass;
-      for (int b = lane; b < 256; b += 64) hist[b] = 0;
-      __syncthreads();
-      if (row_ok) {
-        for (int j = lane; j < nB; j += 64) {
-          const uint64_t key = order_key(sc[j]);
-          if (pass == 0 || (key >> (shift + 8)) == prefix)
-            atomicAdd(&hist[(key >> shift) & 255u], 1u);
-        }
-      }
-      __syncthreads();
-      // lane l owns bins 255-4l .. 252-4l (descending); scan counts from the top
-      uint32_t c[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) c[e] = hist[255 - 4 * lane - e];
-      const uint32_t tot = c[0] + c[1] + c[2] + c[3];
-      const uint32_t incl = wave_incl_scan(tot);
-      const uint32_t excl = incl - tot;
-      const bool mine = excl < need && need <= incl;
-      int digit = 0;
-      uint32_t above = excl;
-      if (mine) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          if (above + c[e] >= need) { digit = 255 - 4 * lane - e; break; }
-          above += c[e];
-        }
-      }
-      const uint64_t bal = __ballot(mine);
-      const int src = bal ? (__ffsll((unsigned long long)bal) - 1) : 0;
-      digit = __shfl(digit, src, 64);
-      above = __shfl(above, src, 64);
-      prefix = (prefix << 8) | (uint64_t)digit;
-      need -= above;
-    }
-    const uint64_t T = prefix;
-    unsigned char* flags = reinterpret_cast<unsigned char*>(area) + kRows * 256 * sizeof(uint32_t) +
-                           (size_t)w * nB;
-    if (row_ok) {
-      // keys above T are kept; of the keys equal to T, the `need` lowest indices
-      const int per = (nB + 63) / 64;
-      const int j0 = min(nB, lane * per), j1 = min(nB, j0 + per);
-      uint32_t neq = 0;
-      for (int j = j0; j < j1; ++j) neq += (order_key(sc[j]) == T) ? 1u : 0u;
-      uint32_t tie_rank = wave_incl_scan(neq) - neq;   // ties in lower lanes' ranges
-      for (int j = j0; j < j1; ++j) {
-        const uint64_t key = order_key(sc[j]);
-        bool kp = key > T;
-        if (key == T) kp = (tie_rank++ < need);
-        flags[j] = kp ? 1 : 0;
-      }
-      wave_lds_sync();
-      compact_row(a, row, lane, [&](int j) -> bool { return flags[j] != 0; });
-    }
-  } else {
-    // ---------------- cumulative mass ----------------
-    const int nF = a.n_forced;
-    const int M = nB - nF;
-    const int P = a.sort_n;
-    uint64_t* skey = reinterpret_cast<uint64_t*>(area) + (size_t)w * P;
-    uint16_t* sidx = reinterpret_cast<uint16_t*>(reinterpret_cast<uint64_t*>(area) + (size_t)kRows * P) +
-                     (size_t)w * P;
-    unsigned char* flags = reinterpret_cast<unsigned char*>(
-                               reinterpret_cast<uint16_t*>(reinterpret_cast<uint64_t*>(area) +
-                                                           (size_t)kRows * P) + (size_t)kRows * P) +
-                           (size_t)w * nB;
-
-    double mx = -INFINITY;
-    for (int j = lane; j < nB; j += 64) mx = fmax(mx, sc[j]);
-    mx = wave_max_f64(mx);
-    double z = 0.0;
-    for (int j = lane; j < nB; j += 64) z += exp(sc[j] - mx);
-    z = wave_sum_f64(z);
-    const double inv_z = 1.0 / z;
-    double mf = 0.0;
-    for (int j = lane; j < nF; j += 64) mf += exp(sc[j] - mx) * inv_z;
-    mf = wave_sum_f64(mf);
-
-    for (int t = lane; t < P; t += 64) {
-      if (t < M) { skey[t] = order_key(sc[nF + t]); sidx[t] = (uint16_t)(nF + t); }
-      else { skey[t] = 0; sidx[t] = 0xFFFF; }
-    }
-    for (int j = lane; j < nB; j += 64) flags[j] = (j < nF) ? 1 : 0;
-    __syncthreads();
-    // bitonic sort, final order: key descending, index ascending
-    for (int size = 2; size <= P; size <<= 1) {
-      for (int stride = size >> 1; stride > 0; stride >>= 1) {
-        for (int t = lane; t < P / 2; t += 64) {
-          const int lo = 2 * t - (t & (stride - 1));
-          const int hi = lo + stride;
-          const bool desc = (lo & size) == 0;   // this run ends up "before" order
-          const uint64_t ka = skey[lo], kb = skey[hi];
-          const uint16_t ia = sidx[lo], ib = sidx[hi];
-          // "a before b" in the final order
-          const bool a_first = (ka > kb) || (ka == kb && ia < ib);
-          if (a_first != desc) {
-            skey[lo] = kb; skey[hi] = ka;
-            sidx[lo] = ib; sidx[hi] = ia;
-          }
-        }
-        __syncthreads();
-      }
-    }
-    if (row_ok) {
-      int n_add = 0;
-      const int budget = a.cap - nF;
-      if (mf < a.tau && budget > 0) {
-        const int L = min(M, budget);
-        const int per = (L + 63) / 64;
-        const int t0 = min(L, lane * per), t1 = min(L, t0 + per);
-        double part = 0.0;
-        for (int t = t0; t < t1; ++t) part += exp(sc[sidx[t]] - mx) * inv_z;
-        double m = mf + (wave_incl_scan_f64(part) - part);
-        int first = L;   // position of the first block whose addition reaches tau
-        for (int t = t0; t < t1; ++t) {
-          m += exp(sc[sidx[t]] - mx) * inv_z;
-          if (m >= a.tau) { first = t; break; }
-        }
-        first = wave_min_i32(first);
-        n_add = (first < L) ? first + 1 : L;
-      }
-      for (int t = lane; t < n_add; t += 64) flags[sidx[t]] = 1;
-      wave_lds_sync();
-      compact_row(a, row, lane, [&](int j) -> bool { return flags[j] != 0; });
-    }
-  }
-}
-
 // ---------------------------------------------------------------------------
-// Top-k with the scores in registers.  A workgroup (4 waves) takes R = 4*RW
+// Selection with the scores in registers.  A workgroup (4 waves) takes R = 4*RW
 // query-block rows of one (b, h); each wave owns RW of them, and lane l holds
 // the float64 scores of blocks j = t*64 + l (t < NT) for each of its rows.
 // kbar is staged through LDS 64 blocks at a time (the next chunk is loaded
 // into registers while this one is used), so every kbar row is read once per
-// R query rows; each score is the same sequential float64 fma chain over d as
-// in select_kernel, so both give identical bits.
-// The threshold T is found bit by bit from the top: a candidate bit stays set
-// when at least k keys are >= the candidate (counted with one ballot per
-// register); the search ends at the k-th largest key, or earlier once exactly
-// k keys are >= the candidate.  Keys above T are kept, and of the keys equal to
-// T the k - #above lowest block indices; the kept indices are written in
-// ascending order from ballots.
-template <int NT, int RW>
-__global__ __launch_bounds__(kThreads) void topk_kernel(SelectArgs a) {
+// R query rows.  Each score is one sequential float64 fma chain over d: the
+// fp32 products are exact in float64, so only the running sum rounds.
+//
+// Both rules end in a threshold key T and a quota: keys above T are kept, and
+// of the keys equal to T the `quota` lowest block indices.
+// top-k : T is the k-th largest order key, found bit by bit from the top (a
+//         candidate bit stays set when at least k keys are >= the candidate,
+//         counted with one ballot per register); the search stops early once
+//         exactly k keys are >= the candidate.
+// mass  : the forced (first-frame) blocks are kept and their softmax mass
+//         counted; over the other blocks T is the largest key whose upper set
+//         (keys >= T) brings the mass to tau, found bit by bit with the mass
+//         of each candidate's upper set as a wave sum.  The search stops once
+//         the bracket [T, T_hi) holds a single key (the block whose addition
+//         crosses tau); equal keys at T are added in index order until the
+//         mass reaches tau.  If that needs more blocks than the cap allows,
+//         the kept blocks are the top (cap - forced) by the top-k search.
+// The kept indices are written in ascending order from ballots.
+__device__ __forceinline__ uint32_t lanes_below(uint64_t m) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+__device__ __forceinline__ double wave_sum_d(double v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+__device__ __forceinline__ double wave_max_d(double v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v = fmax(v, __shfl_xor(v, off, 64));
+  return v;
+}
+
+// k-th largest key (k >= 1, at least k keys > 0); returns T and the number of
+// keys equal to T to keep.
+template <int NT>
+__device__ __forceinline__ void kth_key(const uint64_t (&key)[NT], uint32_t k, uint64_t& T_out,
+                                        uint32_t& quota) {
+  uint64_t T = 0;
+  for (int b = 63; b >= 0; --b) {
+    const uint64_t cand = T | (1ull << b);
+    uint32_t cnt = 0;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) cnt += __builtin_popcountll(__builtin_amdgcn_ballot_w64(key[t] >= cand));
+    if (cnt >= k) T = cand;
+    if (cnt == k) break;
+  }
+  uint32_t above = 0;
+#pragma unroll
+  for (int t = 0; t < NT; ++t) above += __builtin_popcountll(__builtin_amdgcn_ballot_w64(key[t] > T));
+  T_out = T;
+  quota = k - above;
+}
+
+template <int NT, int RW, bool MASS>
+__global__ __launch_bounds__(kThreads) void select_reg_kernel(SelectArgs a) {
   constexpr int R = 4 * RW;
   constexpr int KP = 132;            // kbar row pitch in LDS (floats): conflict-free b128 reads
   constexpr int QP = 128;            // qbar row pitch in LDS (doubles)
@@ -392,43 +165,150 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(SelectArgs a) {
     for (int r = 0; r < RW; ++r) sc[r][c] = a.scale * acc[r];
   }
 
-  const uint32_t k = (uint32_t)a.k;
-#pragma unroll
-  for (int r = 0; r < RW; ++r) {
+  // one row at a time: the row index must be a compile-time constant so the
+  // score registers stay registers
+  auto select_row = [&](auto rc) {
+    constexpr int r = decltype(rc)::value;
     const int i = i0 + w * RW + r;
-    if (i >= nB) break;                // uniform: rows past the head's last block
+    if (i >= nB) return;               // uniform: rows past the head's last block
     const size_t row = (size_t)bh * nB + i;
+    const int nF = MASS ? a.n_forced : 0;
     uint64_t key[NT];
+    // every valid key is > 0 (order_key maps -inf to 0x000F...); forced and
+    // padding blocks get key 0 and never pass a candidate
 #pragma unroll
-    for (int t = 0; t < NT; ++t) key[t] = (t * 64 + lane < nB) ? order_key(sc[r][t]) : 0ull;
-    // every valid key is > 0 (order_key maps -inf to 0x000F...), so T > 0.
-    // Once exactly k keys are >= the candidate they are the top k (equal keys
-    // cannot straddle it) and the search stops with T = candidate.
-    uint64_t T = 0;
-    for (int b = 63; b >= 0; --b) {
-      const uint64_t cand = T | (1ull << b);
-      uint32_t cnt = 0;
-#pragma unroll
-      for (int t = 0; t < NT; ++t) cnt += __builtin_popcountll(__builtin_amdgcn_ballot_w64(key[t] >= cand));
-      if (cnt >= k) T = cand;
-      if (cnt == k) break;
+    for (int t = 0; t < NT; ++t) {
+      const int j = t * 64 + lane;
+      key[t] = (j < nB && j >= nF) ? order_key(sc[r][t]) : 0ull;
     }
-    uint32_t above = 0;
+    uint64_t T = 0;
+    uint32_t quota = 0;
+    if constexpr (!MASS) {
+      kth_key<NT>(key, (uint32_t)a.k, T, quota);
+    } else {
+      // softmax weights over all blocks, as the definition: exp(s - max) / sum
+      double mx = -INFINITY;
 #pragma unroll
-    for (int t = 0; t < NT; ++t) above += __builtin_popcountll(__builtin_amdgcn_ballot_w64(key[t] > T));
-    const uint32_t need = k - above;   // keys equal to T still to take, lowest indices first
+      for (int t = 0; t < NT; ++t)
+        if (t * 64 + lane < nB) mx = fmax(mx, sc[r][t]);
+      mx = wave_max_d(mx);
+      double p[NT];
+      double z = 0.0;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        p[t] = (t * 64 + lane < nB) ? exp(sc[r][t] - mx) : 0.0;
+        z += p[t];
+      }
+      z = wave_sum_d(z);
+      double mf = 0.0, mo = 0.0;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        p[t] = p[t] / z;
+        if (t * 64 + lane < nF) mf += p[t];
+        else mo += p[t];
+      }
+      mf = wave_sum_d(mf);
+      mo = wave_sum_d(mo);
+      const int M = nB - nF;             // blocks that may be added
+      const int budget = a.cap - nF;
+      int n_add;                         // blocks the mass rule adds (before the cap)
+      if (mf >= a.tau || budget <= 0 || M <= 0) {
+        n_add = 0;
+      } else if (mf + mo < a.tau) {
+        n_add = M;                       // tau is out of reach: everything, up to the cap
+        T = 0;
+        quota = 0;
+      } else {
+        // bracket: mass(upper set of T) >= tau > mass(upper set of T_hi)
+        uint64_t T_lo = 0;
+        uint32_t cnt_lo = (uint32_t)M, cnt_hi = 0;
+        double mass_hi = mf;
+        bool single = false;
+        for (int b = 63; b >= 0; --b) {
+          const uint64_t cand = T_lo | (1ull << b);
+          uint32_t cnt = 0;
+          double part = 0.0;
+#pragma unroll
+          for (int t = 0; t < NT; ++t) {
+            const bool ge = key[t] >= cand;
+            cnt += __builtin_popcountll(__builtin_amdgcn_ballot_w64(ge));
+            part += ge ? p[t] : 0.0;
+          }
+          const double m = mf + wave_sum_d(part);
+          if (m >= a.tau) { T_lo = cand; cnt_lo = cnt; }
+          else { cnt_hi = cnt; mass_hi = m; }
+          if (cnt_lo - cnt_hi == 1) { single = true; break; }
+        }
+        if (single) {
+          // the one key in [T_lo, T_hi) is the block whose addition crosses
+          // tau; the (non-zero) keys >= T_lo are it and the cnt_hi keys above
+          // it, so it is their minimum
+          uint64_t mn = ~0ull;
+#pragma unroll
+          for (int t = 0; t < NT; ++t)
+            if (key[t] != 0 && key[t] >= T_lo && key[t] < mn) mn = key[t];
+#pragma unroll
+          for (int off = 32; off > 0; off >>= 1) {
+            const uint64_t o = __shfl_xor(mn, off, 64);
+            mn = o < mn ? o : mn;
+          }
+          T = mn;
+          quota = 1;
+          n_add = (int)cnt_hi + 1;
+        } else {
+          // T_lo is an exact key held by several blocks: add them in index
+          // order until the mass reaches tau
+          T = T_lo;
+          double run = mass_hi;
+          uint32_t taken = 0;
+          bool done = false;
+#pragma unroll
+          for (int t = 0; t < NT; ++t) {
+            const bool eq = key[t] == T;
+            const uint64_t em = __builtin_amdgcn_ballot_w64(eq);
+            if (!done && em != 0) {       // uniform
+              double v = eq ? p[t] : 0.0;
+              for (int off = 1; off < 64; off <<= 1) {
+                const double o = __shfl_up(v, off, 64);
+                if (lane >= off) v += o;
+              }
+              // first tie lane whose running mass reaches tau
+              const uint64_t hit = __builtin_amdgcn_ballot_w64(eq && run + v >= a.tau);
+              if (hit != 0) {
+                const int l0 = __builtin_ctzll(hit);
+                taken += __builtin_popcountll(em & ((2ull << l0) - 1));
+                done = true;
+              } else {
+                taken += __builtin_popcountll(em);
+                run += __shfl(v, 63, 64);
+              }
+            }
+          }
+          quota = taken;
+          n_add = (int)cnt_hi + (int)taken;
+        }
+      }
+      if (n_add > budget) {
+        // the cap binds: the best (cap - forced) blocks
+        kth_key<NT>(key, (uint32_t)budget, T, quota);
+      } else if (n_add == 0) {
+        T = ~0ull;                       // nothing but the forced blocks
+        quota = 0;
+      }
+    }
     int32_t* out = a.kv_idx + row * (size_t)a.kmax;
     uint8_t* mrow = a.mask ? a.mask + row * (size_t)nB : nullptr;
     uint32_t base = 0, ties = 0;
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
       const int j = t * 64 + lane;
-      const bool eq = key[t] == T;
+      const bool eq = key[t] != 0 && key[t] == T;
       const uint64_t em = __builtin_amdgcn_ballot_w64(eq);
-      const uint32_t my_tie = ties + __builtin_amdgcn_mbcnt_hi((uint32_t)(em >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)em, 0u));
-      const bool kp = key[t] > T || (eq && my_tie < need);
+      const uint32_t my_tie = ties + lanes_below(em);
+      const bool forced = j < nF && j < nB;
+      const bool kp = forced || (key[t] != 0 && key[t] > T) || (eq && my_tie < quota);
       const uint64_t km = __builtin_amdgcn_ballot_w64(kp);
-      const uint32_t pos = base + __builtin_amdgcn_mbcnt_hi((uint32_t)(km >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)km, 0u));
+      const uint32_t pos = base + lanes_below(km);
       if (kp && pos < (uint32_t)a.kmax) out[pos] = j;
       if (mrow && j < nB) mrow[j] = kp ? 1 : 0;
       base += __builtin_popcountll(km);
@@ -436,30 +316,23 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(SelectArgs a) {
     }
     for (int p = (int)base + lane; p < a.kmax; p += 64) out[p] = -1;
     if (lane == 0) a.kv_count[row] = (int32_t)min(base, (uint32_t)a.kmax);
-  }
+  };
+  select_row(std::integral_constant<int, 0>{});
+  if constexpr (RW > 1) select_row(std::integral_constant<int, 1>{});
+  if constexpr (RW > 2) select_row(std::integral_constant<int, 2>{});
+  if constexpr (RW > 3) select_row(std::integral_constant<int, 3>{});
 }
 
 template <int NT, int RW>
-hipError_t launch_topk(SelectArgs a, int B, int H, hipStream_t stream) {
+hipError_t launch_reg(SelectArgs a, int B, int H, hipStream_t stream) {
   a.n_groups = (a.nB + 4 * RW - 1) / (4 * RW);
   a.n_work = B * H * a.n_groups;
-  hipLaunchKernelGGL((topk_kernel<NT, RW>), dim3(a.n_work), dim3(kThreads), 0, stream, a);
+  if (a.mode == 0) hipLaunchKernelGGL((select_reg_kernel<NT, RW, false>), dim3(a.n_work), dim3(kThreads), 0, stream, a);
+  else hipLaunchKernelGGL((select_reg_kernel<NT, RW, true>), dim3(a.n_work), dim3(kThreads), 0, stream, a);
   return hipGetLastError();
 }
 
 }  // namespace
-
-size_t select_smem_bytes(int nB, int D, int mode, int sort_n) {
-  const size_t scores = (size_t)kRows * nB * sizeof(double);
-  const size_t p1 = (size_t)kRows * D * sizeof(float) + (size_t)kChunkJ * (D + 1) * sizeof(float);
-  size_t p2;
-  if (mode == 0) {
-    p2 = (size_t)kRows * 256 * sizeof(uint32_t) + (size_t)kRows * nB;
-  } else {
-    p2 = (size_t)kRows * sort_n * (sizeof(uint64_t) + sizeof(uint16_t)) + (size_t)kRows * nB;
-  }
-  return scores + (p1 > p2 ? p1 : p2);
-}
 
 hipError_t launch_select(const Dims& d, const SelectRule& r, const float* q_pool,
                          const float* k_pool, int kmax, int32_t* kv_idx, int32_t* kv_count,
@@ -473,34 +346,22 @@ hipError_t launch_select(const Dims& d, const SelectRule& r, const float* q_pool
   a.nB = d.nB;
   a.D = d.D;
   a.kmax = kmax;
-  a.n_groups = (d.nB + kRows - 1) / kRows;
-  a.n_work = d.B * d.H * a.n_groups;
   a.scale = (double)d.scale;
   a.mode = r.mode;
   a.k = r.k;
   a.cap = r.cap;
   a.n_forced = r.n_forced;
   a.tau = r.tau;
-  int m = d.nB - r.n_forced;
-  int p = 1;
-  while (p < m) p <<= 1;
-  a.sort_n = (r.mode == 1) ? p : 0;
-  if (r.mode == 0 && d.D <= 128) {
-    const int nt = (d.nB + 63) / 64;
-    if (nt <= 1) return launch_topk<1, 4>(a, d.B, d.H, stream);
-    if (nt <= 2) return launch_topk<2, 4>(a, d.B, d.H, stream);
-    if (nt <= 4) return launch_topk<4, 4>(a, d.B, d.H, stream);
-    if (nt <= 8) return launch_topk<8, 4>(a, d.B, d.H, stream);
-    if (nt <= 16) return launch_topk<16, 4>(a, d.B, d.H, stream);
-    if (nt <= 24) return launch_topk<24, 2>(a, d.B, d.H, stream);
-    if (nt <= 32) return launch_topk<32, 2>(a, d.B, d.H, stream);
-  }
-  const size_t smem = select_smem_bytes(d.nB, d.D, r.mode, a.sort_n);
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(select_kernel),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(select_kernel, dim3(a.n_work), dim3(kThreads), smem, stream, a);
-  return hipGetLastError();
+  // nB <= SVA_SELECT_MAX_BLOCKS (2048) and D <= 128 are checked by the caller
+  const int nt = (d.nB + 63) / 64;
+  if (nt <= 1) return launch_reg<1, 4>(a, d.B, d.H, stream);
+  if (nt <= 2) return launch_reg<2, 4>(a, d.B, d.H, stream);
+  if (nt <= 4) return launch_reg<4, 4>(a, d.B, d.H, stream);
+  if (nt <= 8) return launch_reg<8, 4>(a, d.B, d.H, stream);
+  if (nt <= 16) return launch_reg<16, 4>(a, d.B, d.H, stream);
+  if (nt <= 24) return launch_reg<24, 2>(a, d.B, d.H, stream);
+  if (nt <= 32) return launch_reg<32, 2>(a, d.B, d.H, stream);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace sva
