@@ -8,11 +8,11 @@
 //
 // Keys are processed in 32-key chunks staged in LDS, chunk c of a kept block
 // in stage c (S/32 stages), filled by buffer_load ... lds straight from global
-// memory S/32 - 1 chunks ahead.  Tiles are unpadded and XOR-swizzled on
-// 16-byte pieces so that both the ds_read_b128 K operand reads and the
-// ds_read_b64_tr_b16 V transpose reads are free of bank conflicts.  With
-// S = 128 each wave also overlaps the next chunk's S^T MFMAs with the current
-// chunk's softmax.
+// memory ahead of use (S = 128: three chunks ahead; S = 64: K two chunks and
+// V one chunk ahead).  Tiles are unpadded and XOR-swizzled on 16-byte pieces
+// so that both the ds_read_b128 K operand reads and the ds_read_b64_tr_b16 V
+// transpose reads are free of bank conflicts.  Each wave overlaps the next
+// chunk's S^T MFMAs with the current chunk's softmax.
 //
 // Per 32-key sub-chunk (lane = one query; its 16 S^T registers are keys
 // (r/4)*8 + half*4 + r%4):
@@ -26,6 +26,8 @@
 // logits jump by more than ~2^63 over the running sum inside one block) is
 // marked (NaN first element) and recomputed by the per-iteration rescaling
 // kernel that runs next.
+#include <type_traits>
+
 #include "attn_common.h"
 
 namespace sva {
@@ -42,7 +44,7 @@ void attn_q32_kernel(AttnArgs a) {
   constexpr int NCK = S / CK;                // chunks per block
   constexpr int NST = NCK;                   // LDS stages: chunk c of a block in stage c
   constexpr int PD = NST - 1;                // prefetch distance, in chunks
-  constexpr bool PIPE = NST >= 4;            // S of chunk c+1 overlaps chunk c's softmax
+  constexpr bool PIPE = NST >= 4;            // four stages (S = 128); else two (S = 64)
   constexpr int CT = CK * G::RB;             // bytes of one chunk tile (K or V)
   constexpr int NUW = CT / 1024 / NW;        // direct-load pieces per wave per tile
   static_assert(NUW >= 1 && PD >= 1, "tile split");
@@ -126,15 +128,16 @@ void attn_q32_kernel(AttnArgs a) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_u8*)(size_t)__builtin_amdgcn_readfirstlane(lds_addr), 16,
                                              voff, __builtin_amdgcn_readfirstlane(soff), 0, 0);
   };
-  auto fetch = [&](int st, int key0) {
+  // One tensor's pieces of one chunk into stage st (TK: K, else V).
+  auto fetch_one = [&](auto tk, int st, int key0) {
+    constexpr bool TK = decltype(tk)::value;
+    const __amdgpu_buffer_rsrc_t& rs = TK ? krs : vrs;
+    const unsigned base = (TK ? ks_base : vs_base) + st * CT;
     key0 = __builtin_amdgcn_readfirstlane(key0);
     if (key0 + CK <= N) {
 #pragma unroll
-      for (int v = 0; v < NUW; ++v) {
-        const int u = w * NUW + v;
-        bll(krs, ks_base + st * CT + u * 1024, kgv[v], key0 * D * 2);
-        bll(vrs, vs_base + st * CT + u * 1024, vgv[v], key0 * D * 2);
-      }
+      for (int v = 0; v < NUW; ++v)
+        bll(rs, base + (w * NUW + v) * 1024, TK ? kgv[v] : vgv[v], key0 * D * 2);
     } else {
       // The lane id goes through an empty asm so this rare path's per-lane
       // values are recomputed here rather than hoisted and kept live.
@@ -147,14 +150,18 @@ void attn_q32_kernel(AttnArgs a) {
       for (int v = 0; v < NUW; ++v) {
         const int u = w * NUW + v;
         const int r = u * G::RPI + ln / G::NCH;
-        const int rs = r < valid ? r : 0;
-        int ck = swz_k<G::NCH>(r, p), cv = swz_v<G::NCH>(r, p);
-        if (ck >= G::DCH) ck = 0;
-        if (cv >= G::DCH) cv = 0;
-        bll(krs, ks_base + st * CT + u * 1024, (rs * D + ck * 8) * 2, key0 * D * 2);
-        bll(vrs, vs_base + st * CT + u * 1024, (rs * D + cv * 8) * 2, key0 * D * 2);
+        const int rs_ = r < valid ? r : 0;
+        int c = TK ? swz_k<G::NCH>(r, p) : swz_v<G::NCH>(r, p);
+        if (c >= G::DCH) c = 0;
+        bll(rs, base + u * 1024, (rs_ * D + c * 8) * 2, key0 * D * 2);
       }
     }
+  };
+  auto fetch_k = [&](int st, int key0) { fetch_one(std::true_type{}, st, key0); };
+  auto fetch_v = [&](int st, int key0) { fetch_one(std::false_type{}, st, key0); };
+  auto fetch = [&](int st, int key0) {
+    fetch_k(st, key0);
+    fetch_v(st, key0);
   };
 
   // Per-lane LDS offsets.  K operand, step s: row l32 of the tile, piece
@@ -230,29 +237,6 @@ void attn_q32_kernel(AttnArgs a) {
     }
   };
 
-  // One chunk: the tail mask and the reference maximum are small uniform
-  // branches that touch only S and m, never O, so the O registers carry
-  // through every copy of the body without moves.
-  auto chunk = [&](const unsigned char* kt, const unsigned char* vt, int key0, bool first) {
-    f32x16 sacc;
-    bf16x8 pop[2];
-    qk(sacc, kt);
-    const int valid = __builtin_amdgcn_readfirstlane(N - key0);
-    if (valid < CK) {
-      asm volatile("");          // keep this a real (rarely taken) branch, not select code
-      mask_tail(sacc, valid);
-    }
-    if (first) {
-      // the first chunk holds at least one valid key, so the maximum is finite
-      float mx = sacc[0];
-#pragma unroll
-      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[r]);
-      m_ref = swap_halves_max(mx) * sl2;
-    }
-    softmax(sacc, pop);
-    pv(pop, vt);
-  };
-
   // After every kept block: if a row sum has grown past 2^64 (the reference
   // maximum was far below this row's logits), move the reference up by the
   // sum's binary exponent and scale that query's O and l by the same power of
@@ -294,6 +278,7 @@ void attn_q32_kernel(AttnArgs a) {
   if (it < count) {
 #pragma unroll
     for (int c = 0; c < PD; ++c) fetch(c, j * S + c * CK);
+    if constexpr (!PIPE) fetch_k(1, j * S + CK);
   }
   auto advance_block = [&](int itnn, int jnn) {
     it = itn;
@@ -353,20 +338,50 @@ void attn_q32_kernel(AttnArgs a) {
       advance_block(itnn, jnn);
     }
   } else {
-    bool first = true;
+    // Two stages (S = 64): the same overlap with K and V prefetched at
+    // different distances.  At iteration c the wave reads K of chunk c+1 and
+    // V of chunk c; after the barrier K stage c (last read by the S MFMAs of
+    // iteration c-1) receives K of chunk c+2, i.e. chunk c of the next block,
+    // and V stage c+1 (last read by the PV of iteration c-1) receives V of
+    // chunk c+1.  Each iteration issues one K and one V group and waits for
+    // the previous iteration's, so the wait is for everything.
+    static_assert(NST == 2 && NCK == 2, "two-stage pipeline");
+    f32x16 sacc = f32x16{};
+    if (it < count) {
+      wait_vmcnt<0>();
+      wg_barrier();
+      qk(sacc, &Ks[0][0]);
+      const int valid = __builtin_amdgcn_readfirstlane(N - j * S);
+      if (valid < CK) mask_tail(sacc, valid);
+      float mx = sacc[0];                 // chunk 0 holds a valid key: finite
+#pragma unroll
+      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[r]);
+      m_ref = swap_halves_max(mx) * sl2;
+    }
     while (it < count) {
       const int itnn = itn + 1;
       int jnn = -1;
 #pragma unroll
       for (int c = 0; c < NCK; ++c) {
-        wait_vmcnt_lds_idle<2 * NUW * (PD - 1)>();
+        wait_vmcnt_lds_idle<0>();          // K of chunk c+1 and V of chunk c landed
         wg_barrier();
-        if (c + PD < NCK) fetch((c + PD) % NST, j * S + (c + PD) * CK);
-        else fetch((c + PD) % NST, jn >= 0 ? jn * S + (c + PD - NCK) * CK : 0);
+        fetch_k(c, jn >= 0 ? jn * S + c * CK : 0);
+        if (c + 1 < NCK) fetch_v(c + 1, j * S + (c + 1) * CK);
+        else fetch_v(0, jn >= 0 ? jn * S : 0);
         if (c == 0) jnn = itnn < count ? raw_at(itnn) : -1;
-        chunk(&Ks[c][0], &Vs[c][0], j * S + c * CK, c == 0 && first);
+        const int nkey0 = c + 1 < NCK ? j * S + (c + 1) * CK : (jn >= 0 ? jn * S : 0);
+        f32x16 snext;
+        bf16x8 pop[2];
+        qk(snext, &Ks[(c + 1) % NST][0]);
+        softmax(sacc, pop);
+        pv(pop, &Vs[c][0]);
+        const int nvalid = __builtin_amdgcn_readfirstlane(N - nkey0);
+        if (nvalid < CK) {
+          asm volatile("");        // keep this a real (rarely taken) branch, not select code
+          mask_tail(snext, nvalid);
+        }
+        sacc = snext;
       }
-      first = false;
       rescale_if_large();
       advance_block(itnn, jnn);
     }
