@@ -5,6 +5,10 @@ this package.  The GPU library never calls it, and it shares no code with the
 GPU path: every function here is a plain, slow, float64 restatement of what the
 path computes, written for a reader to check by eye.
 
+The fused QKNorm + RoPE + pool producer (Section 4.2.5 names "fused RoPE +
+norm"; Appendix A.2.2 lists fused QKNorm+RoPE in the LTX-2.3 stack) is in
+qknorm_rope.py with its own readings.
+
 What the paper fixes (Section 4.2.2, "Sparse Attention"; Appendix A.2.2, the
 LTX-2.3 pipeline): attention over the spatiotemporal token set is replaced by a
 block-sparse pattern; blocks are routed by a score ("score-based routing", a
@@ -23,6 +27,13 @@ Parity status per function:
   attention.block_sparse_attention / dense_attention
                               pinned (pure-Python brute force, torch SDPA in float64,
                                       closed forms, invariants)
+  qknorm_rope.round_bf16      pinned (bit-level float32 rounding, ties, double-rounding case)
+  qknorm_rope.rms_norm        pinned (closed forms, library norm, scale invariance)
+  qknorm_rope.rope_angles / apply_rope
+                              pinned (hand-derived angles, complex multiplication,
+                                      identity at the origin, norm, relative position)
+  qknorm_rope.qknorm_rope_pool
+                              pinned (pool of the rounded outputs; parts above)
   The paper's own routing rule and its Taylor remainder for non-kept blocks:
                               parity unpinned (not defined in the paper's text).
 """
@@ -30,10 +41,14 @@ from .blocks import bf16_bits_to_f64, num_blocks, block_bounds, pool_blocks
 from .select import (block_scores, topk_count, select_topk, first_frame_blocks,
                      mass_cap, select_cummass, kept_to_arrays, kept_to_mask)
 from .attention import block_sparse_attention, dense_attention
+from .qknorm_rope import (round_bf16, rms_norm, rope_pair_groups, rope_angles, apply_rope,
+                          qknorm_rope, qknorm_rope_pool)
 
 __all__ = [
     "bf16_bits_to_f64", "num_blocks", "block_bounds", "pool_blocks",
     "block_scores", "topk_count", "select_topk", "first_frame_blocks", "mass_cap",
     "select_cummass", "kept_to_arrays", "kept_to_mask",
     "block_sparse_attention", "dense_attention",
+    "round_bf16", "rms_norm", "rope_pair_groups", "rope_angles", "apply_rope", "qknorm_rope",
+    "qknorm_rope_pool",
 ]

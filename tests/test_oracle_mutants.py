@@ -117,3 +117,75 @@ def test_mutant_is_caught(name, mod, attr, fn, pins, monkeypatch, golden_dir):
     for pin in pins:
         with pytest.raises(AssertionError):
             pin(golden_dir)
+
+
+# ---- QKNorm + RoPE + pool ----
+import oracle.qknorm_rope as oqr  # noqa: E402
+
+from . import test_oracle_qknorm_rope as TQ  # noqa: E402
+
+
+def _rope_half_split(x, angles):
+    x = np.asarray(x, dtype=np.float64)
+    h = x.shape[-1] // 2
+    a, b = x[..., :h], x[..., h:]
+    c, s = np.cos(angles), np.sin(angles)
+    return np.concatenate([a * c - b * s, a * s + b * c], axis=-1)
+
+
+_ORIG_APPLY_ROPE = oqr.apply_rope
+
+
+def _rope_turned_backwards(x, angles):
+    return _ORIG_APPLY_ROPE(x, -np.asarray(angles))
+_ORIG_ROPE_ANGLES = oqr.rope_angles
+_ORIG_RMS_NORM = oqr.rms_norm
+_ORIG_ROUND = oqr.round_bf16
+
+
+def _angles_axes_reversed(grid, head_dim, base):
+    T, H, W = grid
+    ang = _ORIG_ROPE_ANGLES((W, H, T), head_dim, base)      # x treated as t and t as x
+    return ang.reshape(W, H, T, -1).transpose(2, 1, 0, 3).reshape(T * H * W, -1)
+
+
+def _rms_norm_without_eps(x, gamma, eps):
+    return _ORIG_RMS_NORM(x, gamma, 0.0)
+
+
+def _rms_norm_without_gamma(x, gamma, eps):
+    return _ORIG_RMS_NORM(x, np.ones_like(np.asarray(gamma, dtype=np.float64)), eps)
+
+
+def _round_via_float32(x):
+    return _ORIG_ROUND(np.asarray(x, dtype=np.float64).astype(np.float32).astype(np.float64))
+
+
+def _producer_pools_before_rounding(q, k, gamma_q, gamma_k, grid, block, eps, base):
+    qx = oqr.qknorm_rope(q, gamma_q, grid, eps, base)
+    kx = oqr.qknorm_rope(k, gamma_k, grid, eps, base)
+    return (oqr.round_bf16(qx), oqr.round_bf16(kx), oqr.pool_blocks(qx, block), oqr.pool_blocks(kx, block))
+
+
+QKR_MUTANTS = [
+    ("RoPE pairs split in halves", "apply_rope", _rope_half_split,
+     [TQ.test_rope_is_complex_multiplication]),
+    ("RoPE turned backwards", "apply_rope", _rope_turned_backwards,
+     [TQ.test_rope_is_complex_multiplication]),
+    ("RoPE axes in x, y, t order", "rope_angles", _angles_axes_reversed,
+     [TQ.test_rope_angles_hand_derived]),
+    ("RMSNorm without eps", "rms_norm", _rms_norm_without_eps, [TQ.test_rms_norm_closed_forms]),
+    ("RMSNorm without gamma", "rms_norm", _rms_norm_without_gamma, [TQ.test_rms_norm_closed_forms]),
+    ("bf16 rounding through float32", "round_bf16", _round_via_float32,
+     [TQ.test_round_bf16_ties_and_no_double_rounding]),
+    ("pooled before rounding", "qknorm_rope_pool", _producer_pools_before_rounding,
+     [TQ.test_producer_pools_its_rounded_outputs]),
+]
+
+
+@pytest.mark.parametrize("name,attr,fn,pins", QKR_MUTANTS, ids=[m[0] for m in QKR_MUTANTS])
+def test_qknorm_rope_mutant_is_caught(name, attr, fn, pins, monkeypatch):
+    monkeypatch.setattr(oqr, attr, fn)
+    for pin in pins:
+        with pytest.raises(AssertionError):
+            pin()
