@@ -42,13 +42,13 @@ from .select import (block_scores, topk_count, select_topk, first_frame_blocks,
                      mass_cap, select_cummass, kept_to_arrays, kept_to_mask)
 from .attention import block_sparse_attention, dense_attention
 from .qknorm_rope import (round_bf16, rms_norm, rope_pair_groups, rope_angles, apply_rope,
-                          qknorm_rope, qknorm_rope_pool)
+                          norm_rope, qknorm_rope_pool)
 
 __all__ = [
     "bf16_bits_to_f64", "num_blocks", "block_bounds", "pool_blocks",
     "block_scores", "topk_count", "select_topk", "first_frame_blocks", "mass_cap",
     "select_cummass", "kept_to_arrays", "kept_to_mask",
     "block_sparse_attention", "dense_attention",
-    "round_bf16", "rms_norm", "rope_pair_groups", "rope_angles", "apply_rope", "qknorm_rope",
+    "round_bf16", "rms_norm", "rope_pair_groups", "rope_angles", "apply_rope", "norm_rope",
     "qknorm_rope_pool",
 ]

@@ -84,7 +84,7 @@ def apply_rope(x: np.ndarray, angles: np.ndarray) -> np.ndarray:
     return out
 
 
-def qknorm_rope(x: np.ndarray, gamma: np.ndarray, grid, eps: float, base: float) -> np.ndarray:
+def norm_rope(x: np.ndarray, gamma: np.ndarray, grid, eps: float, base: float) -> np.ndarray:
     """RMSNorm then RoPE of x [B, H, N, D] (float64, not rounded)."""
     D = x.shape[-1]
     return apply_rope(rms_norm(x, gamma, eps), rope_angles(grid, D, base))
@@ -93,6 +93,6 @@ def qknorm_rope(x: np.ndarray, gamma: np.ndarray, grid, eps: float, base: float)
 def qknorm_rope_pool(q, k, gamma_q, gamma_k, grid, block: int, eps: float, base: float):
     """The fused producer: (q_out, k_out, q_pool, k_pool), outputs as float64
     holding bf16 values, summaries as float64 means of those outputs."""
-    q_out = round_bf16(qknorm_rope(q, gamma_q, grid, eps, base))
-    k_out = round_bf16(qknorm_rope(k, gamma_k, grid, eps, base))
+    q_out = round_bf16(norm_rope(q, gamma_q, grid, eps, base))
+    k_out = round_bf16(norm_rope(k, gamma_k, grid, eps, base))
     return q_out, k_out, pool_blocks(q_out, block), pool_blocks(k_out, block)

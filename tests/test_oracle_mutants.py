@@ -162,8 +162,8 @@ def _round_via_float32(x):
 
 
 def _producer_pools_before_rounding(q, k, gamma_q, gamma_k, grid, block, eps, base):
-    qx = oqr.qknorm_rope(q, gamma_q, grid, eps, base)
-    kx = oqr.qknorm_rope(k, gamma_k, grid, eps, base)
+    qx = oqr.norm_rope(q, gamma_q, grid, eps, base)
+    kx = oqr.norm_rope(k, gamma_k, grid, eps, base)
     return (oqr.round_bf16(qx), oqr.round_bf16(kx), oqr.pool_blocks(qx, block), oqr.pool_blocks(kx, block))
 
 

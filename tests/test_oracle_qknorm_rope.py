@@ -132,5 +132,5 @@ def test_producer_pools_its_rounded_outputs():
         assert np.allclose(pooled[..., 1, :], out[..., 16:32, :].mean(axis=-2), rtol=0, atol=1e-15)
         assert np.allclose(pooled[..., 3, :], out[..., 48:60, :].mean(axis=-2), rtol=0, atol=1e-15)
     # and the unrounded values are RMSNorm then RoPE
-    exact = oqr.qknorm_rope(q, gq, grid, 1e-6, 10000.0)
+    exact = oqr.norm_rope(q, gq, grid, 1e-6, 10000.0)
     assert np.max(np.abs(qo - exact) / np.maximum(np.abs(exact), 1e-30)) <= 2.0 ** -8
