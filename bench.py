@@ -280,6 +280,28 @@ def measure(args, wl, with_cpu: bool):
                                     "sparse_path_speedup": dense_ms / ms_step}
         del dout
 
+    # the fused QKNorm + RoPE + pool producer on the same Q and K (unit gamma):
+    # an alternative to the pool stage when Q and K arrive before their norm
+    gam = torch.ones(D, dtype=torch.float32, device="cuda")
+    qo, ko = torch.empty_like(dev["q"]), torch.empty_like(dev["k"])
+    sva.qknorm_rope_pool(prob, dev["q"], dev["k"], gam, gam, q_out=qo, k_out=ko, q_pool=qp, k_pool=kp,
+                         stream=stream)
+    a, b = ev(), ev()
+    a.record(stream)
+    for _ in range(args.steps):
+        sva.qknorm_rope_pool(prob, dev["q"], dev["k"], gam, gam, q_out=qo, k_out=ko, q_pool=qp,
+                             k_pool=kp, stream=stream)
+    b.record(stream)
+    torch.cuda.synchronize()
+    prod_ms = a.elapsed_time(b) / args.steps
+    prod_bytes = 4 * B * H * N * D * 2 + 2 * B * H * nb * D * 4 + 2 * D * 4
+    extra["qknorm_rope_pool"] = {
+        "ms": round(prod_ms, 4), "algorithmic_bytes": prod_bytes,
+        "hbm_gbs": round(prod_bytes / (prod_ms * 1e-3) / 1e9, 1),
+        "frac_of_hbm_peak": round(prod_bytes / (prod_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "replaces_pool_ms": round(pool_ms, 4)}
+    del qo, ko
+
     cpu = None
     if with_cpu:
         print(f"[bench] cpu baseline (~{args.cpu_seconds:.0f} s)", file=sys.stderr, flush=True)

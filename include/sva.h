@@ -93,7 +93,8 @@ typedef struct sva_select_params {
                                frame t = 0 (blocks j with j*S < grid_h*grid_w)      */
 } sva_select_params;
 
-/* Largest nB that sva_select_blocks accepts (block rows are selected in LDS). */
+/* Largest nB that sva_select_blocks accepts (a row's scores are held in
+ * registers, 32 per lane). */
 #define SVA_SELECT_MAX_BLOCKS 2048
 
 /* nB = ceil(N / S) for a validated problem.  Host only. */
@@ -112,6 +113,41 @@ int sva_max_keep(const sva_problem* prob, const sva_select_params* sel, int32_t*
  * float64 and rounded once to float32. */
 int sva_pool_blocks(const sva_problem* prob, const void* q, const void* k,
                     float* q_pool, float* k_pool, void* stream);
+
+/* RMSNorm and rotary-embedding parameters of sva_qknorm_rope_pool. */
+typedef struct sva_rope_params {
+  double eps;        /* RMSNorm epsilon, finite and >= 0 (e.g. 1e-6)              */
+  double rope_base;  /* rotary base, finite and > 1 (e.g. 10000)                   */
+} sva_rope_params;
+
+/* Step 1 fused with the producer of Q and K (Section 4.2.5 names fused
+ * RoPE + norm; Appendix A.2.2 lists fused QKNorm+RoPE in the LTX-2.3 stack;
+ * the paper prints no formula, so this is the reading implemented).  For every
+ * token of Q and of K:
+ *   y = x / sqrt(mean_d x_d^2 + eps) * gamma          RMSNorm over D
+ *   pair p = (y[2p], y[2p+1]) turned by the angle pos_a * base^(-i/n_a)
+ * where the D/2 pairs form contiguous groups for the t, y and x axes of sizes
+ * n_t = D/2 - 2*floor(D/6) and n_y = n_x = floor(D/6), i is the pair's index
+ * in its group and pos_a the token's coordinate on that axis (t-major raster
+ * order); a turn by phi maps (a, b) to (a cos phi - b sin phi,
+ * a sin phi + b cos phi).  The result is rounded once to bf16 (nearest, ties
+ * to even) and written, and the block summaries of step 1 are taken from the
+ * written values in the same pass: they equal what sva_pool_blocks gives for
+ * q_out and k_out.
+ *   q_in, k_in       : bf16 [B, H, N, D] device, 16-byte aligned
+ *   gamma_q, gamma_k : float32 [D] device, RMSNorm weights shared by the heads
+ *   q_out, k_out     : bf16 [B, H, N, D] device, 16-byte aligned, written; each
+ *                      may be its input (in place) but must not otherwise
+ *                      overlap it
+ *   q_pool, k_pool   : float32 [B, H, nB, D] device, written
+ * Float32 arithmetic; the rotation angle is reduced modulo one turn in
+ * float64 before its sine and cosine are taken.
+ * SVA_ERR_INVALID_ARG for a null pointer, eps < 0, rope_base <= 1 or a
+ * non-finite parameter. */
+int sva_qknorm_rope_pool(const sva_problem* prob, const sva_rope_params* rope,
+                         const void* q_in, const void* k_in, const float* gamma_q,
+                         const float* gamma_k, void* q_out, void* k_out,
+                         float* q_pool, float* k_pool, void* stream);
 
 /* Steps 2-3: block scores and block selection ("score-based routing",
  * Appendix A.2.2).

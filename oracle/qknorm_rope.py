@@ -23,7 +23,6 @@ list them):
 """
 from __future__ import annotations
 
-import math
 
 import numpy as np
 

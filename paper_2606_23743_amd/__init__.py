@@ -6,12 +6,14 @@ workload shapes.  Importing the package does not load the library; the first
 call into it does, and raises if libsva.so has not been built.
 """
 from . import workloads
-from ._lib import (SvaError, Problem, SelectParams, load, problem, problem_for, select_topk,
-                   select_mass, select_for, num_blocks, max_keep, pool_blocks, select_blocks,
-                   sparse_attention, dense_attention, status_string, LIB_PATH)
+from ._lib import (SvaError, Problem, SelectParams, RopeParams, load, problem, problem_for,
+                   select_topk, select_mass, select_for, num_blocks, max_keep, pool_blocks,
+                   qknorm_rope_pool, select_blocks, sparse_attention, dense_attention,
+                   status_string, LIB_PATH)
 
 __all__ = [
-    "workloads", "SvaError", "Problem", "SelectParams", "load", "problem", "problem_for",
-    "select_topk", "select_mass", "select_for", "num_blocks", "max_keep", "pool_blocks",
-    "select_blocks", "sparse_attention", "dense_attention", "status_string", "LIB_PATH",
+    "workloads", "SvaError", "Problem", "SelectParams", "RopeParams", "load", "problem",
+    "problem_for", "select_topk", "select_mass", "select_for", "num_blocks", "max_keep",
+    "pool_blocks", "qknorm_rope_pool", "select_blocks", "sparse_attention", "dense_attention",
+    "status_string", "LIB_PATH",
 ]

@@ -33,6 +33,10 @@ class Problem(ctypes.Structure):
                 ("softmax_scale", ctypes.c_double), ("out_dtype", ctypes.c_int32)]
 
 
+class RopeParams(ctypes.Structure):
+    _fields_ = [("eps", ctypes.c_double), ("rope_base", ctypes.c_double)]
+
+
 class SelectParams(ctypes.Structure):
     _fields_ = [("mode", ctypes.c_int32), ("keep_ratio", ctypes.c_double), ("topk", ctypes.c_int32),
                 ("mass_threshold", ctypes.c_double), ("max_keep_ratio", ctypes.c_double),
@@ -58,6 +62,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "sva_num_blocks": [P, i32p],
         "sva_max_keep": [P, S, i32p],
         "sva_pool_blocks": [P, vp, vp, vp, vp, vp],
+        "sva_qknorm_rope_pool": [P, ctypes.POINTER(RopeParams), vp, vp, vp, vp, vp, vp, vp, vp, vp],
         "sva_select_blocks": [P, S, vp, vp, ctypes.c_int32, vp, vp, vp, vp],
         "sva_sparse_attention": [P, vp, vp, vp, vp, vp, ctypes.c_int32, vp, vp, vp],
         "sva_dense_attention": [P, vp, vp, vp, vp, vp, vp],
@@ -185,6 +190,39 @@ def pool_blocks(prob: Problem, q, k, q_pool=None, k_pool=None, stream=None) -> T
     _check(load().sva_pool_blocks(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(q_pool), _ptr(k_pool),
                                   _stream(stream)), "sva_pool_blocks")
     return q_pool, k_pool
+
+
+def qknorm_rope_pool(prob: Problem, q_in, k_in, gamma_q, gamma_k, eps: float = 1e-6,
+                     rope_base: float = 10000.0, q_out=None, k_out=None, q_pool=None, k_pool=None,
+                     stream=None) -> Tuple:
+    """RMSNorm + 3-D RoPE of Q and K with the block summaries of the written
+    values (sva_qknorm_rope_pool).  q_out / k_out may be q_in / k_in (in place)."""
+    torch = _torch()
+    nb = num_blocks(prob)
+    shp = _qkv_shape(prob)
+    _need(q_in, torch.bfloat16, shp, "q_in")
+    _need(k_in, torch.bfloat16, shp, "k_in")
+    _need(gamma_q, torch.float32, (prob.head_dim,), "gamma_q")
+    _need(gamma_k, torch.float32, (prob.head_dim,), "gamma_k")
+    if q_out is None:
+        q_out = torch.empty_like(q_in)
+    if k_out is None:
+        k_out = torch.empty_like(k_in)
+    _need(q_out, torch.bfloat16, shp, "q_out")
+    _need(k_out, torch.bfloat16, shp, "k_out")
+    pshape = (prob.batch, prob.heads, nb, prob.head_dim)
+    if q_pool is None:
+        q_pool = torch.empty(pshape, dtype=torch.float32, device=q_in.device)
+    if k_pool is None:
+        k_pool = torch.empty(pshape, dtype=torch.float32, device=q_in.device)
+    _need(q_pool, torch.float32, pshape, "q_pool")
+    _need(k_pool, torch.float32, pshape, "k_pool")
+    rp = RopeParams(float(eps), float(rope_base))
+    _check(load().sva_qknorm_rope_pool(ctypes.byref(prob), ctypes.byref(rp), _ptr(q_in), _ptr(k_in),
+                                       _ptr(gamma_q), _ptr(gamma_k), _ptr(q_out), _ptr(k_out),
+                                       _ptr(q_pool), _ptr(k_pool), _stream(stream)),
+           "sva_qknorm_rope_pool")
+    return q_out, k_out, q_pool, k_pool
 
 
 def select_blocks(prob: Problem, sel: SelectParams, q_pool, k_pool, kmax: Optional[int] = None,

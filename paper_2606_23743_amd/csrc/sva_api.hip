@@ -143,6 +143,42 @@ int sva_pool_blocks(const sva_problem* prob, const void* q, const void* k, float
                                      static_cast<hipStream_t>(stream)));
 }
 
+int sva_qknorm_rope_pool(const sva_problem* prob, const sva_rope_params* rope, const void* q_in,
+                         const void* k_in, const float* gamma_q, const float* gamma_k, void* q_out,
+                         void* k_out, float* q_pool, float* k_pool, void* stream) {
+  Dims d;
+  const int st = check_problem(prob, &d);
+  if (st != SVA_OK) return st;
+  if (!rope || !q_in || !k_in || !gamma_q || !gamma_k || !q_out || !k_out || !q_pool || !k_pool)
+    return SVA_ERR_INVALID_ARG;
+  if (!isfinite(rope->eps) || rope->eps < 0.0 || !isfinite(rope->rope_base) || rope->rope_base <= 1.0)
+    return SVA_ERR_INVALID_ARG;
+  if (!aligned(q_in, 16) || !aligned(k_in, 16) || !aligned(q_out, 16) || !aligned(k_out, 16) ||
+      !aligned(gamma_q, 4) || !aligned(gamma_k, 4) || !aligned(q_pool, 4) || !aligned(k_pool, 4))
+    return SVA_ERR_ALIGNMENT;
+  // an output is either its input (in place) or disjoint from it
+  const size_t bytes = (size_t)d.B * d.H * d.N * d.D * 2;
+  auto overlap = [bytes](const void* x, const void* y) {
+    const uintptr_t a = reinterpret_cast<uintptr_t>(x), b = reinterpret_cast<uintptr_t>(y);
+    return a != b && a < b + bytes && b < a + bytes;
+  };
+  if (overlap(q_in, q_out) || overlap(k_in, k_out)) return SVA_ERR_INVALID_ARG;
+  sva::RopeArgs a{};
+  a.q_in = static_cast<const uint16_t*>(q_in);
+  a.k_in = static_cast<const uint16_t*>(k_in);
+  a.gamma_q = gamma_q;
+  a.gamma_k = gamma_k;
+  a.q_out = static_cast<uint16_t*>(q_out);
+  a.k_out = static_cast<uint16_t*>(k_out);
+  a.q_pool = q_pool;
+  a.k_pool = k_pool;
+  a.grid_h = prob->grid_h;
+  a.grid_w = prob->grid_w;
+  a.eps = (float)rope->eps;
+  a.base = rope->rope_base;
+  return hip_status(sva::launch_qknorm_rope_pool(d, a, static_cast<hipStream_t>(stream)));
+}
+
 int sva_select_blocks(const sva_problem* prob, const sva_select_params* sel, const float* q_pool,
                       const float* k_pool, int32_t kmax, int32_t* kv_idx, int32_t* kv_count,
                       uint8_t* mask, void* stream) {

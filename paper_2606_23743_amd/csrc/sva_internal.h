@@ -39,14 +39,28 @@ struct AttnArgs {
 // The rescaling (per-iteration online softmax) kernel; attention.hip.
 hipError_t launch_attention_rescaling(const Dims& d, bool sparse, const AttnArgs& a, hipStream_t stream);
 
-// 64-queries-per-wave attention with a fixed reference max; attention_q64.hip.
-hipError_t launch_attention_q64(const Dims& d, bool sparse, const AttnArgs& a, hipStream_t stream);
 // 32-queries-per-wave, two-waves-per-SIMD attention with a fixed reference max;
 // attention_q32.hip.
 hipError_t launch_attention_q32(const Dims& d, bool sparse, const AttnArgs& a, hipStream_t stream);
 
 hipError_t launch_pool(const Dims& d, const uint16_t* q, const uint16_t* k, float* q_pool,
                        float* k_pool, hipStream_t stream);
+
+// Arguments of the fused QKNorm + RoPE + pool producer; qknorm_rope.hip.
+struct RopeArgs {
+  const uint16_t* q_in;
+  const uint16_t* k_in;
+  const float* gamma_q;
+  const float* gamma_k;
+  uint16_t* q_out;
+  uint16_t* k_out;
+  float* q_pool;
+  float* k_pool;
+  int N, nB, S, n_rows, grid_h, grid_w;
+  float eps;
+  double base;
+};
+hipError_t launch_qknorm_rope_pool(const Dims& d, const RopeArgs& a, hipStream_t stream);
 
 hipError_t launch_select(const Dims& d, const SelectRule& r, const float* q_pool,
                          const float* k_pool, int kmax, int32_t* kv_idx, int32_t* kv_count,

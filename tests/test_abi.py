@@ -24,7 +24,7 @@ def test_every_declared_symbol_is_exported(lib):
     names = _lib.header_functions()
     assert set(names) >= {"sva_pool_blocks", "sva_select_blocks", "sva_sparse_attention",
                           "sva_dense_attention", "sva_num_blocks", "sva_max_keep",
-                          "sva_status_string", "sva_version"}
+                          "sva_qknorm_rope_pool", "sva_status_string", "sva_version"}
     for n in names:
         assert hasattr(lib, n), n
 
@@ -115,7 +115,7 @@ def test_compute_entry_points_reject_before_launch(lib):
         == _lib.SVA_ERR_ALIGNMENT
     big = sva.problem(1, 1, 2049 * 64, 64, (1, 1, 2049 * 64), 64)
     assert lib.sva_select_blocks(ctypes.byref(big), ctypes.byref(sel), A, A, 4, A, A, None, None) \
-        == _lib.SVA_ERR_UNSUPPORTED                              # nB above the LDS bound
+        == _lib.SVA_ERR_UNSUPPORTED                              # nB above the register bound
     assert lib.sva_sparse_attention(ctypes.byref(p), A, A, A, A, A, 0, A, None, None) == _lib.SVA_ERR_SHAPE
     assert lib.sva_sparse_attention(ctypes.byref(p), A, A, None, A, A, 4, A, None, None) \
         == _lib.SVA_ERR_INVALID_ARG
@@ -123,3 +123,21 @@ def test_compute_entry_points_reject_before_launch(lib):
         == _lib.SVA_ERR_ALIGNMENT
     assert lib.sva_dense_attention(ctypes.byref(p), A, A, A, None, None, None) == _lib.SVA_ERR_INVALID_ARG
     assert lib.sva_dense_attention(ctypes.byref(p), A, A, A, A, A + 2, None) == _lib.SVA_ERR_ALIGNMENT
+
+
+def test_qknorm_rope_pool_rejects_before_launch(lib):
+    p = sva.problem_for(workloads.TINY)
+    A = 1 << 20
+    B = A + (1 << 24)    # disjoint from A for this problem's 256 KB tensors
+    ok = _lib.RopeParams(1e-6, 10000.0)
+    f = lib.sva_qknorm_rope_pool
+    assert f(ctypes.byref(p), None, A, A, A, A, B, B, A, A, None) == _lib.SVA_ERR_INVALID_ARG
+    assert f(ctypes.byref(p), ctypes.byref(ok), None, A, A, A, B, B, A, A, None) == _lib.SVA_ERR_INVALID_ARG
+    for bad in (_lib.RopeParams(-1.0, 10000.0), _lib.RopeParams(1e-6, 1.0),
+                _lib.RopeParams(float("nan"), 10000.0), _lib.RopeParams(1e-6, float("inf"))):
+        assert f(ctypes.byref(p), ctypes.byref(bad), A, A, A, A, B, B, A, A, None) == _lib.SVA_ERR_INVALID_ARG
+    assert f(ctypes.byref(p), ctypes.byref(ok), A + 2, A, A, A, B, B, A, A, None) == _lib.SVA_ERR_ALIGNMENT
+    assert f(ctypes.byref(p), ctypes.byref(ok), A, A, A + 1, A, B, B, A, A, None) == _lib.SVA_ERR_ALIGNMENT
+    # an output that overlaps its input without being it
+    assert f(ctypes.byref(p), ctypes.byref(ok), A, A, A, A, A + 64, B, A, A, None) == _lib.SVA_ERR_INVALID_ARG
+    assert f(None, ctypes.byref(ok), A, A, A, A, B, B, A, A, None) == _lib.SVA_ERR_INVALID_ARG
