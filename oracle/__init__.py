@@ -7,7 +7,8 @@ path computes, written for a reader to check by eye.
 
 The fused QKNorm + RoPE + pool producer (Section 4.2.5 names "fused RoPE +
 norm"; Appendix A.2.2 lists fused QKNorm+RoPE in the LTX-2.3 stack) is in
-qknorm_rope.py with its own readings.
+qknorm_rope.py with its own readings; feat_norm token pruning (Section 4.2.3;
+Appendix A.2.2 keeps 50% of video tokens by that score) in token_prune.py.
 
 What the paper fixes (Section 4.2.2, "Sparse Attention"; Appendix A.2.2, the
 LTX-2.3 pipeline): attention over the spatiotemporal token set is replaced by a
@@ -34,6 +35,11 @@ Parity status per function:
                                       identity at the origin, norm, relative position)
   qknorm_rope.qknorm_rope_pool
                               pinned (pool of the rounded outputs; parts above)
+  token_prune.token_scores    pinned (library norm, closed forms, axis check)
+  token_prune.select_tokens   pinned (pure-Python sort with tie key, hand-worked example)
+  token_prune.keep_count      pinned (closed forms incl. the 0.1*1180 case)
+  token_prune.gather_tokens / scatter_tokens
+                              pinned (round trip, placement and base identities)
   The paper's own routing rule and its Taylor remainder for non-kept blocks:
                               parity unpinned (not defined in the paper's text).
 """
@@ -43,6 +49,7 @@ from .select import (block_scores, topk_count, select_topk, first_frame_blocks,
 from .attention import block_sparse_attention, dense_attention
 from .qknorm_rope import (round_bf16, rms_norm, rope_pair_groups, rope_angles, apply_rope,
                           norm_rope, qknorm_rope_pool)
+from .token_prune import token_scores, keep_count, select_tokens, gather_tokens, scatter_tokens
 
 __all__ = [
     "bf16_bits_to_f64", "num_blocks", "block_bounds", "pool_blocks",
@@ -50,5 +57,6 @@ __all__ = [
     "select_cummass", "kept_to_arrays", "kept_to_mask",
     "block_sparse_attention", "dense_attention",
     "round_bf16", "rms_norm", "rope_pair_groups", "rope_angles", "apply_rope", "norm_rope",
-    "qknorm_rope_pool",
+    "qknorm_rope_pool", "token_scores", "keep_count", "select_tokens", "gather_tokens",
+    "scatter_tokens",
 ]

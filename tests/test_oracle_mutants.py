@@ -5,6 +5,8 @@ wrong divisor, transposed operand, reversed tie-break, ...) on the CPU and runs
 the pins that should fail.  A pin set that let a mutant through would not pin
 the oracle.
 """
+import math
+
 import numpy as np
 import pytest
 
@@ -186,6 +188,67 @@ QKR_MUTANTS = [
 @pytest.mark.parametrize("name,attr,fn,pins", QKR_MUTANTS, ids=[m[0] for m in QKR_MUTANTS])
 def test_qknorm_rope_mutant_is_caught(name, attr, fn, pins, monkeypatch):
     monkeypatch.setattr(oqr, attr, fn)
+    for pin in pins:
+        with pytest.raises(AssertionError):
+            pin()
+
+
+# ---- token pruning ----
+import oracle.token_prune as otp  # noqa: E402
+
+from . import test_oracle_token_prune as TT  # noqa: E402
+
+_ORIG_SELECT_TOKENS = otp.select_tokens
+
+
+def _scores_over_tokens(x):
+    x = np.asarray(x, dtype=np.float64)
+    s = np.sum(x * x, axis=-2, keepdims=True)            # reduced over the wrong axis
+    return np.broadcast_to(s[..., 0], x.shape[:-1]).copy()
+
+
+def _select_high_index_wins(scores, k):
+    scores = np.asarray(scores, dtype=np.float64)
+    B, N = scores.shape
+    out = np.empty((B, k), dtype=np.int64)
+    idx = np.arange(N)
+    for b in range(B):
+        out[b] = np.sort(np.lexsort((-idx, -scores[b]))[:k])
+    return out
+
+
+def _select_unsorted(scores, k):
+    scores = np.asarray(scores, dtype=np.float64)
+    return np.stack([np.lexsort((np.arange(scores.shape[1]), -row))[:k] for row in scores])
+
+
+def _keep_count_floor(n_tokens, keep_ratio):
+    return max(1, min(int(n_tokens), int(math.floor(keep_ratio * n_tokens))))
+
+
+def _scatter_without_base(y_kept, kept, base):
+    out = np.zeros_like(np.asarray(base))
+    for b in range(out.shape[0]):
+        out[b, kept[b]] = y_kept[b]
+    return out
+
+
+TP_MUTANTS = [
+    ("scores over the token axis", "token_scores", _scores_over_tokens,
+     [TT.test_scores_are_squared_library_norms_and_closed_form]),
+    ("token ties go to the higher index", "select_tokens", _select_high_index_wins,
+     [TT.test_select_matches_python_sort_with_ties, TT.test_select_hand_worked]),
+    ("kept tokens not in ascending order", "select_tokens", _select_unsorted,
+     [TT.test_select_matches_python_sort_with_ties, TT.test_select_hand_worked]),
+    ("keep count rounded down", "keep_count", _keep_count_floor, [TT.test_keep_count]),
+    ("scatter drops the base rows", "scatter_tokens", _scatter_without_base,
+     [TT.test_gather_scatter_identities]),
+]
+
+
+@pytest.mark.parametrize("name,attr,fn,pins", TP_MUTANTS, ids=[m[0] for m in TP_MUTANTS])
+def test_token_prune_mutant_is_caught(name, attr, fn, pins, monkeypatch):
+    monkeypatch.setattr(otp, attr, fn)
     for pin in pins:
         with pytest.raises(AssertionError):
             pin()
