@@ -302,6 +302,39 @@ def measure(args, wl, with_cpu: bool):
         "replaces_pool_ms": round(pool_ms, 4)}
     del qo, ko
 
+    # feat_norm token pruning at keep ratio 0.5 on this workload's hidden
+    # states (the video stream's Q heads laid out token-major, [B, N, H*D])
+    x = dev["q"].permute(0, 2, 1, 3).reshape(B, N, H * D).contiguous()
+    C = H * D
+    scores, kept_idx, kept_pos = sva.token_select(x, 0.5, stream=stream)
+    ws = torch.empty(sva.token_select_workspace(sva.tokens(B, N, C)), dtype=torch.uint8, device="cuda")
+    kt = kept_idx.shape[1]
+    xk = sva.token_gather(x, kept_idx, stream=stream)
+    xo = torch.empty_like(x)
+    tp_ms = {}
+    for name, fn in (("select", lambda: sva.token_select(x, 0.5, scores, kept_idx, kept_pos, ws, stream)),
+                     ("gather", lambda: sva.token_gather(x, kept_idx, xk, stream)),
+                     ("scatter", lambda: sva.token_scatter(xk, kept_pos, x, xo, stream))):
+        fn()
+        a, b = ev(), ev()
+        a.record(stream)
+        for _ in range(args.steps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        tp_ms[name] = a.elapsed_time(b) / args.steps
+    tp_bytes = {"select": B * N * C * 2 + B * N * (8 + 4) + B * kt * 4,
+                "gather": 2 * B * kt * C * 2 + B * kt * 4,
+                "scatter": 2 * B * N * C * 2 + B * N * 4}
+    extra["token_prune"] = {
+        "hidden": [B, N, C], "keep_ratio": 0.5, "kept": kt,
+        "ms": {n: round(v, 4) for n, v in tp_ms.items()},
+        "algorithmic_bytes": tp_bytes,
+        "hbm_gbs": {n: round(tp_bytes[n] / (tp_ms[n] * 1e-3) / 1e9, 1) for n in tp_ms},
+        "frac_of_hbm_peak": {n: round(tp_bytes[n] / (tp_ms[n] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
+                             for n in tp_ms}}
+    del x, scores, kept_idx, kept_pos, ws, xk, xo
+
     cpu = None
     if with_cpu:
         print(f"[bench] cpu baseline (~{args.cpu_seconds:.0f} s)", file=sys.stderr, flush=True)

@@ -188,6 +188,57 @@ int sva_sparse_attention(const sva_problem* prob, const void* q, const void* k,
 int sva_dense_attention(const sva_problem* prob, const void* q, const void* k,
                         const void* v, void* out, float* lse, void* stream);
 
+/* ---- feat_norm token pruning (Section 4.2.3 token pruning; Appendix A.2.2
+ * keeps 50% of the video tokens by the feat_norm saliency score in the LTX-2.3
+ * refinement stage; the paper prints no formula, so this is the reading
+ * implemented).  Hidden states are bf16 [B, N, C] (C fastest), 16-byte
+ * aligned, C a multiple of 8. ---- */
+typedef struct sva_tokens {
+  int32_t batch;     /* B >= 1                                                   */
+  int32_t tokens;    /* N >= 1                                                   */
+  int32_t channels;  /* C >= 8, a multiple of 8                                  */
+} sva_tokens;
+
+/* Tokens kept per batch entry: k = clamp(ceil(r*N - 1e-6), 1, N) for a keep
+ * ratio r in (0, 1].  Host only. */
+int sva_token_keep_count(const sva_tokens* t, double keep_ratio, int32_t* k);
+
+/* Bytes of device workspace sva_token_select needs (batch * 33024).  Host only. */
+int sva_token_select_workspace(const sva_tokens* t, size_t* bytes);
+
+/* Scores and kept tokens.
+ *   x         : bf16 [B, N, C] device
+ *   scores    : float64 [B, N] device, written: sum over c of x[b, n, c]^2
+ *               (the squared L2 norm, accumulated in float64)
+ *   kept_idx  : int32 [B, k] device, written: per batch entry the k tokens
+ *               with the largest score (ties to the lower index), ascending
+ *   kept_pos  : int32 [B, N] device, written: a kept token's position in
+ *               kept_idx, -1 for a dropped token
+ *   workspace : device memory of at least sva_token_select_workspace bytes,
+ *               8-byte aligned, owned by the caller; its contents on entry do
+ *               not matter.  Calls that share a workspace must not overlap
+ *               (order them on one stream).
+ * k as sva_token_keep_count gives it.  For x holding Inf or NaN the choice
+ * among those tokens is unspecified (it stays within bounds).
+ * SVA_ERR_SHAPE when workspace_bytes is too small. */
+int sva_token_select(const sva_tokens* t, double keep_ratio, const void* x, double* scores,
+                     int32_t* kept_idx, int32_t* kept_pos, void* workspace, size_t workspace_bytes,
+                     void* stream);
+
+/* x_kept[b, j, :] = x[b, kept_idx[b, j], :] for j < k (an index outside
+ * [0, N) gives a row of zeros).
+ *   x: bf16 [B, N, C]; kept_idx: int32 [B, k]; x_kept: bf16 [B, k, C], written. */
+int sva_token_gather(const sva_tokens* t, int32_t k, const void* x, const int32_t* kept_idx,
+                     void* x_kept, void* stream);
+
+/* Reconstruction after the pruned span: out[b, n, :] = y_kept[b, p, :] where
+ * p = kept_pos[b, n] is in [0, k), else base[b, n, :] (a dropped token keeps
+ * its input).
+ *   y_kept: bf16 [B, k, C]; kept_pos: int32 [B, N]; base, out: bf16 [B, N, C];
+ *   out must not overlap y_kept; it may be base (in place). */
+int sva_token_scatter(const sva_tokens* t, int32_t k, const void* y_kept, const int32_t* kept_pos,
+                      const void* base, void* out, void* stream);
+
 /* Static text for a status code. */
 const char* sva_status_string(int status);
 

@@ -9,11 +9,13 @@ from . import workloads
 from ._lib import (SvaError, Problem, SelectParams, RopeParams, load, problem, problem_for,
                    select_topk, select_mass, select_for, num_blocks, max_keep, pool_blocks,
                    qknorm_rope_pool, select_blocks, sparse_attention, dense_attention,
-                   status_string, LIB_PATH)
+                   status_string, LIB_PATH, Tokens, tokens, token_keep_count, token_select,
+                   token_gather, token_scatter, token_select_workspace)
 
 __all__ = [
     "workloads", "SvaError", "Problem", "SelectParams", "RopeParams", "load", "problem",
     "problem_for", "select_topk", "select_mass", "select_for", "num_blocks", "max_keep",
     "pool_blocks", "qknorm_rope_pool", "select_blocks", "sparse_attention", "dense_attention",
-    "status_string", "LIB_PATH",
+    "status_string", "LIB_PATH", "Tokens", "tokens", "token_keep_count", "token_select",
+    "token_gather", "token_scatter", "token_select_workspace",
 ]

@@ -37,6 +37,10 @@ class RopeParams(ctypes.Structure):
     _fields_ = [("eps", ctypes.c_double), ("rope_base", ctypes.c_double)]
 
 
+class Tokens(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("tokens", ctypes.c_int32), ("channels", ctypes.c_int32)]
+
+
 class SelectParams(ctypes.Structure):
     _fields_ = [("mode", ctypes.c_int32), ("keep_ratio", ctypes.c_double), ("topk", ctypes.c_int32),
                 ("mass_threshold", ctypes.c_double), ("max_keep_ratio", ctypes.c_double),
@@ -66,6 +70,12 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "sva_select_blocks": [P, S, vp, vp, ctypes.c_int32, vp, vp, vp, vp],
         "sva_sparse_attention": [P, vp, vp, vp, vp, vp, ctypes.c_int32, vp, vp, vp],
         "sva_dense_attention": [P, vp, vp, vp, vp, vp, vp],
+        "sva_token_keep_count": [ctypes.POINTER(Tokens), ctypes.c_double, i32p],
+        "sva_token_select_workspace": [ctypes.POINTER(Tokens), ctypes.POINTER(ctypes.c_size_t)],
+        "sva_token_select": [ctypes.POINTER(Tokens), ctypes.c_double, vp, vp, vp, vp, vp,
+                             ctypes.c_size_t, vp],
+        "sva_token_gather": [ctypes.POINTER(Tokens), ctypes.c_int32, vp, vp, vp, vp],
+        "sva_token_scatter": [ctypes.POINTER(Tokens), ctypes.c_int32, vp, vp, vp, vp, vp],
         "sva_status_string": [ctypes.c_int],
         "sva_version": [],
     }
@@ -295,3 +305,91 @@ def dense_attention(prob: Problem, q, k, v, out=None, want_lse: bool = False, ls
     _check(load().sva_dense_attention(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(out),
                                       _ptr(lse), _stream(stream)), "sva_dense_attention")
     return out, lse
+
+
+# ------------------------------------------------------------- token pruning
+
+def tokens(batch: int, n_tokens: int, channels: int) -> Tokens:
+    return Tokens(int(batch), int(n_tokens), int(channels))
+
+
+def token_keep_count(t: Tokens, keep_ratio: float) -> int:
+    out = ctypes.c_int32(0)
+    _check(load().sva_token_keep_count(ctypes.byref(t), float(keep_ratio), ctypes.byref(out)),
+           "sva_token_keep_count")
+    return out.value
+
+
+def token_select_workspace(t: Tokens) -> int:
+    out = ctypes.c_size_t(0)
+    _check(load().sva_token_select_workspace(ctypes.byref(t), ctypes.byref(out)),
+           "sva_token_select_workspace")
+    return out.value
+
+
+def token_select(x, keep_ratio: float, scores=None, kept_idx=None, kept_pos=None,
+                 workspace=None, stream=None) -> Tuple:
+    """feat_norm scores and kept tokens of hidden states x (bf16 [B, N, C]),
+    sva_token_select: returns (scores float64 [B, N], kept_idx int32 [B, k]
+    ascending, kept_pos int32 [B, N] with -1 for dropped tokens).  workspace:
+    a uint8 device tensor of token_select_workspace bytes (allocated when
+    None; pass one to reuse it)."""
+    torch = _torch()
+    if x.dim() != 3:
+        raise ValueError("x must be [B, N, C]")
+    B, N, C = x.shape
+    t = tokens(B, N, C)
+    k = token_keep_count(t, keep_ratio)
+    _need(x, torch.bfloat16, (B, N, C), "x")
+    if scores is None:
+        scores = torch.empty((B, N), dtype=torch.float64, device=x.device)
+    if kept_idx is None:
+        kept_idx = torch.empty((B, k), dtype=torch.int32, device=x.device)
+    if kept_pos is None:
+        kept_pos = torch.empty((B, N), dtype=torch.int32, device=x.device)
+    _need(scores, torch.float64, (B, N), "scores")
+    _need(kept_idx, torch.int32, (B, k), "kept_idx")
+    _need(kept_pos, torch.int32, (B, N), "kept_pos")
+    ws_bytes = token_select_workspace(t)
+    if workspace is None:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=x.device)
+    if not (isinstance(workspace, torch.Tensor) and workspace.is_cuda and workspace.is_contiguous()
+            and workspace.numel() * workspace.element_size() >= ws_bytes):
+        raise ValueError(f"workspace must be a contiguous device tensor of >= {ws_bytes} bytes")
+    _check(load().sva_token_select(ctypes.byref(t), float(keep_ratio), _ptr(x), _ptr(scores),
+                                   _ptr(kept_idx), _ptr(kept_pos), _ptr(workspace),
+                                   workspace.numel() * workspace.element_size(), _stream(stream)),
+           "sva_token_select")
+    return scores, kept_idx, kept_pos
+
+
+def token_gather(x, kept_idx, x_kept=None, stream=None):
+    """x_kept[b, j] = x[b, kept_idx[b, j]] (sva_token_gather)."""
+    torch = _torch()
+    B, N, C = x.shape
+    k = kept_idx.shape[1]
+    _need(x, torch.bfloat16, (B, N, C), "x")
+    _need(kept_idx, torch.int32, (B, k), "kept_idx")
+    if x_kept is None:
+        x_kept = torch.empty((B, k, C), dtype=torch.bfloat16, device=x.device)
+    _need(x_kept, torch.bfloat16, (B, k, C), "x_kept")
+    _check(load().sva_token_gather(ctypes.byref(tokens(B, N, C)), k, _ptr(x), _ptr(kept_idx),
+                                   _ptr(x_kept), _stream(stream)), "sva_token_gather")
+    return x_kept
+
+
+def token_scatter(y_kept, kept_pos, base, out=None, stream=None):
+    """out[b, n] = y_kept[b, kept_pos[b, n]] for kept tokens, base[b, n] for the
+    others (sva_token_scatter); out may be base (in place)."""
+    torch = _torch()
+    B, N, C = base.shape
+    k = y_kept.shape[1]
+    _need(y_kept, torch.bfloat16, (B, k, C), "y_kept")
+    _need(kept_pos, torch.int32, (B, N), "kept_pos")
+    _need(base, torch.bfloat16, (B, N, C), "base")
+    if out is None:
+        out = torch.empty_like(base)
+    _need(out, torch.bfloat16, (B, N, C), "out")
+    _check(load().sva_token_scatter(ctypes.byref(tokens(B, N, C)), k, _ptr(y_kept), _ptr(kept_pos),
+                                    _ptr(base), _ptr(out), _stream(stream)), "sva_token_scatter")
+    return out

@@ -50,6 +50,14 @@ int check_problem(const sva_problem* p, Dims* d) {
   return SVA_OK;
 }
 
+int check_tokens(const sva_tokens* t) {
+  if (!t) return SVA_ERR_INVALID_ARG;
+  if (t->batch < 1 || t->tokens < 1 || t->channels < 8 || t->channels % 8 != 0) return SVA_ERR_INVALID_ARG;
+  // row offsets are formed in 64-bit, row counts in 32-bit
+  if ((int64_t)t->batch * t->tokens > INT32_MAX) return SVA_ERR_SHAPE;
+  return SVA_OK;
+}
+
 int check_select(const sva_select_params* s, const Dims& d, SelectRule* r) {
   if (!s) return SVA_ERR_INVALID_ARG;
   SelectRule out{};
@@ -177,6 +185,76 @@ int sva_qknorm_rope_pool(const sva_problem* prob, const sva_rope_params* rope, c
   a.eps = (float)rope->eps;
   a.base = rope->rope_base;
   return hip_status(sva::launch_qknorm_rope_pool(d, a, static_cast<hipStream_t>(stream)));
+}
+
+int sva_token_keep_count(const sva_tokens* t, double keep_ratio, int32_t* k) {
+  if (!k) return SVA_ERR_INVALID_ARG;
+  const int st = check_tokens(t);
+  if (st != SVA_OK) return st;
+  if (!(keep_ratio > 0.0) || keep_ratio > 1.0) return SVA_ERR_INVALID_ARG;
+  int64_t kk = (int64_t)ceil(keep_ratio * t->tokens - kCountEps);
+  if (kk < 1) kk = 1;
+  if (kk > t->tokens) kk = t->tokens;
+  *k = (int32_t)kk;
+  return SVA_OK;
+}
+
+int sva_token_select_workspace(const sva_tokens* t, size_t* bytes) {
+  if (!bytes) return SVA_ERR_INVALID_ARG;
+  const int st = check_tokens(t);
+  if (st != SVA_OK) return st;
+  *bytes = (size_t)t->batch * sva::kTokenSelectWsStride;
+  return SVA_OK;
+}
+
+int sva_token_select(const sva_tokens* t, double keep_ratio, const void* x, double* scores,
+                     int32_t* kept_idx, int32_t* kept_pos, void* workspace, size_t workspace_bytes,
+                     void* stream) {
+  int32_t k;
+  const int st = sva_token_keep_count(t, keep_ratio, &k);
+  if (st != SVA_OK) return st;
+  if (!x || !scores || !kept_idx || !kept_pos || !workspace) return SVA_ERR_INVALID_ARG;
+  if (workspace_bytes < (size_t)t->batch * sva::kTokenSelectWsStride) return SVA_ERR_SHAPE;
+  if (!aligned(x, 16) || !aligned(scores, 8) || !aligned(kept_idx, 4) || !aligned(kept_pos, 4) ||
+      !aligned(workspace, 8))
+    return SVA_ERR_ALIGNMENT;
+  return hip_status(sva::launch_token_select(t->batch, t->tokens, t->channels, k,
+                                             static_cast<const uint16_t*>(x), scores, kept_idx,
+                                             kept_pos, workspace, static_cast<hipStream_t>(stream)));
+}
+
+int sva_token_gather(const sva_tokens* t, int32_t k, const void* x, const int32_t* kept_idx,
+                     void* x_kept, void* stream) {
+  const int st = check_tokens(t);
+  if (st != SVA_OK) return st;
+  if (k < 1 || k > t->tokens) return SVA_ERR_SHAPE;
+  if (!x || !kept_idx || !x_kept) return SVA_ERR_INVALID_ARG;
+  if (!aligned(x, 16) || !aligned(x_kept, 16) || !aligned(kept_idx, 4)) return SVA_ERR_ALIGNMENT;
+  return hip_status(sva::launch_token_gather(t->batch, t->tokens, t->channels, k,
+                                             static_cast<const uint16_t*>(x), kept_idx,
+                                             static_cast<uint16_t*>(x_kept),
+                                             static_cast<hipStream_t>(stream)));
+}
+
+int sva_token_scatter(const sva_tokens* t, int32_t k, const void* y_kept, const int32_t* kept_pos,
+                      const void* base, void* out, void* stream) {
+  const int st = check_tokens(t);
+  if (st != SVA_OK) return st;
+  if (k < 1 || k > t->tokens) return SVA_ERR_SHAPE;
+  if (!y_kept || !kept_pos || !base || !out) return SVA_ERR_INVALID_ARG;
+  if (!aligned(y_kept, 16) || !aligned(base, 16) || !aligned(out, 16) || !aligned(kept_pos, 4))
+    return SVA_ERR_ALIGNMENT;
+  const uintptr_t o = reinterpret_cast<uintptr_t>(out), y = reinterpret_cast<uintptr_t>(y_kept);
+  const size_t out_bytes = (size_t)t->batch * t->tokens * t->channels * 2;
+  const size_t y_bytes = (size_t)t->batch * k * t->channels * 2;
+  if (o < y + y_bytes && y < o + out_bytes) return SVA_ERR_INVALID_ARG;   // out overlaps y_kept
+  const uintptr_t bs = reinterpret_cast<uintptr_t>(base);
+  if (bs != o && bs < o + out_bytes && o < bs + out_bytes) return SVA_ERR_INVALID_ARG;
+  return hip_status(sva::launch_token_scatter(t->batch, t->tokens, t->channels, k,
+                                              static_cast<const uint16_t*>(y_kept), kept_pos,
+                                              static_cast<const uint16_t*>(base),
+                                              static_cast<uint16_t*>(out),
+                                              static_cast<hipStream_t>(stream)));
 }
 
 int sva_select_blocks(const sva_problem* prob, const sva_select_params* sel, const float* q_pool,

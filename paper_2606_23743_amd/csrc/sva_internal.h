@@ -62,6 +62,18 @@ struct RopeArgs {
 };
 hipError_t launch_qknorm_rope_pool(const Dims& d, const RopeArgs& a, hipStream_t stream);
 
+// feat_norm token pruning; token_prune.hip.
+// Device workspace of the token selection: one slice of this many bytes per batch entry.
+constexpr size_t kTokenSelectWsStride = 33024;
+hipError_t launch_token_select(int B, int N, int C, int k, const uint16_t* x, double* scores,
+                               int32_t* kept_idx, int32_t* kept_pos, void* workspace,
+                               hipStream_t stream);
+hipError_t launch_token_gather(int B, int N, int C, int k, const uint16_t* x, const int32_t* kept_idx,
+                               uint16_t* x_kept, hipStream_t stream);
+hipError_t launch_token_scatter(int B, int N, int C, int k, const uint16_t* y_kept,
+                                const int32_t* kept_pos, const uint16_t* base, uint16_t* out,
+                                hipStream_t stream);
+
 hipError_t launch_select(const Dims& d, const SelectRule& r, const float* q_pool,
                          const float* k_pool, int kmax, int32_t* kv_idx, int32_t* kv_count,
                          uint8_t* mask, hipStream_t stream);

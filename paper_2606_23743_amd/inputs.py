@@ -102,6 +102,39 @@ def generate(wl: Workload, seed: int | None = None) -> Dict[str, np.ndarray]:
     return out
 
 
+def hidden_states(batch: int, n_tokens: int, channels: int, seed: int,
+                  dup_frac: float = 0.05, n_zero: int = 2) -> np.ndarray:
+    """Seeded transformer hidden states, uint16 bf16 bits [B, N, C].
+
+    Recipe: per token a log-normal scale exp(0.5 g), g ~ N(0, 1), times
+    N(0, 1) channel values, rounded once to bf16; then per batch entry a
+    fraction dup_frac of the tokens are overwritten with copies of other
+    tokens' rows (bit-identical rows: exact score ties between tokens far
+    apart), and n_zero tokens are set to zero rows (ties at the lowest score).
+    """
+    root = np.random.SeedSequence(seed)
+    seqs = root.spawn(batch)
+    out = np.empty((batch, n_tokens, channels), dtype=np.uint16)
+
+    def fill(b):
+        g = np.random.Generator(np.random.PCG64(seqs[b]))
+        scale = np.exp(0.5 * g.standard_normal(n_tokens)).astype(np.float32)
+        n_dup = int(dup_frac * n_tokens)
+        dst = g.choice(n_tokens, size=n_dup + min(n_zero, n_tokens), replace=False)
+        src = g.integers(0, n_tokens, size=n_dup)
+        step = 8192
+        for s0 in range(0, n_tokens, step):
+            z = g.standard_normal((min(step, n_tokens - s0), channels), dtype=np.float32)
+            z *= scale[s0:s0 + step, None]
+            out[b, s0:s0 + step] = _round_bf16(z)
+        out[b, dst[:n_dup]] = out[b, src]
+        out[b, dst[n_dup:]] = 0
+
+    with ThreadPoolExecutor(min(_workers(), batch)) as ex:
+        list(ex.map(fill, range(batch)))
+    return out
+
+
 def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
     """Exact widening of bf16 bit patterns to float32 (for plumbing and tests)."""
     return (bits.astype(np.uint32) << np.uint32(16)).view(np.float32)

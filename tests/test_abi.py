@@ -24,7 +24,10 @@ def test_every_declared_symbol_is_exported(lib):
     names = _lib.header_functions()
     assert set(names) >= {"sva_pool_blocks", "sva_select_blocks", "sva_sparse_attention",
                           "sva_dense_attention", "sva_num_blocks", "sva_max_keep",
-                          "sva_qknorm_rope_pool", "sva_status_string", "sva_version"}
+                          "sva_qknorm_rope_pool", "sva_token_keep_count", "sva_token_select",
+                          "sva_token_select_workspace",
+                          "sva_token_gather", "sva_token_scatter", "sva_status_string",
+                          "sva_version"}
     for n in names:
         assert hasattr(lib, n), n
 
@@ -141,3 +144,48 @@ def test_qknorm_rope_pool_rejects_before_launch(lib):
     # an output that overlaps its input without being it
     assert f(ctypes.byref(p), ctypes.byref(ok), A, A, A, A, A + 64, B, A, A, None) == _lib.SVA_ERR_INVALID_ARG
     assert f(None, ctypes.byref(ok), A, A, A, A, B, B, A, A, None) == _lib.SVA_ERR_INVALID_ARG
+
+
+def test_token_keep_count_matches_the_oracle_reading():
+    import oracle.token_prune as otp
+    for n, r in ((111600, 0.5), (1180, 0.1), (10, 0.25), (7, 1e-9), (7, 1.0), (3, 0.34)):
+        assert sva.token_keep_count(sva.tokens(2, n, 8), r) == otp.keep_count(n, r), (n, r)
+
+
+def test_token_entry_points_reject_before_launch(lib):
+    A = 1 << 20
+    B = A + (1 << 26)
+    t = sva.tokens(2, 100, 64)
+    k = ctypes.c_int32()
+    for bad in (sva.tokens(0, 100, 64), sva.tokens(1, 0, 64), sva.tokens(1, 100, 4), sva.tokens(1, 100, 12)):
+        assert lib.sva_token_keep_count(ctypes.byref(bad), 0.5, ctypes.byref(k)) == _lib.SVA_ERR_INVALID_ARG
+    assert lib.sva_token_keep_count(ctypes.byref(sva.tokens(1 << 16, 1 << 16, 8)), 0.5, ctypes.byref(k)) \
+        == _lib.SVA_ERR_SHAPE                                    # B*N beyond int32
+    for r in (0.0, -0.5, 1.0000001, float("nan")):
+        assert lib.sva_token_keep_count(ctypes.byref(t), r, ctypes.byref(k)) == _lib.SVA_ERR_INVALID_ARG
+    assert lib.sva_token_keep_count(ctypes.byref(t), 0.5, None) == _lib.SVA_ERR_INVALID_ARG
+    ws = ctypes.c_size_t()
+    assert lib.sva_token_select_workspace(ctypes.byref(t), ctypes.byref(ws)) == _lib.SVA_OK
+    assert ws.value == 2 * 33024 and sva.token_select_workspace(t) == ws.value
+    assert lib.sva_token_select_workspace(ctypes.byref(t), None) == _lib.SVA_ERR_INVALID_ARG
+    W = ws.value
+    sel = lib.sva_token_select
+    assert sel(ctypes.byref(t), 0.5, None, A, A, A, B, W, None) == _lib.SVA_ERR_INVALID_ARG
+    assert sel(ctypes.byref(t), 0.5, A, A, A, A, None, W, None) == _lib.SVA_ERR_INVALID_ARG
+    assert sel(ctypes.byref(t), 0.5, A, A, A, A, B, W - 1, None) == _lib.SVA_ERR_SHAPE
+    assert sel(ctypes.byref(t), 0.5, A + 8, A, A, A, B, W, None) == _lib.SVA_ERR_ALIGNMENT
+    assert sel(ctypes.byref(t), 0.5, A, A + 4, A, A, B, W, None) == _lib.SVA_ERR_ALIGNMENT
+    assert sel(ctypes.byref(t), 0.5, A, A, A, A, B + 4, W, None) == _lib.SVA_ERR_ALIGNMENT
+    assert sel(ctypes.byref(t), 2.0, A, A, A, A, B, W, None) == _lib.SVA_ERR_INVALID_ARG
+    g = lib.sva_token_gather
+    assert g(ctypes.byref(t), 0, A, A, B, None) == _lib.SVA_ERR_SHAPE
+    assert g(ctypes.byref(t), 101, A, A, B, None) == _lib.SVA_ERR_SHAPE
+    assert g(ctypes.byref(t), 50, A, None, B, None) == _lib.SVA_ERR_INVALID_ARG
+    assert g(ctypes.byref(t), 50, A, A + 2, B, None) == _lib.SVA_ERR_ALIGNMENT
+    sc = lib.sva_token_scatter
+    assert sc(ctypes.byref(t), 50, A, A, B, None, None) == _lib.SVA_ERR_INVALID_ARG
+    assert sc(ctypes.byref(t), 50, A + 8, A, B, B, None) == _lib.SVA_ERR_ALIGNMENT
+    # out overlapping y_kept, and a base that overlaps out without being it
+    assert sc(ctypes.byref(t), 50, A, A, B, A + 256, None) == _lib.SVA_ERR_INVALID_ARG
+    assert sc(ctypes.byref(t), 50, A, A, B + 256, B, None) == _lib.SVA_ERR_INVALID_ARG
+    assert sc(None, 50, A, A, B, B, None) == _lib.SVA_ERR_INVALID_ARG
