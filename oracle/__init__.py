@@ -8,7 +8,9 @@ path computes, written for a reader to check by eye.
 The fused QKNorm + RoPE + pool producer (Section 4.2.5 names "fused RoPE +
 norm"; Appendix A.2.2 lists fused QKNorm+RoPE in the LTX-2.3 stack) is in
 qknorm_rope.py with its own readings; feat_norm token pruning (Section 4.2.3;
-Appendix A.2.2 keeps 50% of video tokens by that score) in token_prune.py.
+Appendix A.2.2 keeps 50% of video tokens by that score) in token_prune.py;
+8-bit attention (Section 4.2.4 points to the SageAttention series) in
+fp8_attention.py.
 
 What the paper fixes (Section 4.2.2, "Sparse Attention"; Appendix A.2.2, the
 LTX-2.3 pipeline): attention over the spatiotemporal token set is replaced by a
@@ -40,6 +42,15 @@ Parity status per function:
   token_prune.keep_count      pinned (closed forms incl. the 0.1*1180 case)
   token_prune.gather_tokens / scatter_tokens
                               pinned (round trip, placement and base identities)
+  fp8_attention.round_e4m3 / e4m3_value / encode_e4m3
+                              pinned (format code table, brute-force nearest-even
+                                      search, library float32 cast)
+  fp8_attention.scale_exponent / quantize_qkv
+                              pinned (brute-force exponents, pure-Python grouping
+                                      and codes, error bounds)
+  fp8_attention.fp8_block_sparse_attention
+                              pinned (smoothing invariance, exactly representable
+                                      inputs equal plain attention)
   The paper's own routing rule and its Taylor remainder for non-kept blocks:
                               parity unpinned (not defined in the paper's text).
 """
@@ -50,6 +61,8 @@ from .attention import block_sparse_attention, dense_attention
 from .qknorm_rope import (round_bf16, rms_norm, rope_pair_groups, rope_angles, apply_rope,
                           norm_rope, qknorm_rope_pool)
 from .token_prune import token_scores, keep_count, select_tokens, gather_tokens, scatter_tokens
+from .fp8_attention import (e4m3_value, round_e4m3, encode_e4m3, scale_exponent, quantize_qkv,
+                            fp8_block_sparse_attention)
 
 __all__ = [
     "bf16_bits_to_f64", "num_blocks", "block_bounds", "pool_blocks",
@@ -58,5 +71,7 @@ __all__ = [
     "block_sparse_attention", "dense_attention",
     "round_bf16", "rms_norm", "rope_pair_groups", "rope_angles", "apply_rope", "norm_rope",
     "qknorm_rope_pool", "token_scores", "keep_count", "select_tokens", "gather_tokens",
+    "e4m3_value", "round_e4m3", "encode_e4m3", "scale_exponent", "quantize_qkv",
+    "fp8_block_sparse_attention",
     "scatter_tokens",
 ]

@@ -14,10 +14,12 @@ import oracle
 import oracle.attention as oatt
 import oracle.blocks as oblk
 import oracle.select as osel
+import oracle.fp8_attention as of8
 
 from . import test_oracle_attention as TA
 from . import test_oracle_pool as TP
 from . import test_oracle_select as TS
+from . import test_oracle_fp8 as TF8
 
 pytestmark = pytest.mark.cpu
 
@@ -251,4 +253,60 @@ def test_token_prune_mutant_is_caught(name, attr, fn, pins, monkeypatch):
     monkeypatch.setattr(otp, attr, fn)
     for pin in pins:
         with pytest.raises(AssertionError):
+            pin()
+
+
+# ---- fp8 quantisation ----
+
+def _e4m3_half_away(x):
+    x = np.asarray(x, dtype=np.float64)
+    out = np.zeros_like(x)
+    nz = x != 0
+    _, e = np.frexp(x[nz])
+    q = np.ldexp(1.0, np.maximum(e - 4, -9))
+    out[nz] = np.sign(x[nz]) * np.floor(np.abs(x[nz]) / q + 0.5) * q
+    return out
+
+
+def _e4m3_subnormal_step_too_fine(x):
+    x = np.asarray(x, dtype=np.float64)
+    out = np.zeros_like(x)
+    nz = x != 0
+    _, e = np.frexp(x[nz])
+    q = np.ldexp(1.0, np.maximum(e - 4, -10))
+    out[nz] = np.rint(x[nz] / q) * q
+    return out
+
+
+_true_scale_exponent = of8.scale_exponent
+
+
+def _scale_exponent_floor(amax):
+    if amax == 0:
+        return 0
+    return int(math.floor(math.log2(amax / 448.0)))
+
+
+def _no_smoothing(k):
+    k = np.asarray(k, dtype=np.float64)
+    return np.zeros(k.shape[:2] + k.shape[3:])
+
+
+FP8_MUTANTS = [
+    ("e4m3 ties away from zero", "round_e4m3", _e4m3_half_away,
+     [TF8.test_rounding_matches_brute_force_nearest_even]),
+    ("e4m3 subnormal spacing 2^-10", "round_e4m3", _e4m3_subnormal_step_too_fine,
+     [TF8.test_rounding_matches_brute_force_nearest_even]),
+    ("scale exponent rounded down", "scale_exponent", _scale_exponent_floor,
+     [TF8.test_scale_exponent_brute_force]),
+    ("no K smoothing", "k_smooth_mean", _no_smoothing,
+     [TF8.test_quantize_qkv_matches_pure_python_grouping]),
+]
+
+
+@pytest.mark.parametrize("name,attr,fn,pins", FP8_MUTANTS, ids=[m[0] for m in FP8_MUTANTS])
+def test_fp8_mutant_is_caught(name, attr, fn, pins, monkeypatch):
+    monkeypatch.setattr(of8, attr, fn)
+    for pin in pins:
+        with pytest.raises((AssertionError, ValueError)):
             pin()
