@@ -33,6 +33,7 @@ if ROOT not in sys.path:
 
 METRIC = "effective TFLOP/s of sparse attention (kept blocks) + % bf16 MFMA peak"
 BF16_PEAK_TFLOPS = 2516.6   # 256 CU x 2.4 GHz x 4096 dense bf16 flop/clk/CU
+FP8_PEAK_TFLOPS = 5033.2   # dense fp8 MFMA: twice the bf16 rate
 HBM_PEAK_GBS = 8000.0
 
 
@@ -301,6 +302,38 @@ def measure(args, wl, with_cpu: bool):
         "frac_of_hbm_peak": round(prod_bytes / (prod_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "replaces_pool_ms": round(pool_ms, 4)}
     del qo, ko
+
+    # 8-bit (e4m3) attention on the same layer and kept-block lists: the
+    # quantiser once, then the fp8 kernel (kept FLOPs against the fp8 peak)
+    if wl.head_dim in (64, 128):
+        quant = sva.quantize_fp8(prob, dev["q"], dev["k"], dev["v"], stream=stream)
+        o8 = torch.empty_like(out)
+        sva.sparse_attention_fp8(prob, quant, idx, cnt, out=o8, stream=stream)
+        fp8_ms = {}
+        for name, fn in (("quantize", lambda: sva.quantize_fp8(prob, dev["q"], dev["k"], dev["v"], out=quant,
+                                                                 stream=stream)),
+                         ("attention", lambda: sva.sparse_attention_fp8(prob, quant, idx, cnt, out=o8,
+                                                                        stream=stream))):
+            a, b = ev(), ev()
+            a.record(stream)
+            for _ in range(args.steps):
+                fn()
+            b.record(stream)
+            torch.cuda.synchronize()
+            fp8_ms[name] = a.elapsed_time(b) / args.steps
+        sva.sparse_attention(prob, dev["q"], dev["k"], dev["v"], idx, cnt, out=out, stream=stream)
+        torch.cuda.synchronize()
+        diff = (o8.float() - out.float()).abs()
+        fp8_tf = flops / (fp8_ms["attention"] * 1e-3) / 1e12
+        extra["fp8_attention"] = {
+            "format": "e4m3 Q, K (smoothed), V and P; power-of-two scales",
+            "quantize_ms": round(fp8_ms["quantize"], 4), "attention_ms": round(fp8_ms["attention"], 4),
+            "attention_tflops": round(fp8_tf, 2),
+            "frac_of_fp8_peak": round(fp8_tf / FP8_PEAK_TFLOPS, 4),
+            "frac_of_bf16_peak": round(fp8_tf / BF16_PEAK_TFLOPS, 4),
+            "speedup_vs_bf16_attention": round(att_ms / fp8_ms["attention"], 3),
+            "mean_abs_diff_vs_bf16_path": float(diff.mean()), "max_abs_diff_vs_bf16_path": float(diff.max())}
+        del quant, o8, diff
 
     # feat_norm token pruning at keep ratio 0.5 on this workload's hidden
     # states (the video stream's Q heads laid out token-major, [B, N, H*D])

@@ -239,6 +239,49 @@ int sva_token_gather(const sva_tokens* t, int32_t k, const void* x, const int32_
 int sva_token_scatter(const sva_tokens* t, int32_t k, const void* y_kept, const int32_t* kept_pos,
                       const void* base, void* out, void* stream);
 
+/* ---- 8-bit (fp8 e4m3) attention (Section 4.2.4 points to the SageAttention
+ * series: 8-bit attention with outlier smoothing; no formula is given, so
+ * this is the reading implemented).  Codes are OCP e4m3 bytes (round to
+ * nearest even); every scale is a power of two 2^e, e in [-127, 127], the
+ * smallest with (group's largest magnitude) <= 448 * 2^e.  D in {64, 128}.
+ * Np = nB * S (sva_fp8_padded_len); code rows past N are zero. ---- */
+typedef struct sva_fp8_tensors {
+  void* q8;          /* u8 [B, H, Np, D]: Q codes, one exponent per query block */
+  void* k8;          /* u8 [B, H, Np, D]: codes of K - k_mean, one exponent per key block */
+  void* v8;          /* u8 [B, H, Np/64, D, 64]: V codes in 64-key tiles, channel-major
+                        inside a tile; one exponent per channel */
+  int32_t* q_exp;    /* [B, H, nB] */
+  int32_t* k_exp;    /* [B, H, nB] */
+  int32_t* v_exp;    /* [B, H, D] */
+  void* k_mean;      /* bf16 [B, H, D]: K's channel mean over the N tokens, rounded
+                        once to bf16 (the smoothing vector; every logit of a query
+                        moves by the same amount, so the softmax is unchanged) */
+} sva_fp8_tensors;
+
+/* Np = nB * S, the padded token count of the code tensors.  Host only.
+ * SVA_ERR_UNSUPPORTED for D outside {64, 128}. */
+int sva_fp8_padded_len(const sva_problem* prob, int32_t* np);
+
+/* Quantise bf16 Q, K, V [B, H, N, D] into the code tensors and exponents of
+ * `out` (all device memory the caller owns; k_mean is written too).  K is
+ * smoothed first (K - k_mean, in float32).  Pointers 16-byte aligned
+ * (exponent arrays 4). */
+int sva_quantize_fp8(const sva_problem* prob, const void* q, const void* k, const void* v,
+                     const sva_fp8_tensors* out, void* stream);
+
+/* Block-sparse attention on quantised inputs, with the kept-block lists of
+ * sva_select_blocks (kmax <= 2048, else SVA_ERR_UNSUPPORTED).  The
+ * unnormalised probabilities are rounded to e4m3 before the PV product and l
+ * sums those rounded weights.  out: bf16 or f32 [B, H, N, D] as
+ * prob->out_dtype; lse (optional) f32 [B, H, N], natural log.  k_mean is not
+ * read. */
+int sva_sparse_attention_fp8(const sva_problem* prob, const sva_fp8_tensors* in, const int32_t* kv_idx,
+                             const int32_t* kv_count, int32_t kmax, void* out, float* lse, void* stream);
+
+/* The same with every block kept (nB <= 2048). */
+int sva_dense_attention_fp8(const sva_problem* prob, const sva_fp8_tensors* in, void* out, float* lse,
+                            void* stream);
+
 /* Static text for a status code. */
 const char* sva_status_string(int status);
 

@@ -41,6 +41,12 @@ class Tokens(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("tokens", ctypes.c_int32), ("channels", ctypes.c_int32)]
 
 
+class Fp8Tensors(ctypes.Structure):
+    _fields_ = [("q8", ctypes.c_void_p), ("k8", ctypes.c_void_p), ("v8", ctypes.c_void_p),
+                ("q_exp", ctypes.c_void_p), ("k_exp", ctypes.c_void_p), ("v_exp", ctypes.c_void_p),
+                ("k_mean", ctypes.c_void_p)]
+
+
 class SelectParams(ctypes.Structure):
     _fields_ = [("mode", ctypes.c_int32), ("keep_ratio", ctypes.c_double), ("topk", ctypes.c_int32),
                 ("mass_threshold", ctypes.c_double), ("max_keep_ratio", ctypes.c_double),
@@ -76,6 +82,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                              ctypes.c_size_t, vp],
         "sva_token_gather": [ctypes.POINTER(Tokens), ctypes.c_int32, vp, vp, vp, vp],
         "sva_token_scatter": [ctypes.POINTER(Tokens), ctypes.c_int32, vp, vp, vp, vp, vp],
+        "sva_fp8_padded_len": [P, i32p],
+        "sva_quantize_fp8": [P, vp, vp, vp, ctypes.POINTER(Fp8Tensors), vp],
+        "sva_sparse_attention_fp8": [P, ctypes.POINTER(Fp8Tensors), vp, vp, ctypes.c_int32, vp, vp, vp],
+        "sva_dense_attention_fp8": [P, ctypes.POINTER(Fp8Tensors), vp, vp, vp],
         "sva_status_string": [ctypes.c_int],
         "sva_version": [],
     }
@@ -304,6 +314,104 @@ def dense_attention(prob: Problem, q, k, v, out=None, want_lse: bool = False, ls
         _need(lse, torch.float32, shp[:3], "lse")
     _check(load().sva_dense_attention(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(out),
                                       _ptr(lse), _stream(stream)), "sva_dense_attention")
+    return out, lse
+
+
+# --------------------------------------------------------- fp8 (e4m3) attention
+
+def fp8_padded_len(prob: Problem) -> int:
+    out = ctypes.c_int32(0)
+    _check(load().sva_fp8_padded_len(ctypes.byref(prob), ctypes.byref(out)), "sva_fp8_padded_len")
+    return out.value
+
+
+def _fp8_struct(t: dict) -> Fp8Tensors:
+    return Fp8Tensors(*(_ptr(t.get(n)) for n in ("q8", "k8", "v8", "q_exp", "k_exp", "v_exp", "k_mean")))
+
+
+def _need_fp8(prob: Problem, t: dict, need_mean: bool):
+    torch = _torch()
+    nb, npad = num_blocks(prob), fp8_padded_len(prob)
+    B, H, D = prob.batch, prob.heads, prob.head_dim
+    _need(t["q8"], torch.uint8, (B, H, npad, D), "q8")
+    _need(t["k8"], torch.uint8, (B, H, npad, D), "k8")
+    _need(t["v8"], torch.uint8, (B, H, npad // 64, D, 64), "v8")
+    _need(t["q_exp"], torch.int32, (B, H, nb), "q_exp")
+    _need(t["k_exp"], torch.int32, (B, H, nb), "k_exp")
+    _need(t["v_exp"], torch.int32, (B, H, D), "v_exp")
+    if need_mean:
+        _need(t["k_mean"], torch.bfloat16, (B, H, D), "k_mean")
+
+
+def quantize_fp8(prob: Problem, q, k, v, out: Optional[dict] = None, stream=None) -> dict:
+    """e4m3 codes and power-of-two exponents of Q, K (smoothed) and V
+    (sva_quantize_fp8).  Returns {q8, k8, v8, q_exp, k_exp, v_exp, k_mean}."""
+    torch = _torch()
+    shp = _qkv_shape(prob)
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        _need(t, torch.bfloat16, shp, n)
+    if out is None:
+        nb, npad = num_blocks(prob), fp8_padded_len(prob)
+        B, H, D = prob.batch, prob.heads, prob.head_dim
+        dev = q.device
+        out = {"q8": torch.empty((B, H, npad, D), dtype=torch.uint8, device=dev),
+               "k8": torch.empty((B, H, npad, D), dtype=torch.uint8, device=dev),
+               "v8": torch.empty((B, H, npad // 64, D, 64), dtype=torch.uint8, device=dev),
+               "q_exp": torch.empty((B, H, nb), dtype=torch.int32, device=dev),
+               "k_exp": torch.empty((B, H, nb), dtype=torch.int32, device=dev),
+               "v_exp": torch.empty((B, H, D), dtype=torch.int32, device=dev),
+               "k_mean": torch.empty((B, H, D), dtype=torch.bfloat16, device=dev)}
+    _need_fp8(prob, out, True)
+    st = _fp8_struct(out)
+    _check(load().sva_quantize_fp8(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), ctypes.byref(st),
+                                   _stream(stream)), "sva_quantize_fp8")
+    return out
+
+
+def sparse_attention_fp8(prob: Problem, quant: dict, kv_idx, kv_count, out=None,
+                         want_lse: bool = False, lse=None, stream=None) -> Tuple:
+    """Block-sparse attention on the codes of quantize_fp8 (sva_sparse_attention_fp8)."""
+    torch = _torch()
+    nb = num_blocks(prob)
+    shp = _qkv_shape(prob)
+    _need_fp8(prob, quant, False)
+    kmax = kv_idx.shape[-1]
+    _need(kv_idx, torch.int32, (prob.batch, prob.heads, nb, kmax), "kv_idx")
+    _need(kv_count, torch.int32, (prob.batch, prob.heads, nb), "kv_count")
+    ref = quant["q8"]
+    if out is None:
+        dt = torch.float32 if prob.out_dtype == SVA_F32 else torch.bfloat16
+        out = torch.empty(shp, dtype=dt, device=ref.device)
+    _need(out, torch.float32 if prob.out_dtype == SVA_F32 else torch.bfloat16, shp, "out")
+    if want_lse and lse is None:
+        lse = torch.empty(shp[:3], dtype=torch.float32, device=ref.device)
+    if lse is not None:
+        _need(lse, torch.float32, shp[:3], "lse")
+    st = _fp8_struct(quant)
+    _check(load().sva_sparse_attention_fp8(ctypes.byref(prob), ctypes.byref(st), _ptr(kv_idx),
+                                           _ptr(kv_count), int(kmax), _ptr(out), _ptr(lse),
+                                           _stream(stream)), "sva_sparse_attention_fp8")
+    return out, lse
+
+
+def dense_attention_fp8(prob: Problem, quant: dict, out=None, want_lse: bool = False, lse=None,
+                        stream=None) -> Tuple:
+    """Every block kept, on the codes of quantize_fp8 (sva_dense_attention_fp8)."""
+    torch = _torch()
+    shp = _qkv_shape(prob)
+    _need_fp8(prob, quant, False)
+    ref = quant["q8"]
+    dt = torch.float32 if prob.out_dtype == SVA_F32 else torch.bfloat16
+    if out is None:
+        out = torch.empty(shp, dtype=dt, device=ref.device)
+    _need(out, dt, shp, "out")
+    if want_lse and lse is None:
+        lse = torch.empty(shp[:3], dtype=torch.float32, device=ref.device)
+    if lse is not None:
+        _need(lse, torch.float32, shp[:3], "lse")
+    st = _fp8_struct(quant)
+    _check(load().sva_dense_attention_fp8(ctypes.byref(prob), ctypes.byref(st), _ptr(out), _ptr(lse),
+                                          _stream(stream)), "sva_dense_attention_fp8")
     return out, lse
 
 

@@ -101,6 +101,46 @@ int hip_status(hipError_t e) { return e == hipSuccess ? SVA_OK : SVA_ERR_HIP; }
 
 }  // namespace
 
+// ---- fp8 (e4m3) quantisation and attention ----
+
+namespace {
+int check_fp8(const sva_problem* prob, Dims* d) {
+  const int st = check_problem(prob, d);
+  if (st != SVA_OK) return st;
+  if (d->D != 64 && d->D != 128) return SVA_ERR_UNSUPPORTED;
+  // per-head byte ranges of the padded codes are 32-bit buffer offsets
+  if ((int64_t)d->nB * d->S * d->D > INT32_MAX) return SVA_ERR_SHAPE;
+  return SVA_OK;
+}
+
+int check_fp8_tensors(const sva_fp8_tensors* t, bool need_mean) {
+  if (!t || !t->q8 || !t->k8 || !t->v8 || !t->q_exp || !t->k_exp || !t->v_exp) return SVA_ERR_INVALID_ARG;
+  if (need_mean && !t->k_mean) return SVA_ERR_INVALID_ARG;
+  if (!aligned(t->q8, 16) || !aligned(t->k8, 16) || !aligned(t->v8, 16) || !aligned(t->q_exp, 4) ||
+      !aligned(t->k_exp, 4) || !aligned(t->v_exp, 4) || (need_mean && !aligned(t->k_mean, 16)))
+    return SVA_ERR_ALIGNMENT;
+  return SVA_OK;
+}
+
+sva::Fp8AttnArgs fp8_attn_args(const Dims& d, const sva_fp8_tensors* t, const int32_t* kv_idx,
+                               const int32_t* kv_count, int32_t kmax, void* out, float* lse) {
+  sva::Fp8AttnArgs a{};
+  a.q8 = static_cast<const uint8_t*>(t->q8);
+  a.k8 = static_cast<const uint8_t*>(t->k8);
+  a.v8 = static_cast<const uint8_t*>(t->v8);
+  a.q_exp = t->q_exp;
+  a.k_exp = t->k_exp;
+  a.v_exp = t->v_exp;
+  a.kv_idx = kv_idx;
+  a.kv_count = kv_count;
+  a.kmax = kmax;
+  a.out = out;
+  a.lse = lse;
+  a.scale_log2 = (float)(d.scale * 1.4426950408889634);
+  return a;
+}
+}  // namespace
+
 extern "C" {
 
 int sva_version(void) { return SVA_VERSION_MAJOR * 100 + SVA_VERSION_MINOR; }
@@ -306,6 +346,65 @@ int sva_dense_attention(const sva_problem* prob, const void* q, const void* k, c
       d, false, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
       static_cast<const uint16_t*>(v), nullptr, nullptr, 1, out, lse,
       static_cast<hipStream_t>(stream)));
+}
+
+int sva_fp8_padded_len(const sva_problem* prob, int32_t* np) {
+  if (!np) return SVA_ERR_INVALID_ARG;
+  Dims d;
+  const int st = check_fp8(prob, &d);
+  if (st != SVA_OK) return st;
+  *np = d.nB * d.S;
+  return SVA_OK;
+}
+
+int sva_quantize_fp8(const sva_problem* prob, const void* q, const void* k, const void* v,
+                     const sva_fp8_tensors* out, void* stream) {
+  Dims d;
+  int st = check_fp8(prob, &d);
+  if (st != SVA_OK) return st;
+  if (!q || !k || !v) return SVA_ERR_INVALID_ARG;
+  if ((st = check_fp8_tensors(out, true)) != SVA_OK) return st;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16)) return SVA_ERR_ALIGNMENT;
+  sva::Fp8QuantArgs a{};
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.q8 = static_cast<uint8_t*>(out->q8);
+  a.k8 = static_cast<uint8_t*>(out->k8);
+  a.v8 = static_cast<uint8_t*>(out->v8);
+  a.q_exp = out->q_exp;
+  a.k_exp = out->k_exp;
+  a.v_exp = out->v_exp;
+  a.k_mean = static_cast<uint16_t*>(out->k_mean);
+  return hip_status(sva::launch_quantize_fp8(d, a, static_cast<hipStream_t>(stream)));
+}
+
+int sva_sparse_attention_fp8(const sva_problem* prob, const sva_fp8_tensors* in, const int32_t* kv_idx,
+                             const int32_t* kv_count, int32_t kmax, void* out, float* lse, void* stream) {
+  Dims d;
+  int st = check_fp8(prob, &d);
+  if (st != SVA_OK) return st;
+  if ((st = check_fp8_tensors(in, false)) != SVA_OK) return st;
+  if (!kv_idx || !kv_count || !out) return SVA_ERR_INVALID_ARG;
+  if (kmax < 1) return SVA_ERR_SHAPE;
+  if (kmax > sva::kFp8MaxList) return SVA_ERR_UNSUPPORTED;
+  if (!aligned(out, 16) || !aligned(kv_idx, 4) || !aligned(kv_count, 4) || (lse && !aligned(lse, 4)))
+    return SVA_ERR_ALIGNMENT;
+  return hip_status(sva::launch_attention_fp8(d, true, fp8_attn_args(d, in, kv_idx, kv_count, kmax, out, lse),
+                                              static_cast<hipStream_t>(stream)));
+}
+
+int sva_dense_attention_fp8(const sva_problem* prob, const sva_fp8_tensors* in, void* out, float* lse,
+                            void* stream) {
+  Dims d;
+  int st = check_fp8(prob, &d);
+  if (st != SVA_OK) return st;
+  if ((st = check_fp8_tensors(in, false)) != SVA_OK) return st;
+  if (!out) return SVA_ERR_INVALID_ARG;
+  if (d.nB > sva::kFp8MaxList) return SVA_ERR_UNSUPPORTED;
+  if (!aligned(out, 16) || (lse && !aligned(lse, 4))) return SVA_ERR_ALIGNMENT;
+  return hip_status(sva::launch_attention_fp8(d, false, fp8_attn_args(d, in, nullptr, nullptr, 1, out, lse),
+                                              static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

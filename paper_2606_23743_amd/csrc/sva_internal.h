@@ -43,6 +43,42 @@ hipError_t launch_attention_rescaling(const Dims& d, bool sparse, const AttnArgs
 // attention_q32.hip.
 hipError_t launch_attention_q32(const Dims& d, bool sparse, const AttnArgs& a, hipStream_t stream);
 
+// fp8 (e4m3) quantisation and attention; fp8_quant.hip, attention_fp8.hip.
+// Codes: q8, k8 [B, H, Np, D]; v8 [B, H, Np/64, D, 64] (Np = nB * S, padding
+// rows zero).  Exponents: q_exp, k_exp [B, H, nB]; v_exp [B, H, D].
+struct Fp8QuantArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  uint8_t* q8;
+  uint8_t* k8;
+  uint8_t* v8;
+  int32_t* q_exp;
+  int32_t* k_exp;
+  int32_t* v_exp;
+  uint16_t* k_mean;   // bf16 [B, H, D]
+  int N, nB, Np, n_rows;
+};
+hipError_t launch_quantize_fp8(const Dims& d, const Fp8QuantArgs& a, hipStream_t stream);
+
+struct Fp8AttnArgs {
+  const uint8_t* q8;
+  const uint8_t* k8;
+  const uint8_t* v8;
+  const int32_t* q_exp;
+  const int32_t* k_exp;
+  const int32_t* v_exp;
+  const int32_t* kv_idx;
+  const int32_t* kv_count;
+  void* out;
+  float* lse;
+  int N, nB, Np, kmax, n_rows;
+  float scale_log2;   // c * log2(e)
+};
+// Largest kept-block list (and nB for the dense form) the fp8 kernel holds.
+constexpr int kFp8MaxList = 2048;
+hipError_t launch_attention_fp8(const Dims& d, bool sparse, const Fp8AttnArgs& a, hipStream_t stream);
+
 hipError_t launch_pool(const Dims& d, const uint16_t* q, const uint16_t* k, float* q_pool,
                        float* k_pool, hipStream_t stream);
 

@@ -25,11 +25,19 @@ def test_every_declared_symbol_is_exported(lib):
     assert set(names) >= {"sva_pool_blocks", "sva_select_blocks", "sva_sparse_attention",
                           "sva_dense_attention", "sva_num_blocks", "sva_max_keep",
                           "sva_qknorm_rope_pool", "sva_token_keep_count", "sva_token_select",
-                          "sva_token_select_workspace",
+                          "sva_token_select_workspace", "sva_fp8_padded_len", "sva_quantize_fp8",
+                          "sva_sparse_attention_fp8", "sva_dense_attention_fp8",
                           "sva_token_gather", "sva_token_scatter", "sva_status_string",
                           "sva_version"}
     for n in names:
         assert hasattr(lib, n), n
+
+
+def test_library_binds_every_symbol_at_load():
+    """Immediate binding: a kernel launch stub or any other symbol left
+    undefined fails here instead of at its first call."""
+    import os
+    ctypes.CDLL(_lib.LIB_PATH, mode=os.RTLD_NOW | os.RTLD_LOCAL)
 
 
 def test_version_and_status_strings(lib):
@@ -189,3 +197,33 @@ def test_token_entry_points_reject_before_launch(lib):
     assert sc(ctypes.byref(t), 50, A, A, B, A + 256, None) == _lib.SVA_ERR_INVALID_ARG
     assert sc(ctypes.byref(t), 50, A, A, B + 256, B, None) == _lib.SVA_ERR_INVALID_ARG
     assert sc(None, 50, A, A, B, B, None) == _lib.SVA_ERR_INVALID_ARG
+
+
+def test_fp8_entry_points_reject_before_launch(lib):
+    p = sva.problem_for(workloads.TINY)                       # D=64, S=64
+    n = ctypes.c_int32()
+    assert lib.sva_fp8_padded_len(ctypes.byref(p), ctypes.byref(n)) == _lib.SVA_OK and n.value == 1024
+    assert lib.sva_fp8_padded_len(ctypes.byref(sva.problem_for(workloads.SMALL_2B)), ctypes.byref(n)) \
+        == _lib.SVA_ERR_UNSUPPORTED                           # D=112
+    assert lib.sva_fp8_padded_len(ctypes.byref(p), None) == _lib.SVA_ERR_INVALID_ARG
+    A = 1 << 20
+    ok = _lib.Fp8Tensors(A, A, A, A, A, A, A)
+    f = lib.sva_quantize_fp8
+    assert f(ctypes.byref(p), A, A, A, None, None) == _lib.SVA_ERR_INVALID_ARG
+    assert f(ctypes.byref(p), A, A, None, ctypes.byref(ok), None) == _lib.SVA_ERR_INVALID_ARG
+    assert f(ctypes.byref(p), A, A, A, ctypes.byref(_lib.Fp8Tensors(A, A, A, A, A, A, None)), None) \
+        == _lib.SVA_ERR_INVALID_ARG                           # k_mean is written by the quantiser
+    assert f(ctypes.byref(p), A, A, A, ctypes.byref(_lib.Fp8Tensors(A + 8, A, A, A, A, A, A)), None) \
+        == _lib.SVA_ERR_ALIGNMENT
+    assert f(ctypes.byref(p), A + 2, A, A, ctypes.byref(ok), None) == _lib.SVA_ERR_ALIGNMENT
+    g = lib.sva_sparse_attention_fp8
+    assert g(ctypes.byref(p), ctypes.byref(ok), A, A, 0, A, None, None) == _lib.SVA_ERR_SHAPE
+    assert g(ctypes.byref(p), ctypes.byref(ok), A, A, 2049, A, None, None) == _lib.SVA_ERR_UNSUPPORTED
+    assert g(ctypes.byref(p), ctypes.byref(ok), None, A, 4, A, None, None) == _lib.SVA_ERR_INVALID_ARG
+    assert g(ctypes.byref(p), ctypes.byref(ok), A, A, 4, A + 8, None, None) == _lib.SVA_ERR_ALIGNMENT
+    assert g(ctypes.byref(p), ctypes.byref(_lib.Fp8Tensors(A, A, A, A + 2, A, A, None)), A, A, 4, A, None,
+             None) == _lib.SVA_ERR_ALIGNMENT
+    h = lib.sva_dense_attention_fp8
+    assert h(ctypes.byref(p), None, A, None, None) == _lib.SVA_ERR_INVALID_ARG
+    assert h(ctypes.byref(sva.problem_for(workloads.SMALL_2B)), ctypes.byref(ok), A, None, None) \
+        == _lib.SVA_ERR_UNSUPPORTED

@@ -1,0 +1,240 @@
+"""GPU parity of fp8 (e4m3) quantisation and attention against the oracle.
+
+Quantisation decides integers (codes, exponents) from exact comparisons and
+one float32 subtraction, the same on both sides: codes, exponents and the
+bf16 smoothing vector must be bit-equal.
+
+Attention: the oracle computes softmax attention of the dequantised Q, K, V
+in float64.  The GPU also rounds each unnormalised probability p to e4m3
+before the PV product (l sums the same rounded weights), so
+    O_gpu - O = -sum_m (p^_m - p_m)(V_m - O_gpu) / sum_m p_m,
+a weighted sum of independent rounding errors.  Rounding to nearest with 3
+mantissa bits errs by at most e = 2^-4 p in the normal range (2^-16 of the
+row maximum among the subnormals, given the GPU's 2^6 offset), uniformly, so each term has standard deviation at most
+e_m/sqrt(3) * |V_m - O|.  The test predicts the RMS error of every output
+element from the oracle's p and V and requires the observed RMS to stay below
+twice that; the worst case, all errors aligned (sum of e_m |V_m - O| / l), is
+checked per element.  The fp8 matrix instructions add their own summation
+error (measured below 2e-4 of the sum of magnitudes), budgeted as 4e-3 p.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import oracle.fp8_attention as of8
+import paper_2606_23743_amd as sva
+from paper_2606_23743_amd import inputs, workloads
+
+from .gpu_cases import device_inputs, oracle_pool_all, oracle_select, say, scale_of
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+E4M3 = np.array([of8.e4m3_value(c) for c in range(256)])
+
+
+def _np(t):
+    return t.cpu().numpy()
+
+
+def _bf16_bits(t):
+    return _np(t.view(torch.int16)).view(np.uint16)
+
+
+def _check_quant(wl, bits, quant, heads=None):
+    """Codes, exponents and the smoothing vector against the oracle (all heads,
+    or the listed (b, h))."""
+    B, H, N, D, S = wl.batch, wl.heads, wl.seq_len, wl.head_dim, wl.block
+    heads = heads or [(b, h) for b in range(B) for h in range(H)]
+    q8, k8, v8 = _np(quant["q8"]), _np(quant["k8"]), _np(quant["v8"])
+    qe, ke, ve = _np(quant["q_exp"]), _np(quant["k_exp"]), _np(quant["v_exp"])
+    km = _bf16_bits(quant["k_mean"])
+    for b, h in heads:
+        sl = slice(b, b + 1), slice(h, h + 1)
+        x = {n: oracle.bf16_bits_to_f64(bits[n][sl]) for n in ("q", "k", "v")}
+        ref = of8.quantize_qkv(x["q"], x["k"], x["v"], S)
+        assert np.array_equal(qe[b, h], ref["q_exp"][0, 0]), (b, h)
+        assert np.array_equal(ke[b, h], ref["k_exp"][0, 0]), (b, h)
+        assert np.array_equal(ve[b, h], ref["v_exp"][0, 0]), (b, h)
+        want_mean = oracle.bf16_bits_to_f64(km[b, h])
+        assert np.array_equal(want_mean, ref["k_mean"][0, 0]), (b, h)
+        assert np.array_equal(E4M3[q8[b, h, :N]], ref["q_code"][0, 0]), (b, h)
+        assert np.array_equal(E4M3[k8[b, h, :N]], ref["k_code"][0, 0]), (b, h)
+        assert not q8[b, h, N:].any() and not k8[b, h, N:].any()
+        vt = E4M3[v8[b, h]]                                   # [Np/64, D, 64] -> [Np, D]
+        vt = vt.transpose(0, 2, 1).reshape(-1, D)
+        assert np.array_equal(vt[:N], ref["v_code"][0, 0]), (b, h)
+        assert not vt[N:].any()
+
+
+def _dequantised(bits, S, b, h):
+    x = {n: oracle.bf16_bits_to_f64(bits[n][b:b + 1, h:h + 1]) for n in ("q", "k", "v")}
+    return of8.quantize_qkv(x["q"], x["k"], x["v"], S)
+
+
+def _check_attention(got, got_lse, quant_ref, kept_row_lists, S, scale, rows):
+    """got: [N, D] float64 GPU output of one head; rows: query block ids to check.
+    Per weight p (oracle units, row maximum 1) the GPU's rounding errs by at
+    most e = max(2^-4 p, min(p, 2^-16)): 3 mantissa bits, and e4m3 spacing
+    2^-9 below 2^-6, where the GPU holds p times 2^(6 + k), 0 <= k <= 2.75
+    (its probabilities are offset by 2^6 from a reference within 2.75 of the
+    row maximum); plus 4e-3 p for the float32 summation inside the fp8
+    instructions.  Returns (observed rms, model rms)."""
+    q, k, v = (quant_ref[n][0, 0] for n in ("q_hat", "k_hat", "v_hat"))
+    N = q.shape[0]
+    err2, pred2, cnt = 0.0, 0.0, 0
+    for i in rows:
+        qa, qb = i * S, min(N, (i + 1) * S)
+        blocks = kept_row_lists[i]
+        if not blocks:
+            assert np.all(got[qa:qb] == 0)
+            continue
+        keys = np.concatenate([np.arange(j * S, min(N, (j + 1) * S)) for j in blocks])
+        vk = v[keys]
+        for q0 in range(qa, qb, 8):                          # a few queries at a time
+            q1 = min(qb, q0 + 8)
+            logits = scale * (q[q0:q1] @ k[keys].T)
+            mx = logits.max(axis=1, keepdims=True)
+            p = np.exp(logits - mx)
+            l = p.sum(axis=1, keepdims=True)
+            o = (p @ vk) / l
+            lse = mx[:, 0] + np.log(l[:, 0])
+            e = np.maximum(2.0 ** -4 * p, np.minimum(p, 2.0 ** -16)) + 4e-3 * p
+            dev = np.abs(vk[None, :, :] - o[:, None, :])                # [q, m, D]
+            bound = (e[:, :, None] * dev).sum(axis=1) / l + 2.0 ** -8 * np.abs(o) + 1e-6
+            d = got[q0:q1] - o
+            assert np.all(np.abs(d) <= bound), (i, float((np.abs(d) - bound).max()))
+            var = ((e * e / 3.0)[:, :, None] * dev * dev).sum(axis=1) / (l * l)
+            pred2 += float(var.sum())
+            err2 += float((d * d).sum())
+            cnt += d.size
+            lbound = np.log1p(e.sum(axis=1) / l[:, 0]) + 1e-5
+            assert np.all(np.abs(got_lse[q0:q1] - lse) <= lbound), i
+    return np.sqrt(err2 / cnt), np.sqrt(pred2 / cnt)
+
+
+CASES = [
+    # (name, B, H, D, grid, S, keep)
+    ("d128_s128_ragged", 1, 2, 128, (3, 5, 16), 128, 0.5),
+    ("d128_s64", 1, 2, 128, (2, 6, 20), 64, 0.3),
+    ("d64_s64_ragged", 2, 1, 64, (2, 7, 9), 64, 0.4),
+    ("d64_s128", 1, 2, 64, (4, 4, 24), 128, 0.5),
+    ("d128_s128_short", 1, 1, 128, (1, 1, 40), 128, 1.0),
+]
+
+
+@pytest.mark.parametrize("name,B,H,D,grid,S,keep", CASES, ids=[c[0] for c in CASES])
+def test_fp8_quantise_and_attend(name, B, H, D, grid, S, keep):
+    wl = workloads.small_case(name, B, H, D, grid, S, "topk", keep_ratio=keep, seed=61,
+                              sink_tokens=32, sink_scale=3.0)
+    say(f"[fp8 {name}]")
+    bits = inputs.generate(wl)
+    dev = device_inputs(bits)
+    prob = sva.problem_for(wl)
+    quant = sva.quantize_fp8(prob, dev["q"], dev["k"], dev["v"])
+    torch.cuda.synchronize()
+    _check_quant(wl, bits, quant)
+    # kept lists from the oracle's own selection
+    qp, kp = oracle_pool_all(bits, S)
+    scores = oracle.block_scores(qp, kp, scale_of(wl))
+    kept, _ = oracle_select(wl, scores)
+    nb = oracle.num_blocks(wl.seq_len, S)
+    kmax = max(1, max(len(r) for b in kept for h in b for r in h))
+    idx, cnt = oracle.kept_to_arrays(kept, nb, kmax)
+    idx_d = torch.from_numpy(np.ascontiguousarray(idx, dtype=np.int32)).cuda()
+    cnt_d = torch.from_numpy(np.ascontiguousarray(cnt, dtype=np.int32)).cuda()
+    out, lse = sva.sparse_attention_fp8(prob, quant, idx_d, cnt_d, want_lse=True)
+    dout, dlse = sva.dense_attention_fp8(prob, quant, want_lse=True)
+    torch.cuda.synchronize()
+    o = _np(out.float()).astype(np.float64)
+    do = _np(dout.float()).astype(np.float64)
+    for b in range(B):
+        for h in range(H):
+            ref = _dequantised(bits, S, b, h)
+            rows = range(nb)
+            rms, pred = _check_attention(o[b, h], _np(lse)[b, h], ref, kept[b][h], S, scale_of(wl), rows)
+            assert rms <= 2.0 * pred + 2e-3, (b, h, rms, pred)    # + bf16 output rounding
+            drms, dpred = _check_attention(do[b, h], _np(dlse)[b, h], ref, [list(range(nb))] * nb, S,
+                                           scale_of(wl), rows)
+            assert drms <= 2.0 * dpred + 2e-3, (b, h, drms, dpred)
+            say(f"[fp8 {name}] b{b} h{h}: sparse rms {rms:.2e} (model {pred:.2e}), dense rms {drms:.2e} "
+                f"(model {dpred:.2e})")
+
+
+def test_fp8_f32_output_and_empty_rows():
+    wl = workloads.small_case("f32_empty", 1, 2, 128, (2, 4, 32), 128, "topk", keep_ratio=0.5, seed=67)
+    bits = inputs.generate(wl)
+    dev = device_inputs(bits)
+    prob = sva.problem_for(wl)
+    prob32 = sva.problem_for(wl)
+    prob32.out_dtype = 1
+    quant = sva.quantize_fp8(prob, dev["q"], dev["k"], dev["v"])
+    nb = oracle.num_blocks(wl.seq_len, 128)
+    idx = np.full((1, 2, nb, 2), -1, dtype=np.int32)
+    cnt = np.zeros((1, 2, nb), dtype=np.int32)
+    idx[0, 0, :, 0], cnt[0, 0, :] = 0, 1                       # head 0: block 0 only
+    idx[0, 1, 1, :] = [7, 99]                                   # head 1 row 1: out of range -> empty
+    cnt[0, 1, 1] = 2
+    idx_d, cnt_d = torch.from_numpy(idx).cuda(), torch.from_numpy(cnt).cuda()
+    o16, _ = sva.sparse_attention_fp8(prob, quant, idx_d, cnt_d)
+    o32, lse = sva.sparse_attention_fp8(prob32, quant, idx_d, cnt_d, want_lse=True)
+    torch.cuda.synchronize()
+    assert o32.dtype == torch.float32
+    assert torch.equal(o32.to(torch.bfloat16), o16)
+    assert not o32[0, 1].any() and torch.all(torch.isinf(lse[0, 1]))   # no usable block: zeros, -inf
+    ref = _dequantised(bits, 128, 0, 0)
+    rms, pred = _check_attention(_np(o32[0, 0]).astype(np.float64), _np(lse)[0, 0], ref, [[0]] * nb, 128,
+                                 scale_of(wl), range(nb))
+    assert rms <= 2.0 * pred + 1e-4
+
+
+@pytest.mark.slow
+def test_fp8_full_size_sampled():
+    """The 64B-class layer: every head's Q exponents, two heads' codes and
+    smoothing vectors, and sampled query blocks of three heads' attention
+    (kept lists from the oracle's own selection on those heads), against the
+    oracle."""
+    wl = workloads.LARGE_64B
+    say(f"[fp8 {wl.name}] generating")
+    bits = inputs.generate(wl)
+    dev = device_inputs(bits)
+    prob = sva.problem_for(wl)
+    quant = sva.quantize_fp8(prob, dev["q"], dev["k"], dev["v"])
+    S, H, N = wl.block, wl.heads, wl.seq_len
+    nb = oracle.num_blocks(N, S)
+    sel = sva.select_for(wl)
+    kmax = sva.max_keep(prob, sel)
+    heads = (0, H // 2, H - 1)
+    idx = np.full((1, H, nb, kmax), -1, dtype=np.int32)
+    cnt = np.zeros((1, H, nb), dtype=np.int32)
+    kept_h = {}
+    for h in heads:
+        qp = oracle.pool_blocks(oracle.bf16_bits_to_f64(bits["q"][0, h]), S)
+        kp = oracle.pool_blocks(oracle.bf16_bits_to_f64(bits["k"][0, h]), S)
+        sc = oracle.block_scores(qp, kp, scale_of(wl))
+        kept = oracle.select_topk(sc, oracle.topk_count(nb, wl.keep_ratio, wl.topk))
+        kept_h[h] = [list(r) for r in kept]
+        for i, r in enumerate(kept_h[h]):
+            idx[0, h, i, :len(r)] = sorted(r)
+            cnt[0, h, i] = len(r)
+    out, lse = sva.sparse_attention_fp8(prob, quant, torch.from_numpy(idx).cuda(), torch.from_numpy(cnt).cuda(),
+                                        want_lse=True)
+    torch.cuda.synchronize()
+    say(f"[fp8 {wl.name}] checking")
+    for h in (0, H - 1):
+        _check_quant(wl, bits, quant, heads=[(0, h)])
+    for h in range(H):
+        x = oracle.bf16_bits_to_f64(bits["q"][0, h])
+        amax = [np.abs(x[i * S:min(N, (i + 1) * S)]).max() for i in range(nb)]
+        assert np.array_equal(_np(quant["q_exp"])[0, h], [of8.scale_exponent(a) for a in amax]), h
+    rng = np.random.default_rng(7)
+    o = _np(out.float()).astype(np.float64)
+    for h in heads:
+        ref = _dequantised(bits, S, 0, h)
+        rows = sorted(rng.choice(nb, 5, replace=False).tolist()) + [nb - 1]
+        rms, pred = _check_attention(o[0, h], _np(lse)[0, h], ref, kept_h[h], S, scale_of(wl), rows)
+        say(f"[fp8 {wl.name}] head {h}: rms {rms:.2e} (model {pred:.2e})")
+        assert rms <= 2.0 * pred + 2e-3
+    del dev, quant, out, lse
+    torch.cuda.empty_cache()
