@@ -163,8 +163,8 @@ void attn_fp8_kernel(Fp8AttnArgs a) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_u8*)(size_t)__builtin_amdgcn_readfirstlane(lds_addr), 16,
                                              voff, __builtin_amdgcn_readfirstlane(soff), 0, 0);
   };
-  auto fetch_chunk = [&](int g) {            // chunk g into stage g % NST
-    const int e = __builtin_amdgcn_readfirstlane(entry(g));
+  auto fetch_chunk = [&](int g, int e) {     // chunk g (list entry e) into stage g % NST
+    e = __builtin_amdgcn_readfirstlane(e);
     const int key0 = __builtin_amdgcn_readfirstlane((e >> 8) * S + (g < G ? (g % NCK) * CK : 0));
     const int st = g & (NST - 1);
 #pragma unroll
@@ -213,13 +213,25 @@ void attn_fp8_kernel(Fp8AttnArgs a) {
       for (int r = 0; r < 16; ++r)
         if (32 * t + 16 * hf + r >= valid) sc[t][r] = -INFINITY;
   };
+  // Row maximum of a chunk.  The logits are never NaN (finite or -inf), so the
+  // maxima are taken with v_max3_f32 directly: fmaxf would first canonicalise
+  // every operand, tripling the instruction count of this per-chunk step.
+  auto max3 = [](float a, float b, float c) -> float {
+    float r;
+    asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+    return r;
+  };
   auto row_max = [&](const f32x16 (&sc)[2]) -> float {
-    float mx = fmaxf(sc[0][0], sc[0][1]);
+    float mx = max3(sc[0][0], sc[0][1], sc[0][2]);
 #pragma unroll
-    for (int r = 2; r < 16; r += 2) mx = __builtin_fmaxf(mx, __builtin_fmaxf(sc[0][r], sc[0][r + 1]));
+    for (int r = 3; r < 15; r += 2) mx = max3(mx, sc[0][r], sc[0][r + 1]);
+    mx = max3(mx, sc[0][15], sc[1][0]);
 #pragma unroll
-    for (int r = 0; r < 16; r += 2) mx = __builtin_fmaxf(mx, __builtin_fmaxf(sc[1][r], sc[1][r + 1]));
-    return swap_halves_max(mx);
+    for (int r = 1; r < 15; r += 2) mx = max3(mx, sc[1][r], sc[1][r + 1]);
+    mx = max3(mx, sc[1][15], sc[1][15]);
+    // both halves of the row: lanes l and l ^ 32
+    const u32x2 sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+    return max3(__uint_as_float(sw[0]), __uint_as_float(sw[1]), __uint_as_float(sw[1]));
   };
   // before a chunk's probabilities: keep p = exp2(s*sl2 - m_ref + kShift) <= 2^(kShift + kGuard)
   auto guard = [&](const f32x16 (&sc)[2]) {
@@ -246,8 +258,9 @@ void attn_fp8_kernel(Fp8AttnArgs a) {
         const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[t][4 * e + 1], sl2, kShift - m_ref));
         const float p2 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[t][4 * e + 2], sl2, kShift - m_ref));
         const float p3 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[t][4 * e + 3], sl2, kShift - m_ref));
-        int wv = 0;
-        wv = __builtin_amdgcn_cvt_pk_fp8_f32(p0, p1, wv, false);
+        // the first conversion's other half is overwritten by the second, so
+        // any register serves as its old value (no zeroing move)
+        int wv = __builtin_amdgcn_cvt_pk_fp8_f32(p0, p1, (int)__float_as_uint(p2), false);
         wv = __builtin_amdgcn_cvt_pk_fp8_f32(p2, p3, wv, true);
         pop[4 * t + e] = wv;
       }
@@ -270,39 +283,48 @@ void attn_fp8_kernel(Fp8AttnArgs a) {
   // iteration g-2, its V at g-1) and receives chunk g+3.  Every iteration
   // issues one load group (past the end: block 0's first chunk, in bounds),
   // so the wait count is a constant.
+  // The loop body is written twice (chunks g and g+1) so the S^T tiles of the
+  // current and next chunk swap roles without register copies.  The list
+  // entries a chunk step needs (for chunk g+1's S^T and chunk g+3's loads) are
+  // read from LDS one step earlier, so their latency is hidden.
   if (G > 0) {
-    fetch_chunk(0);
-    fetch_chunk(1);
-    fetch_chunk(2);
-    f32x16 sacc[2];
+    fetch_chunk(0, entry(0));
+    fetch_chunk(1, entry(1));
+    fetch_chunk(2, entry(2));
+    f32x16 sa[2], sb[2];
     wait_vmcnt<2 * GL>();
     wg_barrier();
     {
       const int e0 = __builtin_amdgcn_readfirstlane(entry(0));
-      qk(sacc, 0, e0 & 255);
+      qk(sa, 0, e0 & 255);
       const int valid = __builtin_amdgcn_readfirstlane(N - (e0 >> 8) * S);
-      if (valid < CK) mask_tail(sacc, valid);
-      m_ref = row_max(sacc) * sl2;           // chunk 0 of a block holds a valid key
+      if (valid < CK) mask_tail(sa, valid);
+      m_ref = row_max(sa) * sl2;             // chunk 0 of a block holds a valid key
     }
-    for (int g = 0; g < G; ++g) {
+    int ent1 = entry(1), ent3 = entry(3);
+    auto step = [&](int g, f32x16 (&scur)[2], f32x16 (&snxt)[2]) {
       wait_vmcnt_lds_idle<GL>();             // chunk g+1 landed, this wave's LDS reads done
       wg_barrier();
-      fetch_chunk(g + 3);
-      const int e1 = __builtin_amdgcn_readfirstlane(entry(g + 1));
+      fetch_chunk(g + 3, ent3);
+      const int e1 = __builtin_amdgcn_readfirstlane(ent1);
+      ent1 = entry(g + 2);
+      ent3 = entry(g + 4);
       const int nkey0 = __builtin_amdgcn_readfirstlane((e1 >> 8) * S + (g + 1 < G ? ((g + 1) % NCK) * CK : 0));
-      f32x16 snext[2];
       i32x8 pop;
-      qk(snext, (g + 1) & (NST - 1), e1 & 255);
-      guard(sacc);
-      softmax(sacc, pop);
+      qk(snxt, (g + 1) & (NST - 1), e1 & 255);
+      guard(scur);
+      softmax(scur, pop);
       pv(pop, g & (NST - 1));
       const int nvalid = __builtin_amdgcn_readfirstlane(N - nkey0);
       if (nvalid < CK) {
         asm volatile("");
-        mask_tail(snext, nvalid);
+        mask_tail(snxt, nvalid);
       }
-      sacc[0] = snext[0];
-      sacc[1] = snext[1];
+    };
+    for (int g = 0; g < G; g += 2) {
+      step(g, sa, sb);
+      if (g + 1 >= G) break;
+      step(g + 1, sb, sa);
     }
   }
   wait_vmcnt<0>();                           // no load may still target this workgroup's LDS

@@ -4,6 +4,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "attn_args.h"
+#include "xcd.h"
+
 namespace sva {
 
 // Problem sizes after host validation.
@@ -21,19 +24,6 @@ struct SelectRule {
   double tau;   // mass: threshold
   int cap;      // mass: most blocks kept per row
   int n_forced; // mass: forced first-frame blocks 0 .. n_forced-1
-};
-
-// Arguments shared by the attention kernels.
-struct AttnArgs {
-  const uint16_t* q;
-  const uint16_t* k;
-  const uint16_t* v;
-  const int32_t* kv_idx;
-  const int32_t* kv_count;
-  void* out;
-  float* lse;
-  int N, nB, kmax, n_rows;
-  float scale_log2;   // c * log2(e)
 };
 
 // The rescaling (per-iteration online softmax) kernel; attention.hip.
@@ -117,21 +107,5 @@ hipError_t launch_select(const Dims& d, const SelectRule& r, const float* q_pool
 hipError_t launch_attention(const Dims& d, bool sparse, const uint16_t* q, const uint16_t* k,
                             const uint16_t* v, const int32_t* kv_idx, const int32_t* kv_count,
                             int kmax, void* out, float* lse, hipStream_t stream);
-
-// Workgroup order: the hardware hands consecutive workgroup ids to the 8 XCDs
-// round-robin.  Mapping id -> (id % 8) * ceil(n/8) + id / 8 gives each XCD a
-// contiguous range of logical work items, so neighbouring query blocks of a
-// head (which read overlapping key/value blocks) share one XCD's L2.
-__device__ __forceinline__ int xcd_remap(int id, int n) {
-  constexpr int kXcd = 8;
-  const int per = (n + kXcd - 1) / kXcd;
-  const int xcd = id % kXcd;
-  const int slot = id / kXcd;
-  // the first (n % 8) XCDs (or all, if n is a multiple of 8) own `per` items,
-  // the rest own per-1; compute the start of this XCD's range accordingly
-  const int full = (n % kXcd == 0) ? kXcd : (n % kXcd);
-  const int start = (xcd < full) ? xcd * per : full * per + (xcd - full) * (per - 1);
-  return start + slot;
-}
 
 }  // namespace sva
