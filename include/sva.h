@@ -270,7 +270,7 @@ int sva_quantize_fp8(const sva_problem* prob, const void* q, const void* k, cons
                      const sva_fp8_tensors* out, void* stream);
 
 /* Block-sparse attention on quantised inputs, with the kept-block lists of
- * sva_select_blocks (kmax <= 2048, else SVA_ERR_UNSUPPORTED).  The
+ * sva_select_blocks (kmax <= 2047, else SVA_ERR_UNSUPPORTED).  The
  * unnormalised probabilities are rounded to e4m3 before the PV product and l
  * sums those rounded weights.  out: bf16 or f32 [B, H, N, D] as
  * prob->out_dtype; lse (optional) f32 [B, H, N], natural log.  k_mean is not
@@ -278,7 +278,7 @@ int sva_quantize_fp8(const sva_problem* prob, const void* q, const void* k, cons
 int sva_sparse_attention_fp8(const sva_problem* prob, const sva_fp8_tensors* in, const int32_t* kv_idx,
                              const int32_t* kv_count, int32_t kmax, void* out, float* lse, void* stream);
 
-/* The same with every block kept (nB <= 2048). */
+/* The same with every block kept (nB <= 2047). */
 int sva_dense_attention_fp8(const sva_problem* prob, const sva_fp8_tensors* in, void* out, float* lse,
                             void* stream);
 

@@ -30,8 +30,9 @@
 //   l  += 1^T P^T   one more instruction with an all-ones operand: l is exactly
 //                 the sum of the e4m3 weights the PV product applied.
 // Chunks stream through four LDS stages (K and V tiles of 64 x D bytes)
-// filled three chunks ahead by buffer_load ... lds; the stage is the chunk
-// counter mod 4.  Each wave overlaps the next chunk's S^T with the current
+// filled three chunks ahead by buffer_load ... lds (two stages, K two chunks
+// and V one chunk ahead, at D = 128 with S = 64); the stage is the chunk
+// counter mod the stage count.  Each wave overlaps the next chunk's S^T with the current
 // chunk's softmax and PV, as in the bf16 kernel.  The kept-block list is
 // compacted into LDS at the start (entries outside [0, nB) dropped), packed
 // with each block's K exponent.
@@ -45,7 +46,7 @@ using namespace attn;
 typedef __attribute__((ext_vector_type(8))) int i32x8;
 typedef __attribute__((ext_vector_type(4))) int i32x4;
 
-constexpr int kListMax = kFp8MaxList;  // kept blocks per query block held in LDS
+constexpr int kListSlots = kFp8MaxList + 1;  // LDS list entries; the last slot holds the count
 constexpr float kShift = 6.0f;           // log2 offset of the probabilities (see above)
 constexpr float kGuard = 2.75f;          // allowed excess of a chunk maximum over m
 
@@ -68,7 +69,9 @@ void attn_fp8_kernel(Fp8AttnArgs a) {
   constexpr int NW = S / 32;                 // waves per workgroup
   constexpr int CK = 64;                     // keys per chunk
   constexpr int NCK = S / CK;                // chunks per block
-  constexpr int NST = 4;                     // LDS stages
+  // LDS stages: four (loads three chunks ahead), or two at D = 128, S = 64 so
+  // that four two-wave workgroups (two waves per SIMD) fit a CU's 160 KB
+  constexpr int NST = (D == 128 && S == 64) ? 2 : 4;
   constexpr int TB = CK * D;                 // bytes of one K (or V) tile
   constexpr int NPC = D / 16;                // 16-byte pieces per K row
   constexpr int NUK = TB / 1024 / NW;        // direct-load pieces per wave per tile
@@ -79,8 +82,7 @@ void attn_fp8_kernel(Fp8AttnArgs a) {
 
   __shared__ __attribute__((aligned(1024))) unsigned char Ks[NST][TB];
   __shared__ __attribute__((aligned(1024))) unsigned char Vs[NST][TB];
-  __shared__ int list[kListMax];             // (block << 8) | (K exponent + 127)
-  __shared__ int list_n;
+  __shared__ int list[kListSlots];           // (block << 8) | (K exponent + 127); count last
 
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -106,17 +108,17 @@ void attn_fp8_kernel(Fp8AttnArgs a) {
         const bool ok = j >= 0 && j < nB;
         const unsigned long long m = __builtin_amdgcn_ballot_w64(ok);
         const int pos = n + __builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)m, 0));
-        if (ok && pos < kListMax) list[pos] = (j << 8) | (a.k_exp[(size_t)bh * nB + j] + 127);
+        if (ok && pos < kFp8MaxList) list[pos] = (j << 8) | (a.k_exp[(size_t)bh * nB + j] + 127);
         n += __builtin_popcountll(m);
       }
-      if (lane == 0) list_n = min(n, kListMax);
+      if (lane == 0) list[kFp8MaxList] = min(n, kFp8MaxList);
     }
   } else {
     for (int t = threadIdx.x; t < nB; t += 2 * S) list[t] = (t << 8) | (a.k_exp[(size_t)bh * nB + t] + 127);
-    if (threadIdx.x == 0) list_n = nB;
+    if (threadIdx.x == 0) list[kFp8MaxList] = nB;
   }
   __syncthreads();
-  const int nblk = list_n;
+  const int nblk = list[kFp8MaxList];
   const int G = nblk * NCK;                  // chunks to process
   auto entry = [&](int g) -> int {           // list entry of chunk g (block 0 past the end)
     return g < G ? list[g / NCK] : 127;
@@ -163,14 +165,20 @@ void attn_fp8_kernel(Fp8AttnArgs a) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_u8*)(size_t)__builtin_amdgcn_readfirstlane(lds_addr), 16,
                                              voff, __builtin_amdgcn_readfirstlane(soff), 0, 0);
   };
-  auto fetch_chunk = [&](int g, int e) {     // chunk g (list entry e) into stage g % NST
+  // K (tk) or V of chunk g (list entry e) into stage g % NST
+  auto fetch_half = [&](bool tk, int g, int e) {
     e = __builtin_amdgcn_readfirstlane(e);
     const int key0 = __builtin_amdgcn_readfirstlane((e >> 8) * S + (g < G ? (g % NCK) * CK : 0));
     const int st = g & (NST - 1);
 #pragma unroll
-    for (int v = 0; v < NUK; ++v) bll(krs, ks_base + st * TB + (w * NUK + v) * 1024, kgv[v], key0 * D);
-#pragma unroll
-    for (int v = 0; v < NUK; ++v) bll(vrs, vs_base + st * TB + (w * NUK + v) * 1024, vgv[v], key0 * D);
+    for (int v = 0; v < NUK; ++v) {
+      if (tk) bll(krs, ks_base + st * TB + (w * NUK + v) * 1024, kgv[v], key0 * D);
+      else bll(vrs, vs_base + st * TB + (w * NUK + v) * 1024, vgv[v], key0 * D);
+    }
+  };
+  auto fetch_chunk = [&](int g, int e) {
+    fetch_half(true, g, e);
+    fetch_half(false, g, e);
   };
 
   // per-lane LDS read offsets (the stage and the tile/row offsets are added)
@@ -285,14 +293,20 @@ void attn_fp8_kernel(Fp8AttnArgs a) {
   // so the wait count is a constant.
   // The loop body is written twice (chunks g and g+1) so the S^T tiles of the
   // current and next chunk swap roles without register copies.  The list
-  // entries a chunk step needs (for chunk g+1's S^T and chunk g+3's loads) are
-  // read from LDS one step earlier, so their latency is hidden.
+  // entries a chunk step needs are read from LDS one step earlier, so their
+  // latency is hidden.
   if (G > 0) {
-    fetch_chunk(0, entry(0));
-    fetch_chunk(1, entry(1));
-    fetch_chunk(2, entry(2));
     f32x16 sa[2], sb[2];
-    wait_vmcnt<2 * GL>();
+    if constexpr (NST == 4) {
+      fetch_chunk(0, entry(0));
+      fetch_chunk(1, entry(1));
+      fetch_chunk(2, entry(2));
+      wait_vmcnt<2 * GL>();
+    } else {
+      fetch_chunk(0, entry(0));
+      fetch_half(true, 1, entry(1));
+      wait_vmcnt<0>();
+    }
     wg_barrier();
     {
       const int e0 = __builtin_amdgcn_readfirstlane(entry(0));
@@ -301,13 +315,28 @@ void attn_fp8_kernel(Fp8AttnArgs a) {
       if (valid < CK) mask_tail(sa, valid);
       m_ref = row_max(sa) * sl2;             // chunk 0 of a block holds a valid key
     }
-    int ent1 = entry(1), ent3 = entry(3);
+    // Four stages: after the barrier of step g, chunk g-1's stage is free (its
+    // K was read at step g-2, its V at g-1) and receives chunk g+3; the wait is
+    // for chunk g+1.  Two stages: K stage g (read by the S^T of step g-1)
+    // receives K of chunk g+2 and V stage g+1 (read by the PV of step g-1)
+    // receives V of chunk g+1; every load of the previous step is waited for.
+    // Each step issues the same loads (past the end: block 0, in bounds), so
+    // the wait counts are constants.
+    int ent1 = entry(1), ent2 = entry(2), ent3 = entry(3);
     auto step = [&](int g, f32x16 (&scur)[2], f32x16 (&snxt)[2]) {
-      wait_vmcnt_lds_idle<GL>();             // chunk g+1 landed, this wave's LDS reads done
-      wg_barrier();
-      fetch_chunk(g + 3, ent3);
+      if constexpr (NST == 4) {
+        wait_vmcnt_lds_idle<GL>();           // chunk g+1 landed, this wave's LDS reads done
+        wg_barrier();
+        fetch_chunk(g + 3, ent3);
+      } else {
+        wait_vmcnt_lds_idle<0>();            // K of chunk g+1 and V of chunk g landed
+        wg_barrier();
+        fetch_half(true, g + 2, ent2);
+        fetch_half(false, g + 1, ent1);
+      }
       const int e1 = __builtin_amdgcn_readfirstlane(ent1);
       ent1 = entry(g + 2);
+      ent2 = entry(g + 3);
       ent3 = entry(g + 4);
       const int nkey0 = __builtin_amdgcn_readfirstlane((e1 >> 8) * S + (g + 1 < G ? ((g + 1) % NCK) * CK : 0));
       i32x8 pop;

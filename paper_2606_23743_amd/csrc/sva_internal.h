@@ -66,7 +66,7 @@ struct Fp8AttnArgs {
   float scale_log2;   // c * log2(e)
 };
 // Largest kept-block list (and nB for the dense form) the fp8 kernel holds.
-constexpr int kFp8MaxList = 2048;
+constexpr int kFp8MaxList = 2047;
 hipError_t launch_attention_fp8(const Dims& d, bool sparse, const Fp8AttnArgs& a, hipStream_t stream);
 
 hipError_t launch_pool(const Dims& d, const uint16_t* q, const uint16_t* k, float* q_pool,

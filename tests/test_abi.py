@@ -218,7 +218,7 @@ def test_fp8_entry_points_reject_before_launch(lib):
     assert f(ctypes.byref(p), A + 2, A, A, ctypes.byref(ok), None) == _lib.SVA_ERR_ALIGNMENT
     g = lib.sva_sparse_attention_fp8
     assert g(ctypes.byref(p), ctypes.byref(ok), A, A, 0, A, None, None) == _lib.SVA_ERR_SHAPE
-    assert g(ctypes.byref(p), ctypes.byref(ok), A, A, 2049, A, None, None) == _lib.SVA_ERR_UNSUPPORTED
+    assert g(ctypes.byref(p), ctypes.byref(ok), A, A, 2048, A, None, None) == _lib.SVA_ERR_UNSUPPORTED
     assert g(ctypes.byref(p), ctypes.byref(ok), None, A, 4, A, None, None) == _lib.SVA_ERR_INVALID_ARG
     assert g(ctypes.byref(p), ctypes.byref(ok), A, A, 4, A + 8, None, None) == _lib.SVA_ERR_ALIGNMENT
     assert g(ctypes.byref(p), ctypes.byref(_lib.Fp8Tensors(A, A, A, A + 2, A, A, None)), A, A, 4, A, None,
