@@ -305,7 +305,7 @@ def measure(args, wl, with_cpu: bool):
 
     # 8-bit (e4m3) attention on the same layer and kept-block lists: the
     # quantiser once, then the fp8 kernel (kept FLOPs against the fp8 peak)
-    if wl.head_dim in (64, 128):
+    if wl.head_dim in (64, 112, 128):
         quant = sva.quantize_fp8(prob, dev["q"], dev["k"], dev["v"], stream=stream)
         o8 = torch.empty_like(out)
         sva.sparse_attention_fp8(prob, quant, idx, cnt, out=o8, stream=stream)

@@ -243,24 +243,29 @@ int sva_token_scatter(const sva_tokens* t, int32_t k, const void* y_kept, const 
  * series: 8-bit attention with outlier smoothing; no formula is given, so
  * this is the reading implemented).  Codes are OCP e4m3 bytes (round to
  * nearest even); every scale is a power of two 2^e, e in [-127, 127], the
- * smallest with (group's largest magnitude) <= 448 * 2^e.  D in {64, 128}.
- * Np = nB * S (sva_fp8_padded_len); code rows past N are zero. ---- */
+ * smallest with (group's largest magnitude) <= 448 * 2^e.  D in {64, 112, 128}.
+ * Np = nB * S (sva_fp8_padded_len); code rows past N are zero.  D' = D
+ * rounded up to a multiple of 64 (sva_fp8_code_dim: 64, 128, 128); code
+ * channels D .. D'-1 are zero and have exponent 0. ---- */
 typedef struct sva_fp8_tensors {
-  void* q8;          /* u8 [B, H, Np, D]: Q codes, one exponent per query block */
-  void* k8;          /* u8 [B, H, Np, D]: codes of K - k_mean, one exponent per key block */
-  void* v8;          /* u8 [B, H, Np/64, D, 64]: V codes in 64-key tiles, channel-major
+  void* q8;          /* u8 [B, H, Np, D']: Q codes, one exponent per query block */
+  void* k8;          /* u8 [B, H, Np, D']: codes of K - k_mean, one exponent per key block */
+  void* v8;          /* u8 [B, H, Np/64, D', 64]: V codes in 64-key tiles, channel-major
                         inside a tile; one exponent per channel */
   int32_t* q_exp;    /* [B, H, nB] */
   int32_t* k_exp;    /* [B, H, nB] */
-  int32_t* v_exp;    /* [B, H, D] */
+  int32_t* v_exp;    /* [B, H, D'] */
   void* k_mean;      /* bf16 [B, H, D]: K's channel mean over the N tokens, rounded
                         once to bf16 (the smoothing vector; every logit of a query
                         moves by the same amount, so the softmax is unchanged) */
 } sva_fp8_tensors;
 
 /* Np = nB * S, the padded token count of the code tensors.  Host only.
- * SVA_ERR_UNSUPPORTED for D outside {64, 128}. */
+ * SVA_ERR_UNSUPPORTED for D outside {64, 112, 128}. */
 int sva_fp8_padded_len(const sva_problem* prob, int32_t* np);
+
+/* D', the channel count of the code tensors.  Host only. */
+int sva_fp8_code_dim(const sva_problem* prob, int32_t* dp);
 
 /* Quantise bf16 Q, K, V [B, H, N, D] into the code tensors and exponents of
  * `out` (all device memory the caller owns; k_mean is written too).  K is

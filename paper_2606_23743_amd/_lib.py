@@ -83,6 +83,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "sva_token_gather": [ctypes.POINTER(Tokens), ctypes.c_int32, vp, vp, vp, vp],
         "sva_token_scatter": [ctypes.POINTER(Tokens), ctypes.c_int32, vp, vp, vp, vp, vp],
         "sva_fp8_padded_len": [P, i32p],
+        "sva_fp8_code_dim": [P, i32p],
         "sva_quantize_fp8": [P, vp, vp, vp, ctypes.POINTER(Fp8Tensors), vp],
         "sva_sparse_attention_fp8": [P, ctypes.POINTER(Fp8Tensors), vp, vp, ctypes.c_int32, vp, vp, vp],
         "sva_dense_attention_fp8": [P, ctypes.POINTER(Fp8Tensors), vp, vp, vp],
@@ -325,20 +326,26 @@ def fp8_padded_len(prob: Problem) -> int:
     return out.value
 
 
+def fp8_code_dim(prob: Problem) -> int:
+    out = ctypes.c_int32(0)
+    _check(load().sva_fp8_code_dim(ctypes.byref(prob), ctypes.byref(out)), "sva_fp8_code_dim")
+    return out.value
+
+
 def _fp8_struct(t: dict) -> Fp8Tensors:
     return Fp8Tensors(*(_ptr(t.get(n)) for n in ("q8", "k8", "v8", "q_exp", "k_exp", "v_exp", "k_mean")))
 
 
 def _need_fp8(prob: Problem, t: dict, need_mean: bool):
     torch = _torch()
-    nb, npad = num_blocks(prob), fp8_padded_len(prob)
+    nb, npad, dp = num_blocks(prob), fp8_padded_len(prob), fp8_code_dim(prob)
     B, H, D = prob.batch, prob.heads, prob.head_dim
-    _need(t["q8"], torch.uint8, (B, H, npad, D), "q8")
-    _need(t["k8"], torch.uint8, (B, H, npad, D), "k8")
-    _need(t["v8"], torch.uint8, (B, H, npad // 64, D, 64), "v8")
+    _need(t["q8"], torch.uint8, (B, H, npad, dp), "q8")
+    _need(t["k8"], torch.uint8, (B, H, npad, dp), "k8")
+    _need(t["v8"], torch.uint8, (B, H, npad // 64, dp, 64), "v8")
     _need(t["q_exp"], torch.int32, (B, H, nb), "q_exp")
     _need(t["k_exp"], torch.int32, (B, H, nb), "k_exp")
-    _need(t["v_exp"], torch.int32, (B, H, D), "v_exp")
+    _need(t["v_exp"], torch.int32, (B, H, dp), "v_exp")
     if need_mean:
         _need(t["k_mean"], torch.bfloat16, (B, H, D), "k_mean")
 
@@ -351,15 +358,15 @@ def quantize_fp8(prob: Problem, q, k, v, out: Optional[dict] = None, stream=None
     for t, n in ((q, "q"), (k, "k"), (v, "v")):
         _need(t, torch.bfloat16, shp, n)
     if out is None:
-        nb, npad = num_blocks(prob), fp8_padded_len(prob)
+        nb, npad, dp = num_blocks(prob), fp8_padded_len(prob), fp8_code_dim(prob)
         B, H, D = prob.batch, prob.heads, prob.head_dim
         dev = q.device
-        out = {"q8": torch.empty((B, H, npad, D), dtype=torch.uint8, device=dev),
-               "k8": torch.empty((B, H, npad, D), dtype=torch.uint8, device=dev),
-               "v8": torch.empty((B, H, npad // 64, D, 64), dtype=torch.uint8, device=dev),
+        out = {"q8": torch.empty((B, H, npad, dp), dtype=torch.uint8, device=dev),
+               "k8": torch.empty((B, H, npad, dp), dtype=torch.uint8, device=dev),
+               "v8": torch.empty((B, H, npad // 64, dp, 64), dtype=torch.uint8, device=dev),
                "q_exp": torch.empty((B, H, nb), dtype=torch.int32, device=dev),
                "k_exp": torch.empty((B, H, nb), dtype=torch.int32, device=dev),
-               "v_exp": torch.empty((B, H, D), dtype=torch.int32, device=dev),
+               "v_exp": torch.empty((B, H, dp), dtype=torch.int32, device=dev),
                "k_mean": torch.empty((B, H, D), dtype=torch.bfloat16, device=dev)}
     _need_fp8(prob, out, True)
     st = _fp8_struct(out)

@@ -1,8 +1,10 @@
 // 8-bit (fp8 e4m3) block-sparse attention (Section 4.2.4 points to 8-bit
 // attention with outlier smoothing; Section 4.2.2 / Appendix A.2.2 the
 // block-sparse pattern it runs under).  Inputs come from the fp8 quantiser:
-// Q and K codes [B, H, Np, D] with one power-of-two exponent per block, V codes
-// in 64-key tiles [B, H, Np/64, D, 64] with one exponent per channel.
+// Q and K codes [B, H, Np, DP] with one power-of-two exponent per block, V
+// codes in 64-key tiles [B, H, Np/64, DP, 64] with one exponent per channel
+// (DP = D rounded up to a multiple of 64; the padding channels are zero and
+// are not written out).
 //
 // A workgroup is one query block of S tokens, S/32 waves of 32 queries (one
 // query per lane pair, as in the bf16 kernel).  Keys go in 64-key chunks, one
@@ -66,17 +68,18 @@ __device__ __forceinline__ int v_slot(int d, int p) { return p ^ ((d >> 2) & 3);
 template <int D, int S, bool SPARSE, bool OUT_F32>
 __global__ __launch_bounds__(2 * S) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_fp8_kernel(Fp8AttnArgs a) {
+  constexpr int DP = (D + 63) / 64 * 64;     // code channels (D = 112: 128, the last 16 zero)
   constexpr int NW = S / 32;                 // waves per workgroup
   constexpr int CK = 64;                     // keys per chunk
   constexpr int NCK = S / CK;                // chunks per block
   // LDS stages: four (loads three chunks ahead), or two at D = 128, S = 64 so
   // that four two-wave workgroups (two waves per SIMD) fit a CU's 160 KB
-  constexpr int NST = (D == 128 && S == 64) ? 2 : 4;
-  constexpr int TB = CK * D;                 // bytes of one K (or V) tile
-  constexpr int NPC = D / 16;                // 16-byte pieces per K row
+  constexpr int NST = (DP == 128 && S == 64) ? 2 : 4;
+  constexpr int TB = CK * DP;                // bytes of one K (or V) tile
+  constexpr int NPC = DP / 16;               // 16-byte pieces per K row
   constexpr int NUK = TB / 1024 / NW;        // direct-load pieces per wave per tile
-  constexpr int DQ = D / 64;                 // k-steps of S^T
-  constexpr int DT = D / 32;                 // 32-channel tiles of O^T
+  constexpr int DQ = DP / 64;                // k-steps of S^T
+  constexpr int DT = DP / 32;                // 32-channel tiles of O^T
   constexpr int GL = 2 * NUK;                // loads per wave per chunk
   static_assert(NUK >= 1, "tile split");
 
@@ -94,7 +97,7 @@ void attn_fp8_kernel(Fp8AttnArgs a) {
   const int row = __builtin_amdgcn_readfirstlane(xcd_remap(blockIdx.x, a.n_rows));  // (b*H + h)*nB + i
   const int bh = row / nB;
   const int i = row - bh * nB;
-  const size_t head = (size_t)bh * Np * D;
+  const size_t head = (size_t)bh * Np * DP;
 
   // ---- the block list: compacted, with each block's K exponent ----
   if constexpr (SPARSE) {
@@ -130,29 +133,29 @@ void attn_fp8_kernel(Fp8AttnArgs a) {
   i32x8 qop[DQ];
 #pragma unroll
   for (int s = 0; s < DQ; ++s) {
-    const i32x4 lo = *reinterpret_cast<const i32x4*>(Qh + (size_t)qr * D + s * 64 + hf * 16);
-    const i32x4 hi = *reinterpret_cast<const i32x4*>(Qh + (size_t)qr * D + s * 64 + 32 + hf * 16);
+    const i32x4 lo = *reinterpret_cast<const i32x4*>(Qh + (size_t)qr * DP + s * 64 + hf * 16);
+    const i32x4 hi = *reinterpret_cast<const i32x4*>(Qh + (size_t)qr * DP + s * 64 + 32 + hf * 16);
     qop[s] = i32x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
   }
   const int q_scale = a.q_exp[row] + 127;
   int v_scale[DT];
 #pragma unroll
-  for (int dt = 0; dt < DT; ++dt) v_scale[dt] = a.v_exp[(size_t)bh * D + dt * 32 + l32] + 127;
+  for (int dt = 0; dt < DT; ++dt) v_scale[dt] = a.v_exp[(size_t)bh * DP + dt * 32 + l32] + 127;
 
   // ---- direct global -> LDS fetch of one chunk (this wave's 1 KB pieces) ----
   // K piece u: rows u*RPK .. (RPK = 1024/D), lane L -> row u*RPK + L/NPC, slot
   // L%NPC, holding global piece k_slot(row, L%NPC).  V piece u: channels
   // u*16 .. u*16+15, lane L -> channel u*16 + L/4, slot L%4.  Both tiles of the
   // chunk starting at key key0 begin at byte key0*D of their head.
-  constexpr int RPK = 1024 / D;
-  const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc((void*)(a.k8 + head), (short)0, Np * D, 0x00020000);
-  const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc((void*)(a.v8 + head), (short)0, Np * D, 0x00020000);
+  constexpr int RPK = 1024 / DP;
+  const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc((void*)(a.k8 + head), (short)0, Np * DP, 0x00020000);
+  const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc((void*)(a.v8 + head), (short)0, Np * DP, 0x00020000);
   int kgv[NUK], vgv[NUK];
 #pragma unroll
   for (int v = 0; v < NUK; ++v) {
     const int u = w * NUK + v;
     const int kr = u * RPK + lane / NPC;
-    kgv[v] = kr * D + k_slot<D>(kr, lane % NPC) * 16;
+    kgv[v] = kr * DP + k_slot<DP>(kr, lane % NPC) * 16;
     const int vd = u * 16 + lane / 4;
     vgv[v] = vd * CK + v_slot(vd, lane % 4) * 16;
   }
@@ -172,8 +175,8 @@ void attn_fp8_kernel(Fp8AttnArgs a) {
     const int st = g & (NST - 1);
 #pragma unroll
     for (int v = 0; v < NUK; ++v) {
-      if (tk) bll(krs, ks_base + st * TB + (w * NUK + v) * 1024, kgv[v], key0 * D);
-      else bll(vrs, vs_base + st * TB + (w * NUK + v) * 1024, vgv[v], key0 * D);
+      if (tk) bll(krs, ks_base + st * TB + (w * NUK + v) * 1024, kgv[v], key0 * DP);
+      else bll(vrs, vs_base + st * TB + (w * NUK + v) * 1024, vgv[v], key0 * DP);
     }
   };
   auto fetch_chunk = [&](int g, int e) {
@@ -186,8 +189,8 @@ void attn_fp8_kernel(Fp8AttnArgs a) {
 #pragma unroll
   for (int s = 0; s < DQ; ++s) {
     const int q = pi_row(l32);
-    koff[s][0] = q * D + k_slot<D>(q, s * 4 + hf) * 16;
-    koff[s][1] = q * D + k_slot<D>(q, s * 4 + 2 + hf) * 16;
+    koff[s][0] = q * DP + k_slot<DP>(q, s * 4 + hf) * 16;
+    koff[s][1] = q * DP + k_slot<DP>(q, s * 4 + 2 + hf) * 16;
   }
   const int voff0 = l32 * CK + v_slot(l32, hf) * 16;        // channel l32 (+32*dt: same slot pattern)
   const int voff1 = l32 * CK + v_slot(l32, 2 + hf) * 16;
@@ -207,8 +210,8 @@ void attn_fp8_kernel(Fp8AttnArgs a) {
       sc[t] = f32x16{};
 #pragma unroll
       for (int s = 0; s < DQ; ++s) {
-        const i32x4 lo = *reinterpret_cast<const i32x4*>(kt + koff[s][0] + t * 32 * D);
-        const i32x4 hi = *reinterpret_cast<const i32x4*>(kt + koff[s][1] + t * 32 * D);
+        const i32x4 lo = *reinterpret_cast<const i32x4*>(kt + koff[s][0] + t * 32 * DP);
+        const i32x4 hi = *reinterpret_cast<const i32x4*>(kt + koff[s][1] + t * 32 * DP);
         const i32x8 kop = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
         sc[t] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(kop, qop[s], sc[t], 0, 0, 0, kscale, 0, q_scale);
       }
@@ -369,6 +372,7 @@ void attn_fp8_kernel(Fp8AttnArgs a) {
 #pragma unroll
       for (int r4 = 0; r4 < 4; ++r4) {
         const int d = dt * 32 + r4 * 8 + hf * 4;
+        if (DP != D && d >= D) continue;     // padding channels
         const float o0 = oacc[dt][r4 * 4 + 0] * inv, o1 = oacc[dt][r4 * 4 + 1] * inv;
         const float o2 = oacc[dt][r4 * 4 + 2] * inv, o3 = oacc[dt][r4 * 4 + 3] * inv;
         if constexpr (OUT_F32) {
@@ -408,6 +412,8 @@ hipError_t launch_attention_fp8(const Dims& d, bool sparse, const Fp8AttnArgs& a
   switch (d.D * 1000 + d.S) {
     case 64064: return launch_fp8_ds<64, 64>(d, sparse, a, stream);
     case 64128: return launch_fp8_ds<64, 128>(d, sparse, a, stream);
+    case 112064: return launch_fp8_ds<112, 64>(d, sparse, a, stream);
+    case 112128: return launch_fp8_ds<112, 128>(d, sparse, a, stream);
     case 128064: return launch_fp8_ds<128, 64>(d, sparse, a, stream);
     case 128128: return launch_fp8_ds<128, 128>(d, sparse, a, stream);
     default: return hipErrorInvalidValue;

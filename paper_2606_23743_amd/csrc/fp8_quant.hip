@@ -10,11 +10,14 @@
 //          channel maxima of |V| (V's per-channel exponents).
 //   Q, K   one workgroup per (tensor, b, h, block): K first subtracts the
 //          smoothing vector in float32; the block's largest magnitude sets
-//          its exponent; codes are written [B, H, Np, D] (Np = nB * S, rows
+//          its exponent; codes are written [B, H, Np, DP] (Np = nB * S, rows
 //          past N zero).
 //   V      one workgroup per (b, h, block): codes with the channel exponents,
-//          transposed through LDS into 64-key tiles [B, H, Np/64, D, 64], the
+//          transposed through LDS into 64-key tiles [B, H, Np/64, DP, 64], the
 //          layout the attention kernel stages directly.
+// DP is D rounded up to a multiple of 64 (the fp8 matrix instructions take 64
+// channels per step): at D = 112 the codes of channels 112..127 are zero and
+// their V exponent is 0.
 #include "sva_internal.h"
 
 namespace sva {
@@ -56,18 +59,20 @@ __device__ __forceinline__ uint16_t round_bf16_bits(double x) {
 
 template <int D>
 __global__ __launch_bounds__(kStatThreads) void fp8_stats_kernel(Fp8QuantArgs a) {
-  constexpr int TPR = D / 8;                  // lanes per token row
+  constexpr int DP = (D + 63) / 64 * 64;
+  constexpr int TPR = DP / 8;                 // lanes per token row
   constexpr int RPP = kStatThreads / TPR;     // rows per pass
-  __shared__ double part_s[RPP][D];
-  __shared__ float part_m[RPP][D];
+  __shared__ double part_s[RPP][DP];
+  __shared__ float part_m[RPP][DP];
   const int bh = blockIdx.x;
   const int N = a.N;
   const int r0 = threadIdx.x / TPR, c = threadIdx.x % TPR;
+  const bool live = c < D / 8;                // D = 112: lanes 14, 15 hold no channel
   const uint16_t* K = a.k + (size_t)bh * N * D;
   const uint16_t* V = a.v + (size_t)bh * N * D;
   double s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
   float m[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  for (int r = r0; r < N; r += RPP) {
+  for (int r = r0; live && r < N; r += RPP) {
     const uint4 kw = *reinterpret_cast<const uint4*>(K + (size_t)r * D + c * 8);
     const uint4 vw = *reinterpret_cast<const uint4*>(V + (size_t)r * D + c * 8);
     const float kx[8] = {lo16(kw.x), hi16(kw.x), lo16(kw.y), hi16(kw.y), lo16(kw.z), hi16(kw.z), lo16(kw.w), hi16(kw.w)};
@@ -84,7 +89,7 @@ __global__ __launch_bounds__(kStatThreads) void fp8_stats_kernel(Fp8QuantArgs a)
     part_m[r0][c * 8 + e] = m[e];
   }
   __syncthreads();
-  if (threadIdx.x < D) {
+  if (threadIdx.x < DP) {
     const int d = threadIdx.x;
     double t = 0.0;
     float mx = 0.0f;
@@ -92,15 +97,16 @@ __global__ __launch_bounds__(kStatThreads) void fp8_stats_kernel(Fp8QuantArgs a)
       t += part_s[r][d];
       mx = fmaxf(mx, part_m[r][d]);
     }
-    a.k_mean[(size_t)bh * D + d] = round_bf16_bits(t / (double)N);
-    a.v_exp[(size_t)bh * D + d] = scale_exp(mx);
+    if (d < D) a.k_mean[(size_t)bh * D + d] = round_bf16_bits(t / (double)N);
+    a.v_exp[(size_t)bh * DP + d] = scale_exp(mx);     // padding channels: 0
   }
 }
 
 // Q (blockIdx.y == 0) or smoothed K (blockIdx.y == 1) of one block
 template <int D, int S>
 __global__ __launch_bounds__(kThreads) void fp8_quant_qk_kernel(Fp8QuantArgs a) {
-  constexpr int TPR = D / 8;
+  constexpr int DP = (D + 63) / 64 * 64;
+  constexpr int TPR = DP / 8;
   constexpr int RPP = kThreads / TPR;
   constexpr int NP = S / RPP;
   __shared__ float red[kThreads / 64];
@@ -111,10 +117,11 @@ __global__ __launch_bounds__(kThreads) void fp8_quant_qk_kernel(Fp8QuantArgs a) 
   const int i = row - bh * nB;
   const int valid = min(S, N - i * S);
   const uint16_t* src = (is_k ? a.k : a.q) + ((size_t)bh * N + (size_t)i * S) * D;
-  uint8_t* dst = (is_k ? a.k8 : a.q8) + ((size_t)bh * Np + (size_t)i * S) * D;
+  uint8_t* dst = (is_k ? a.k8 : a.q8) + ((size_t)bh * Np + (size_t)i * S) * DP;
   const int r0 = threadIdx.x / TPR, c = threadIdx.x % TPR;
+  const bool live = c < D / 8;                // padding lanes write zero codes
   float sub[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  if (is_k) {
+  if (is_k && live) {
     const uint4 mw = *reinterpret_cast<const uint4*>(a.k_mean + (size_t)bh * D + c * 8);
     const float mv[8] = {lo16(mw.x), hi16(mw.x), lo16(mw.y), hi16(mw.y), lo16(mw.z), hi16(mw.z), lo16(mw.w), hi16(mw.w)};
 #pragma unroll
@@ -126,11 +133,11 @@ __global__ __launch_bounds__(kThreads) void fp8_quant_qk_kernel(Fp8QuantArgs a) 
   for (int p = 0; p < NP; ++p) {
     const int r = r0 + p * RPP;
     uint4 w = make_uint4(0, 0, 0, 0);
-    if (r < valid) w = *reinterpret_cast<const uint4*>(src + (size_t)r * D + c * 8);
+    if (live && r < valid) w = *reinterpret_cast<const uint4*>(src + (size_t)r * D + c * 8);
     const float v[8] = {lo16(w.x), hi16(w.x), lo16(w.y), hi16(w.y), lo16(w.z), hi16(w.z), lo16(w.w), hi16(w.w)};
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      x[p][e] = r < valid ? v[e] - sub[e] : 0.0f;       // float32 difference (K), exact copy (Q)
+      x[p][e] = (live && r < valid) ? v[e] - sub[e] : 0.0f;   // float32 difference (K), exact copy (Q)
       amax = fmaxf(amax, fabsf(x[p][e]));
     }
   }
@@ -149,13 +156,14 @@ __global__ __launch_bounds__(kThreads) void fp8_quant_qk_kernel(Fp8QuantArgs a) 
     uint2 o;
     o.x = pack4_e4m3(ldexpf(x[p][0], -e), ldexpf(x[p][1], -e), ldexpf(x[p][2], -e), ldexpf(x[p][3], -e));
     o.y = pack4_e4m3(ldexpf(x[p][4], -e), ldexpf(x[p][5], -e), ldexpf(x[p][6], -e), ldexpf(x[p][7], -e));
-    *reinterpret_cast<uint2*>(dst + (size_t)r * D + c * 8) = o;   // rows past N: zeros
+    *reinterpret_cast<uint2*>(dst + (size_t)r * DP + c * 8) = o;   // rows past N, padding: zeros
   }
 }
 
 // V of one block, transposed into 64-key tiles
 template <int D, int S>
 __global__ __launch_bounds__(kThreads) void fp8_quant_v_kernel(Fp8QuantArgs a) {
+  constexpr int DP = (D + 63) / 64 * 64;
   __shared__ __attribute__((aligned(16))) uint16_t tile[S][D];
   const int row = xcd_remap(blockIdx.x, a.n_rows);
   const int nB = a.nB, N = a.N, Np = a.Np;
@@ -172,17 +180,19 @@ __global__ __launch_bounds__(kThreads) void fp8_quant_v_kernel(Fp8QuantArgs a) {
   __syncthreads();
   const int nC = Np / 64;
   // item (d, 8-token group): consecutive threads take consecutive channels
-  for (int u = threadIdx.x; u < D * (S / 8); u += kThreads) {
-    const int d = u % D, t8 = u / D;
-    const int e = a.v_exp[(size_t)bh * D + d];
-    float v[8];
+  for (int u = threadIdx.x; u < DP * (S / 8); u += kThreads) {
+    const int d = u % DP, t8 = u / DP;
+    uint2 o = make_uint2(0, 0);                          // padding channels: zero codes
+    if (d < D) {
+      const int e = a.v_exp[(size_t)bh * DP + d];
+      float v[8];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) v[k] = ldexpf(__uint_as_float((uint32_t)tile[t8 * 8 + k][d] << 16), -e);
-    uint2 o;
-    o.x = pack4_e4m3(v[0], v[1], v[2], v[3]);
-    o.y = pack4_e4m3(v[4], v[5], v[6], v[7]);
+      for (int k = 0; k < 8; ++k) v[k] = ldexpf(__uint_as_float((uint32_t)tile[t8 * 8 + k][d] << 16), -e);
+      o.x = pack4_e4m3(v[0], v[1], v[2], v[3]);
+      o.y = pack4_e4m3(v[4], v[5], v[6], v[7]);
+    }
     const int tok = i * S + t8 * 8;                      // first token of the group
-    const size_t off = (((size_t)bh * nC + tok / 64) * D + d) * 64 + (tok % 64);
+    const size_t off = (((size_t)bh * nC + tok / 64) * DP + d) * 64 + (tok % 64);
     *reinterpret_cast<uint2*>(a.v8 + off) = o;
   }
 }
@@ -206,6 +216,8 @@ hipError_t launch_quantize_fp8(const Dims& d, const Fp8QuantArgs& args, hipStrea
   switch (d.D * 1000 + d.S) {
     case 64064: launch_quant_ds<64, 64>(a, BH, stream); break;
     case 64128: launch_quant_ds<64, 128>(a, BH, stream); break;
+    case 112064: launch_quant_ds<112, 64>(a, BH, stream); break;
+    case 112128: launch_quant_ds<112, 128>(a, BH, stream); break;
     case 128064: launch_quant_ds<128, 64>(a, BH, stream); break;
     case 128128: launch_quant_ds<128, 128>(a, BH, stream); break;
     default: return hipErrorInvalidValue;

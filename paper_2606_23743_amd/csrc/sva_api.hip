@@ -104,12 +104,14 @@ int hip_status(hipError_t e) { return e == hipSuccess ? SVA_OK : SVA_ERR_HIP; }
 // ---- fp8 (e4m3) quantisation and attention ----
 
 namespace {
+int fp8_code_dim(int D) { return (D + 63) / 64 * 64; }
+
 int check_fp8(const sva_problem* prob, Dims* d) {
   const int st = check_problem(prob, d);
   if (st != SVA_OK) return st;
-  if (d->D != 64 && d->D != 128) return SVA_ERR_UNSUPPORTED;
+  // (D = 112 is carried as 128 code channels, the last 16 zero)
   // per-head byte ranges of the padded codes are 32-bit buffer offsets
-  if ((int64_t)d->nB * d->S * d->D > INT32_MAX) return SVA_ERR_SHAPE;
+  if ((int64_t)d->nB * d->S * fp8_code_dim(d->D) > INT32_MAX) return SVA_ERR_SHAPE;
   return SVA_OK;
 }
 
@@ -354,6 +356,15 @@ int sva_fp8_padded_len(const sva_problem* prob, int32_t* np) {
   const int st = check_fp8(prob, &d);
   if (st != SVA_OK) return st;
   *np = d.nB * d.S;
+  return SVA_OK;
+}
+
+int sva_fp8_code_dim(const sva_problem* prob, int32_t* dp) {
+  if (!dp) return SVA_ERR_INVALID_ARG;
+  Dims d;
+  const int st = check_fp8(prob, &d);
+  if (st != SVA_OK) return st;
+  *dp = fp8_code_dim(d.D);
   return SVA_OK;
 }
 

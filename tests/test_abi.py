@@ -25,7 +25,7 @@ def test_every_declared_symbol_is_exported(lib):
     assert set(names) >= {"sva_pool_blocks", "sva_select_blocks", "sva_sparse_attention",
                           "sva_dense_attention", "sva_num_blocks", "sva_max_keep",
                           "sva_qknorm_rope_pool", "sva_token_keep_count", "sva_token_select",
-                          "sva_token_select_workspace", "sva_fp8_padded_len", "sva_quantize_fp8",
+                          "sva_token_select_workspace", "sva_fp8_padded_len", "sva_fp8_code_dim", "sva_quantize_fp8",
                           "sva_sparse_attention_fp8", "sva_dense_attention_fp8",
                           "sva_token_gather", "sva_token_scatter", "sva_status_string",
                           "sva_version"}
@@ -203,8 +203,11 @@ def test_fp8_entry_points_reject_before_launch(lib):
     p = sva.problem_for(workloads.TINY)                       # D=64, S=64
     n = ctypes.c_int32()
     assert lib.sva_fp8_padded_len(ctypes.byref(p), ctypes.byref(n)) == _lib.SVA_OK and n.value == 1024
-    assert lib.sva_fp8_padded_len(ctypes.byref(sva.problem_for(workloads.SMALL_2B)), ctypes.byref(n)) \
-        == _lib.SVA_ERR_UNSUPPORTED                           # D=112
+    p112 = sva.problem_for(workloads.SMALL_2B)                # D=112: carried as 128 code channels
+    assert lib.sva_fp8_padded_len(ctypes.byref(p112), ctypes.byref(n)) == _lib.SVA_OK and n.value == 512 * 64
+    assert lib.sva_fp8_code_dim(ctypes.byref(p112), ctypes.byref(n)) == _lib.SVA_OK and n.value == 128
+    assert lib.sva_fp8_code_dim(ctypes.byref(p), ctypes.byref(n)) == _lib.SVA_OK and n.value == 64
+    assert lib.sva_fp8_code_dim(ctypes.byref(p), None) == _lib.SVA_ERR_INVALID_ARG
     assert lib.sva_fp8_padded_len(ctypes.byref(p), None) == _lib.SVA_ERR_INVALID_ARG
     A = 1 << 20
     ok = _lib.Fp8Tensors(A, A, A, A, A, A, A)
@@ -225,5 +228,5 @@ def test_fp8_entry_points_reject_before_launch(lib):
              None) == _lib.SVA_ERR_ALIGNMENT
     h = lib.sva_dense_attention_fp8
     assert h(ctypes.byref(p), None, A, None, None) == _lib.SVA_ERR_INVALID_ARG
-    assert h(ctypes.byref(sva.problem_for(workloads.SMALL_2B)), ctypes.byref(ok), A, None, None) \
-        == _lib.SVA_ERR_UNSUPPORTED
+    assert h(ctypes.byref(sva.problem(1, 1, 2048 * 64, 64, (1, 1, 2048 * 64), 64)), ctypes.byref(ok), A, None,
+             None) == _lib.SVA_ERR_UNSUPPORTED                # nB = 2048 above the list bound

@@ -46,6 +46,7 @@ def _check_quant(wl, bits, quant, heads=None):
     """Codes, exponents and the smoothing vector against the oracle (all heads,
     or the listed (b, h))."""
     B, H, N, D, S = wl.batch, wl.heads, wl.seq_len, wl.head_dim, wl.block
+    DP = (D + 63) // 64 * 64                                  # code channels; D..DP-1 are zero
     heads = heads or [(b, h) for b in range(B) for h in range(H)]
     q8, k8, v8 = _np(quant["q8"]), _np(quant["k8"]), _np(quant["v8"])
     qe, ke, ve = _np(quant["q_exp"]), _np(quant["k_exp"]), _np(quant["v_exp"])
@@ -56,16 +57,17 @@ def _check_quant(wl, bits, quant, heads=None):
         ref = of8.quantize_qkv(x["q"], x["k"], x["v"], S)
         assert np.array_equal(qe[b, h], ref["q_exp"][0, 0]), (b, h)
         assert np.array_equal(ke[b, h], ref["k_exp"][0, 0]), (b, h)
-        assert np.array_equal(ve[b, h], ref["v_exp"][0, 0]), (b, h)
+        assert np.array_equal(ve[b, h, :D], ref["v_exp"][0, 0]) and not ve[b, h, D:].any(), (b, h)
         want_mean = oracle.bf16_bits_to_f64(km[b, h])
         assert np.array_equal(want_mean, ref["k_mean"][0, 0]), (b, h)
-        assert np.array_equal(E4M3[q8[b, h, :N]], ref["q_code"][0, 0]), (b, h)
-        assert np.array_equal(E4M3[k8[b, h, :N]], ref["k_code"][0, 0]), (b, h)
+        assert np.array_equal(E4M3[q8[b, h, :N, :D]], ref["q_code"][0, 0]), (b, h)
+        assert np.array_equal(E4M3[k8[b, h, :N, :D]], ref["k_code"][0, 0]), (b, h)
         assert not q8[b, h, N:].any() and not k8[b, h, N:].any()
-        vt = E4M3[v8[b, h]]                                   # [Np/64, D, 64] -> [Np, D]
-        vt = vt.transpose(0, 2, 1).reshape(-1, D)
-        assert np.array_equal(vt[:N], ref["v_code"][0, 0]), (b, h)
-        assert not vt[N:].any()
+        assert not q8[b, h, :, D:].any() and not k8[b, h, :, D:].any()
+        vt = E4M3[v8[b, h]]                                   # [Np/64, DP, 64] -> [Np, DP]
+        vt = vt.transpose(0, 2, 1).reshape(-1, DP)
+        assert np.array_equal(vt[:N, :D], ref["v_code"][0, 0]), (b, h)
+        assert not vt[N:].any() and not vt[:, D:].any()
 
 
 def _dequantised(bits, S, b, h):
@@ -121,6 +123,8 @@ CASES = [
     ("d64_s64_ragged", 2, 1, 64, (2, 7, 9), 64, 0.4),
     ("d64_s128", 1, 2, 64, (4, 4, 24), 128, 0.5),
     ("d128_s128_short", 1, 1, 128, (1, 1, 40), 128, 1.0),
+    ("d112_s64_ragged", 1, 2, 112, (2, 7, 9), 64, 0.4),       # 112 channels carried as 128
+    ("d112_s128", 2, 1, 112, (3, 4, 20), 128, 0.5),
 ]
 
 
