@@ -166,6 +166,42 @@ def test_fp8_quantise_and_attend(name, B, H, D, grid, S, keep):
                 f"(model {dpred:.2e})")
 
 
+@pytest.mark.parametrize("S,D,step", [(128, 128, 3.0), (128, 128, 40.0), (64, 128, 3.0), (64, 112, 40.0),
+                                      (128, 64, -3.0)])
+def test_fp8_guard_rescales_with_rising_logits(S, D, step):
+    """Logits move by `step` (log2 units) from one kept block to the next.  Rising,
+    every block's maximum exceeds the reference by more than the kernel's
+    guard, so O and l are rescaled before its probabilities are formed (which
+    would otherwise pass e4m3's largest value); falling, the later blocks'
+    weights sink toward e4m3's subnormals.  Both must match the oracle."""
+    nblk = 5
+    wl = workloads.small_case(f"growth_{S}_{D}", 1, 1, D, (1, nblk * S // 16, 16), S, "topk", topk=nblk,
+                              seed=41)
+    bits = inputs.generate(wl)
+    f = {n: inputs.bf16_bits_to_f32(bits[n]).copy() for n in ("q", "k", "v")}
+    c = scale_of(wl)
+    f["q"][0, 0] = 1.0
+    for b in range(nblk):
+        val = step * (b - nblk // 2) / (np.log2(np.e) * c * D)
+        f["k"][0, 0, b * S:(b + 1) * S] = val + 0.05 * f["k"][0, 0, b * S:(b + 1) * S]
+    new_bits = {n: inputs._round_bf16(f[n]) for n in f}
+    dev = device_inputs(new_bits)
+    prob = sva.problem_for(wl)
+    quant = sva.quantize_fp8(prob, dev["q"], dev["k"], dev["v"])
+    rows = [list(range(nblk)) for _ in range(nblk)]
+    idx = torch.from_numpy(np.array(rows, dtype=np.int32).reshape(1, 1, nblk, nblk)).cuda()
+    cnt = torch.from_numpy(np.full((1, 1, nblk), nblk, dtype=np.int32)).cuda()
+    out, lse = sva.sparse_attention_fp8(prob, quant, idx, cnt, want_lse=True)
+    torch.cuda.synchronize()
+    o = _np(out.float()).astype(np.float64)
+    assert np.isfinite(o).all()
+    ref = _dequantised(new_bits, S, 0, 0)
+    span = np.abs(c * (ref["q_hat"][0, 0] @ ref["k_hat"][0, 0].T)).max() * np.log2(np.e)
+    assert span > 2.0 * abs(step), span                       # the regime this test is about
+    rms, pred = _check_attention(o[0, 0], _np(lse)[0, 0], ref, rows, S, c, range(nblk))
+    assert rms <= 2.0 * pred + 2e-3, (rms, pred)
+
+
 def test_fp8_f32_output_and_empty_rows():
     wl = workloads.small_case("f32_empty", 1, 2, 128, (2, 4, 32), 128, "topk", keep_ratio=0.5, seed=67)
     bits = inputs.generate(wl)
