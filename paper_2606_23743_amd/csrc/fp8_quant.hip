@@ -5,9 +5,9 @@
 // instructions apply themselves): for a group with largest magnitude a, e is
 // the smallest exponent with a <= 448 * 2^e, so x * 2^-e is exact in float32
 // and the hardware conversion (round to nearest even) gives the code.
-//   stats  one workgroup per (b, h): the float64 channel sums of K over all N
-//          tokens (mean rounded once to bf16: the smoothing vector) and the
-//          channel maxima of |V| (V's per-channel exponents).
+//   stats  the float64 channel sums of K over all N tokens (mean rounded once
+//          to bf16: the smoothing vector) and the channel maxima of |V| (V's
+//          per-channel exponents): segment partials, then a fixed-order sum.
 //   Q, K   one workgroup per (tensor, b, h, block): K first subtracts the
 //          smoothing vector in float32; the block's largest magnitude sets
 //          its exponent; codes are written [B, H, Np, DP] (Np = nB * S, rows
@@ -57,22 +57,32 @@ __device__ __forceinline__ uint16_t round_bf16_bits(double x) {
   return (uint16_t)(__float_as_uint((float)r) >> 16);
 }
 
+// Channel statistics in two steps, so that every CU takes part: segment
+// workgroups of kStatRows tokens write float64 partial sums of K and float32
+// partial maxima of |V| per channel, then one small workgroup per (b, h) adds
+// them in segment order (deterministic).  The partials are staged in the
+// head's K-code region, which the Q/K quantiser overwrites right after (it is
+// at least 12 * nseg * DP bytes: Np >= 64 tokens of DP bytes each).
+constexpr int kStatRows = 1024;
+
 template <int D>
-__global__ __launch_bounds__(kStatThreads) void fp8_stats_kernel(Fp8QuantArgs a) {
+__global__ __launch_bounds__(kStatThreads) void fp8_stats_partial_kernel(Fp8QuantArgs a) {
   constexpr int DP = (D + 63) / 64 * 64;
   constexpr int TPR = DP / 8;                 // lanes per token row
   constexpr int RPP = kStatThreads / TPR;     // rows per pass
   __shared__ double part_s[RPP][DP];
   __shared__ float part_m[RPP][DP];
-  const int bh = blockIdx.x;
+  const int seg = blockIdx.x, bh = blockIdx.y;
+  const int nseg = gridDim.x;
   const int N = a.N;
   const int r0 = threadIdx.x / TPR, c = threadIdx.x % TPR;
   const bool live = c < D / 8;                // D = 112: lanes 14, 15 hold no channel
   const uint16_t* K = a.k + (size_t)bh * N * D;
   const uint16_t* V = a.v + (size_t)bh * N * D;
+  const int n0 = seg * kStatRows, n1 = min(N, n0 + kStatRows);
   double s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
   float m[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  for (int r = r0; live && r < N; r += RPP) {
+  for (int r = n0 + r0; live && r < n1; r += RPP) {
     const uint4 kw = *reinterpret_cast<const uint4*>(K + (size_t)r * D + c * 8);
     const uint4 vw = *reinterpret_cast<const uint4*>(V + (size_t)r * D + c * 8);
     const float kx[8] = {lo16(kw.x), hi16(kw.x), lo16(kw.y), hi16(kw.y), lo16(kw.z), hi16(kw.z), lo16(kw.w), hi16(kw.w)};
@@ -97,9 +107,28 @@ __global__ __launch_bounds__(kStatThreads) void fp8_stats_kernel(Fp8QuantArgs a)
       t += part_s[r][d];
       mx = fmaxf(mx, part_m[r][d]);
     }
-    if (d < D) a.k_mean[(size_t)bh * D + d] = round_bf16_bits(t / (double)N);
-    a.v_exp[(size_t)bh * DP + d] = scale_exp(mx);     // padding channels: 0
+    unsigned char* scratch = a.k8 + (size_t)bh * a.Np * DP;
+    reinterpret_cast<double*>(scratch)[(size_t)seg * DP + d] = t;
+    reinterpret_cast<float*>(scratch + (size_t)nseg * DP * sizeof(double))[(size_t)seg * DP + d] = mx;
   }
+}
+
+template <int D>
+__global__ __launch_bounds__(128) void fp8_stats_final_kernel(Fp8QuantArgs a, int nseg) {
+  constexpr int DP = (D + 63) / 64 * 64;
+  const int bh = blockIdx.x, d = threadIdx.x;
+  if (d >= DP) return;
+  const unsigned char* scratch = a.k8 + (size_t)bh * a.Np * DP;
+  const double* ps = reinterpret_cast<const double*>(scratch);
+  const float* pm = reinterpret_cast<const float*>(scratch + (size_t)nseg * DP * sizeof(double));
+  double t = 0.0;
+  float mx = 0.0f;
+  for (int g = 0; g < nseg; ++g) {           // segment order: deterministic
+    t += ps[(size_t)g * DP + d];
+    mx = fmaxf(mx, pm[(size_t)g * DP + d]);
+  }
+  if (d < D) a.k_mean[(size_t)bh * D + d] = round_bf16_bits(t / (double)a.N);
+  a.v_exp[(size_t)bh * DP + d] = scale_exp(mx);     // padding channels: 0
 }
 
 // Q (blockIdx.y == 0) or smoothed K (blockIdx.y == 1) of one block
@@ -199,7 +228,9 @@ __global__ __launch_bounds__(kThreads) void fp8_quant_v_kernel(Fp8QuantArgs a) {
 
 template <int D, int S>
 void launch_quant_ds(const Fp8QuantArgs& a, int BH, hipStream_t stream) {
-  hipLaunchKernelGGL((fp8_stats_kernel<D>), dim3(BH), dim3(kStatThreads), 0, stream, a);
+  const int nseg = (a.N + kStatRows - 1) / kStatRows;
+  hipLaunchKernelGGL((fp8_stats_partial_kernel<D>), dim3(nseg, BH), dim3(kStatThreads), 0, stream, a);
+  hipLaunchKernelGGL((fp8_stats_final_kernel<D>), dim3(BH), dim3(128), 0, stream, a, nseg);
   hipLaunchKernelGGL((fp8_quant_qk_kernel<D, S>), dim3(a.n_rows, 2), dim3(kThreads), 0, stream, a);
   hipLaunchKernelGGL((fp8_quant_v_kernel<D, S>), dim3(a.n_rows), dim3(kThreads), 0, stream, a);
 }
