@@ -11,7 +11,7 @@ before the PV product (l sums the same rounded weights), so
 a weighted sum of independent rounding errors.  Rounding to nearest with 3
 mantissa bits errs by at most e = 2^-4 p in the normal range (2^-16 of the
 row maximum among the subnormals, given the GPU's 2^6 offset), uniformly, so each term has standard deviation at most
-e_m/sqrt(3) * |V_m - O|.  The test predicts the RMS error of every output
+e_m/sqrt(3) * |V_m - O|; a bf16 output adds its own rounding (2^-8 |O| at most).  The test predicts the RMS error of every output
 element from the oracle's p and V and requires the observed RMS to stay below
 twice that; the worst case, all errors aligned (sum of e_m |V_m - O| / l), is
 checked per element.  The fp8 matrix instructions add their own summation
@@ -75,14 +75,16 @@ def _dequantised(bits, S, b, h):
     return of8.quantize_qkv(x["q"], x["k"], x["v"], S)
 
 
-def _check_attention(got, got_lse, quant_ref, kept_row_lists, S, scale, rows):
+def _check_attention(got, got_lse, quant_ref, kept_row_lists, S, scale, rows, out_bf16=True):
     """got: [N, D] float64 GPU output of one head; rows: query block ids to check.
     Per weight p (oracle units, row maximum 1) the GPU's rounding errs by at
     most e = max(2^-4 p, min(p, 2^-16)): 3 mantissa bits, and e4m3 spacing
     2^-9 below 2^-6, where the GPU holds p times 2^(6 + k), 0 <= k <= 2.75
     (its probabilities are offset by 2^6 from a reference within 2.75 of the
     row maximum); plus 4e-3 p for the float32 summation inside the fp8
-    instructions.  Returns (observed rms, model rms)."""
+    instructions.  A bf16 output adds its own rounding, at most half an ulp
+    (2^-8 |O|) and uniform: variance (2^-8 |O|)^2 / 3 per element.  Returns
+    (observed rms, model rms)."""
     q, k, v = (quant_ref[n][0, 0] for n in ("q_hat", "k_hat", "v_hat"))
     N = q.shape[0]
     err2, pred2, cnt = 0.0, 0.0, 0
@@ -94,8 +96,9 @@ def _check_attention(got, got_lse, quant_ref, kept_row_lists, S, scale, rows):
             continue
         keys = np.concatenate([np.arange(j * S, min(N, (j + 1) * S)) for j in blocks])
         vk = v[keys]
-        for q0 in range(qa, qb, 8):                          # a few queries at a time
-            q1 = min(qb, q0 + 8)
+        qstep = max(1, min(8, 20_000_000 // (len(keys) * vk.shape[1])))   # bounded host memory
+        for q0 in range(qa, qb, qstep):
+            q1 = min(qb, q0 + qstep)
             logits = scale * (q[q0:q1] @ k[keys].T)
             mx = logits.max(axis=1, keepdims=True)
             p = np.exp(logits - mx)
@@ -108,6 +111,8 @@ def _check_attention(got, got_lse, quant_ref, kept_row_lists, S, scale, rows):
             d = got[q0:q1] - o
             assert np.all(np.abs(d) <= bound), (i, float((np.abs(d) - bound).max()))
             var = ((e * e / 3.0)[:, :, None] * dev * dev).sum(axis=1) / (l * l)
+            if out_bf16:
+                var = var + (2.0 ** -8 * o) ** 2 / 3.0
             pred2 += float(var.sum())
             err2 += float((d * d).sum())
             cnt += d.size
@@ -158,10 +163,10 @@ def test_fp8_quantise_and_attend(name, B, H, D, grid, S, keep):
             ref = _dequantised(bits, S, b, h)
             rows = range(nb)
             rms, pred = _check_attention(o[b, h], _np(lse)[b, h], ref, kept[b][h], S, scale_of(wl), rows)
-            assert rms <= 2.0 * pred + 2e-3, (b, h, rms, pred)    # + bf16 output rounding
+            assert rms <= 2.0 * pred + 5e-4, (b, h, rms, pred)
             drms, dpred = _check_attention(do[b, h], _np(dlse)[b, h], ref, [list(range(nb))] * nb, S,
                                            scale_of(wl), rows)
-            assert drms <= 2.0 * dpred + 2e-3, (b, h, drms, dpred)
+            assert drms <= 2.0 * dpred + 5e-4, (b, h, drms, dpred)
             say(f"[fp8 {name}] b{b} h{h}: sparse rms {rms:.2e} (model {pred:.2e}), dense rms {drms:.2e} "
                 f"(model {dpred:.2e})")
 
@@ -199,7 +204,7 @@ def test_fp8_guard_rescales_with_rising_logits(S, D, step):
     span = np.abs(c * (ref["q_hat"][0, 0] @ ref["k_hat"][0, 0].T)).max() * np.log2(np.e)
     assert span > 2.0 * abs(step), span                       # the regime this test is about
     rms, pred = _check_attention(o[0, 0], _np(lse)[0, 0], ref, rows, S, c, range(nblk))
-    assert rms <= 2.0 * pred + 2e-3, (rms, pred)
+    assert rms <= 2.0 * pred + 5e-4, (rms, pred)
 
 
 def test_fp8_f32_output_and_empty_rows():
@@ -225,7 +230,7 @@ def test_fp8_f32_output_and_empty_rows():
     assert not o32[0, 1].any() and torch.all(torch.isinf(lse[0, 1]))   # no usable block: zeros, -inf
     ref = _dequantised(bits, 128, 0, 0)
     rms, pred = _check_attention(_np(o32[0, 0]).astype(np.float64), _np(lse)[0, 0], ref, [[0]] * nb, 128,
-                                 scale_of(wl), range(nb))
+                                 scale_of(wl), range(nb), out_bf16=False)
     assert rms <= 2.0 * pred + 1e-4
 
 
@@ -275,6 +280,6 @@ def test_fp8_full_size_sampled():
         rows = sorted(rng.choice(nb, 5, replace=False).tolist()) + [nb - 1]
         rms, pred = _check_attention(o[0, h], _np(lse)[0, h], ref, kept_h[h], S, scale_of(wl), rows)
         say(f"[fp8 {wl.name}] head {h}: rms {rms:.2e} (model {pred:.2e})")
-        assert rms <= 2.0 * pred + 2e-3
+        assert rms <= 2.0 * pred + 5e-4
     del dev, quant, out, lse
     torch.cuda.empty_cache()

@@ -1,0 +1,96 @@
+"""GPU parity at the size limits of the boundary: 2048 key blocks per row (the
+most the selection kernel holds in registers) in both selection modes, with
+attention on sampled query blocks in bf16 and fp8, and fp8 dense attention at
+2047 blocks (the longest kept-block list the fp8 kernel holds in LDS)."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2606_23743_amd as sva
+from paper_2606_23743_amd import inputs, workloads
+
+from . import parity
+from .gpu_cases import device_inputs, flat_rows, oracle_select, say, scale_of
+from .test_gpu_fp8 import _check_attention, _dequantised
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+SC = workloads.small_case
+LIMIT_CASES = [
+    SC("nb2048_topk", 1, 1, 64, (2, 256, 256), 64, "topk", keep_ratio=0.05, seed=211),
+    SC("nb2048_mass", 1, 1, 64, (2, 256, 256), 64, "mass", mass_threshold=0.9, max_keep_ratio=0.3,
+       force_first_frame=False, seed=212),
+]
+
+
+def _kept_arrays(kept, nb):
+    kmax = max(1, max(len(r) for b in kept for h in b for r in h))
+    idx, cnt = oracle.kept_to_arrays(kept, nb, kmax)
+    return (torch.from_numpy(np.ascontiguousarray(idx, dtype=np.int32)).cuda(),
+            torch.from_numpy(np.ascontiguousarray(cnt, dtype=np.int32)).cuda())
+
+
+@pytest.mark.parametrize("wl", LIMIT_CASES, ids=[c.name for c in LIMIT_CASES])
+def test_selection_and_attention_at_2048_blocks(wl):
+    say(f"[limits {wl.name}] N={wl.seq_len} nB={wl.seq_len // wl.block}")
+    bits = inputs.generate(wl)
+    dev = device_inputs(bits)
+    prob = sva.problem_for(wl)
+    sel = sva.select_for(wl)
+    nb = sva.num_blocks(prob)
+    assert nb == 2048
+    qp, kp = sva.pool_blocks(prob, dev["q"], dev["k"])
+    idx, cnt, _ = sva.select_blocks(prob, sel, qp, kp)
+    torch.cuda.synchronize()
+    f64 = {n: oracle.bf16_bits_to_f64(bits[n]) for n in ("q", "k", "v")}
+    oqp = oracle.pool_blocks(f64["q"], wl.block)
+    okp = oracle.pool_blocks(f64["k"], wl.block)
+    scores = oracle.block_scores(oqp, okp, scale_of(wl))
+    kept, info = oracle_select(wl, scores)
+    idx_np, cnt_np = idx.cpu().numpy(), cnt.cpu().numpy()
+    parity.check_idx_layout(idx_np, cnt_np, nb)
+    n, same, problems = parity.compare_masks(flat_rows(kept), parity.gpu_rows(idx_np, cnt_np), scores,
+                                             info["mode"], k=info["k"], tau=info["tau"], forced=info["forced"])
+    assert not problems, problems[:5]
+    say(f"[limits {wl.name}] selection rows={n} identical={same}")
+
+    # attention on sampled query blocks with the oracle's lists, bf16 and fp8
+    oidx, ocnt = _kept_arrays(kept, nb)
+    out, lse = sva.sparse_attention(prob, dev["q"], dev["k"], dev["v"], oidx, ocnt, want_lse=True)
+    quant = sva.quantize_fp8(prob, dev["q"], dev["k"], dev["v"])
+    out8, lse8 = sva.sparse_attention_fp8(prob, quant, oidx, ocnt, want_lse=True)
+    torch.cuda.synchronize()
+    rows = [0, 1, 777, 1500, nb - 1]
+    ref, rlse = oracle.block_sparse_attention(f64["q"], f64["k"], f64["v"], kept, wl.block, scale_of(wl),
+                                              rows=[(0, 0, i) for i in rows])
+    o = out.float().cpu().numpy()
+    for i in rows:
+        sl = slice(i * wl.block, (i + 1) * wl.block)
+        mx, mean = parity.attention_errors(o[0, 0, sl], ref[0, 0, sl], np.ones(ref[0, 0, sl].shape, dtype=bool))
+        assert mx <= parity.MAX_ABS and mean <= parity.MEAN_ABS, (i, mx, mean)
+        assert np.all(np.abs(lse.cpu().numpy()[0, 0, sl] - rlse[0, 0, sl]) <= parity.LSE_TOL), i
+    qref = _dequantised(bits, wl.block, 0, 0)
+    rms, pred = _check_attention(out8.float().cpu().numpy().astype(np.float64)[0, 0], lse8.cpu().numpy()[0, 0],
+                                 qref, kept[0][0], wl.block, scale_of(wl), rows)
+    assert rms <= 2.0 * pred + 5e-4, (rms, pred)
+    say(f"[limits {wl.name}] fp8 rms {rms:.2e} (model {pred:.2e})")
+
+
+def test_fp8_dense_at_2047_blocks():
+    wl = SC("nb2047_dense", 1, 1, 64, (23, 89, 64), 64, "topk", topk=1, seed=213)
+    bits = inputs.generate(wl)
+    dev = device_inputs(bits)
+    prob = sva.problem_for(wl)
+    assert sva.num_blocks(prob) == 2047
+    quant = sva.quantize_fp8(prob, dev["q"], dev["k"], dev["v"])
+    out8, lse8 = sva.dense_attention_fp8(prob, quant, want_lse=True)
+    torch.cuda.synchronize()
+    qref = _dequantised(bits, wl.block, 0, 0)
+    rows = [0, 1023, 2046]
+    every = [list(range(2047))] * 2047
+    rms, pred = _check_attention(out8.float().cpu().numpy().astype(np.float64)[0, 0], lse8.cpu().numpy()[0, 0],
+                                 qref, every, wl.block, scale_of(wl), rows)
+    assert rms <= 2.0 * pred + 5e-4, (rms, pred)
+    say(f"[limits dense fp8 nB=2047] rms {rms:.2e} (model {pred:.2e})")
