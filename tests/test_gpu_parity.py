@@ -221,6 +221,24 @@ def test_keep_all_equals_dense_and_determinism():
     assert torch.equal(o1, od) and torch.equal(l1, ld)      # same block order as dense
 
 
+def test_segment_order_covers_every_row():
+    """Sparse lists at S=128 hand rows to the XCDs in segments of 8 x 128; with
+    3 heads of 393 blocks (ragged last block) there are 1179 rows: one whole
+    segment and a 155-row tail.  Keep-all lists must reproduce dense attention
+    bit for bit on every row, written over a NaN-filled output."""
+    wl, bits, dev, prob = _small(seed=15, D=128, S=128, grid=(8, 40, 157), H=3)
+    nb = sva.num_blocks(prob)
+    assert nb == 393 and 3 * nb > 8 * 128
+    idx = torch.arange(nb, dtype=torch.int32, device="cuda").expand(1, 3, nb, nb).contiguous()
+    cnt = torch.full((1, 3, nb), nb, dtype=torch.int32, device="cuda")
+    out = torch.full_like(dev["q"], float("nan"))
+    lse = torch.full((1, 3, wl.seq_len), float("nan"), device="cuda")
+    sva.sparse_attention(prob, dev["q"], dev["k"], dev["v"], idx, cnt, out=out, want_lse=True, lse=lse)
+    od, ld = sva.dense_attention(prob, dev["q"], dev["k"], dev["v"], want_lse=True)
+    torch.cuda.synchronize()
+    assert torch.equal(out, od) and torch.equal(lse, ld)
+
+
 def test_custom_scale():
     wl, bits, dev, prob = _small(seed=14, D=64, S=64, grid=(2, 8, 9))
     c = 0.3
