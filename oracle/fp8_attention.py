@@ -13,8 +13,12 @@ formula; readings taken here (the design notes list them):
 * scales are powers of two 2^e, e in [-127, 127]: for a group of values with
   largest magnitude a, e is the smallest exponent with a <= 448 * 2^e (e = 0
   for an all-zero group), and a value x is stored as the code of x * 2^-e.
-* Q: one scale per (b, h, query block of S tokens), over the block's valid
-  tokens and all channels.
+* Q carries the softmax scale: it is multiplied by lambda = c * log2(e)
+  (rounded once to float32) before it is quantised, so the matrix product of
+  the codes is the logit in base-2 units and the probabilities are powers of
+  two of it.  The product of a bf16 value and lambda is rounded once to
+  float32, the quantiser's working precision.  Then one scale per (b, h,
+  query block of S tokens), over the block's valid tokens and all channels.
 * K, outlier smoothing: the per-(b, h) channel mean of K over all N tokens,
   rounded to bf16, is subtracted first (every logit of a query moves by the
   same amount, so the softmax is unchanged); the difference is taken in
@@ -22,11 +26,14 @@ formula; readings taken here (the design notes list them):
   one scale per (b, h, key block).
 * V: one scale per (b, h, channel) over all N tokens.
 * attention: the block-sparse attention of the dequantised Q, K, V (the plain
-  float64 definition of the sparse path).  The GPU additionally rounds the
+  float64 definition of the sparse path), with logits ln(2) * (q_hat . k_hat)
+  when Q carries lambda.  The GPU additionally rounds the
   unnormalised probabilities to e4m3 before the PV product; the tests bound
   that rounding's effect, the oracle keeps them exact.
 """
 from __future__ import annotations
+
+import math
 
 import numpy as np
 
@@ -36,6 +43,23 @@ from .qknorm_rope import round_bf16
 
 E4M3_MAX = 448.0
 E_MIN, E_MAX = -127, 127
+LOG2E = 1.4426950408889634          # log2(e), the float64 nearest to it
+LN2 = math.log(2.0)
+
+
+def softmax_scale_log2(head_dim: int, softmax_scale: float = 0.0) -> float:
+    """lambda = c * log2(e) rounded once to float32, where c is the softmax
+    scale: softmax_scale (a float32 value) when positive, else 1/sqrt(D),
+    both in float64."""
+    c = float(np.float32(softmax_scale)) if softmax_scale > 0 else 1.0 / math.sqrt(head_dim)
+    return float(np.float32(c * LOG2E))
+
+
+def fold_scale(q, lam: float) -> np.ndarray:
+    """float32(q * lam) as float64, for bf16 values q and a float32 lam: the
+    product of an 8-bit and a 24-bit significand is exact in float64, and it
+    is rounded once to float32 (nearest, ties to even)."""
+    return (np.asarray(q, dtype=np.float64) * float(lam)).astype(np.float32).astype(np.float64)
 
 
 def e4m3_value(code: int) -> float:
@@ -110,8 +134,10 @@ def k_smooth_mean(k: np.ndarray) -> np.ndarray:
     return round_bf16(np.mean(np.asarray(k, dtype=np.float64), axis=2))
 
 
-def quantize_qkv(q, k, v, block: int):
-    """Quantise Q, K, V [B, H, N, D] (float64 holding bf16 values).
+def quantize_qkv(q, k, v, block: int, lam=None):
+    """Quantise Q, K, V [B, H, N, D] (float64 holding bf16 values).  With lam
+    (softmax_scale_log2), Q is first folded to float32(Q * lam): q_hat is
+    then in base-2 logit units and the attention takes scale LN2.
 
     Returns a dict with
       q_exp [B, H, nB], k_exp [B, H, nB], v_exp [B, H, D]   (int)
@@ -122,6 +148,8 @@ def quantize_qkv(q, k, v, block: int):
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
     v = np.asarray(v, dtype=np.float64)
+    if lam is not None:
+        q = fold_scale(q, lam)
     B, H, N, D = q.shape
     bounds = block_bounds(N, block)
     nb = len(bounds)
@@ -155,6 +183,7 @@ def quantize_qkv(q, k, v, block: int):
 
 
 def fp8_block_sparse_attention(quant: dict, kept, block: int, scale: float, rows=None):
-    """Block-sparse attention of the dequantised tensors (float64)."""
+    """Block-sparse attention of the dequantised tensors (float64); scale is
+    LN2 when Q carries lambda."""
     return block_sparse_attention(quant["q_hat"], quant["k_hat"], quant["v_hat"], kept, block,
                                   scale, rows=rows)

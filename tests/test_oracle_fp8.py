@@ -4,6 +4,7 @@ brute-force scale exponents and grouping, error bounds, the softmax
 invariance that makes K smoothing harmless, and an exactly representable case
 where quantised attention equals plain attention."""
 import math
+import struct
 
 import numpy as np
 import pytest
@@ -168,3 +169,85 @@ def test_exactly_representable_inputs_lose_nothing():
     got, _ = f8.fp8_block_sparse_attention(quant, kept, S, 0.35)
     want, _ = oracle.block_sparse_attention(q, k, v, kept, S, 0.35)
     assert np.array_equal(got, want)
+
+
+def _f32(x):
+    """float32 rounding by the C library's double -> float conversion."""
+    return struct.unpack("<f", struct.pack("<f", float(x)))[0]
+
+
+def test_softmax_scale_log2_closed_forms():
+    """lambda = c * log2(e) in float32: 1/(sqrt(D) ln 2) for the default scale
+    and c/ln 2 for a given one, within half a float32 ulp."""
+    for D in (64, 112, 128):
+        lam = f8.softmax_scale_log2(D)
+        exact = 1.0 / (math.sqrt(D) * math.log(2.0))
+        assert lam == _f32(lam) and abs(lam - exact) <= 2.0 ** -24 * exact, D
+    lam = f8.softmax_scale_log2(128, 0.5)
+    assert lam == _f32(lam) and abs(lam - 0.5 / math.log(2.0)) <= 2.0 ** -24 * lam
+    assert f8.softmax_scale_log2(64) == _f32(0.125 / math.log(2.0))        # 1/8 is exact
+
+
+def test_fold_scale_rounds_once_to_float32():
+    """float32(q * lam) against the C library's conversion of the exact
+    product, including a product exactly half-way between two float32 values
+    (ties to even)."""
+    rng = np.random.default_rng(8)
+    q = _bf16(rng.standard_normal(500) * 4)
+    for lam in (f8.softmax_scale_log2(128), f8.softmax_scale_log2(112), _f32(0.7213475)):
+        got = f8.fold_scale(q, lam)
+        for x, g in zip(q, got):
+            assert g == _f32(float(x) * lam)
+    # (1 + 2^-7)(1 + 2^-17) = 1 + 2^-7 + 2^-17 + 2^-24: half a float32 ulp above
+    # a value with an even last bit
+    tie = f8.fold_scale(np.array([1.0 + 2.0 ** -7]), 1.0 + 2.0 ** -17)[0]
+    assert tie == 1.0 + 2.0 ** -7 + 2.0 ** -17
+    # (1 + 2^-7)(1 + 2^-17 + 2^-23) = 1 + 2^-7 + 2^-17 + 2^-23 + 2^-24 + 2^-30:
+    # more than half an ulp above 1 + 2^-7 + 2^-17 + 2^-23, so it rounds up
+    up = f8.fold_scale(np.array([1.0 + 2.0 ** -7]), 1.0 + 2.0 ** -17 + 2.0 ** -23)[0]
+    assert up == 1.0 + 2.0 ** -7 + 2.0 ** -17 + 2.0 ** -22
+
+
+def test_quantize_q_with_folded_scale_pure_python():
+    """Q's exponents and codes when it carries lambda, element by element in
+    pure Python: the float32 product first, then the block grouping."""
+    rng = np.random.default_rng(9)
+    B, H, N, D, S = 1, 2, 10, 4, 4
+    q = _bf16(rng.standard_normal((B, H, N, D)) * 3)
+    k = _bf16(rng.standard_normal((B, H, N, D)))
+    v = _bf16(rng.standard_normal((B, H, N, D)))
+    lam = f8.softmax_scale_log2(D)
+    out = f8.quantize_qkv(q, k, v, S, lam=lam)
+    table = _finite_table()
+    for h in range(H):
+        qs = [[_f32(float(q[0, h, n, d]) * lam) for d in range(D)] for n in range(N)]
+        for i, a in enumerate(range(0, N, S)):
+            z = min(N, a + S)
+            qa = max(abs(qs[n][d]) for n in range(a, z) for d in range(D))
+            eq = next(e for e in range(-127, 128) if qa <= 448 * 2.0 ** e)
+            assert out["q_exp"][0, h, i] == eq
+            for n in range(a, z):
+                for d in range(D):
+                    assert out["q_code"][0, h, n, d] == _nearest_even(qs[n][d] * 2.0 ** -eq, table)
+
+
+def test_folded_scale_attention_equals_plain_attention():
+    """With lambda = 2^-3 and Q on the e4m3 grid, Q * lambda stays on it: the
+    attention of the quantised inputs with logits ln2 * (q_hat . k_hat) equals
+    plain attention with scale ln2 / 8."""
+    rng = np.random.default_rng(10)
+    B, H, N, D, S = 1, 2, 32, 8, 8
+    grid = np.array([v for v in _finite_table().values() if abs(v) >= 2.0 ** -3])
+    q = rng.choice(grid, (B, H, N, D)) * 2.0 ** -1
+    half = rng.choice(grid, (B, H, N // 2, D)) * 2.0 ** -5
+    k = np.concatenate([half, -half], axis=2)
+    v = rng.choice(grid, (B, H, N, D)) * 2.0 ** -3
+    q[..., 0, 0] = 448.0 * 2.0 ** -1
+    k[..., 0, 0], k[..., N // 2, 0] = 448.0 * 2.0 ** -5, -448.0 * 2.0 ** -5
+    v[..., 0, :] = 448.0 * 2.0 ** -3
+    quant = f8.quantize_qkv(q, k, v, S, lam=0.125)
+    assert np.array_equal(quant["q_hat"], q * 0.125)
+    kept = [[[[0, 1, 3], [2], [1, 2, 3], [0]] for _ in range(H)]]
+    got, gl = f8.fp8_block_sparse_attention(quant, kept, S, f8.LN2)
+    want, wl = oracle.block_sparse_attention(q, k, v, kept, S, f8.LN2 / 8)
+    assert np.array_equal(got, want) and np.array_equal(gl, wl)

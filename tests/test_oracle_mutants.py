@@ -292,7 +292,20 @@ def _no_smoothing(k):
     return np.zeros(k.shape[:2] + k.shape[3:])
 
 
+def _fold_ignores_scale(q, lam):
+    return np.asarray(q, dtype=np.float64)
+
+
+def _fold_in_float64(q, lam):
+    return np.asarray(q, dtype=np.float64) * float(lam)
+
+
 FP8_MUTANTS = [
+    ("softmax scale not folded into Q", "fold_scale", _fold_ignores_scale,
+     [TF8.test_fold_scale_rounds_once_to_float32, TF8.test_quantize_q_with_folded_scale_pure_python,
+      TF8.test_folded_scale_attention_equals_plain_attention]),
+    ("folded Q not rounded to float32", "fold_scale", _fold_in_float64,
+     [TF8.test_fold_scale_rounds_once_to_float32]),
     ("e4m3 ties away from zero", "round_e4m3", _e4m3_half_away,
      [TF8.test_rounding_matches_brute_force_nearest_even]),
     ("e4m3 subnormal spacing 2^-10", "round_e4m3", _e4m3_subnormal_step_too_fine,
