@@ -268,16 +268,20 @@ int sva_fp8_padded_len(const sva_problem* prob, int32_t* np);
 int sva_fp8_code_dim(const sva_problem* prob, int32_t* dp);
 
 /* Quantise bf16 Q, K, V [B, H, N, D] into the code tensors and exponents of
- * `out` (all device memory the caller owns; k_mean is written too).  K is
- * smoothed first (K - k_mean, in float32).  Pointers 16-byte aligned
- * (exponent arrays 4). */
+ * `out` (all device memory the caller owns; k_mean is written too).  Q
+ * carries the softmax scale: it is multiplied by lambda = c * log2(e) (c =
+ * prob->softmax_scale, or 1/sqrt(D) when that is <= 0, in double; lambda
+ * rounded once to float32) and the float32 product is quantised, so the code
+ * product is the logit in base-2 units.  K is smoothed first (K - k_mean, in
+ * float32).  Pointers 16-byte aligned (exponent arrays 4). */
 int sva_quantize_fp8(const sva_problem* prob, const void* q, const void* k, const void* v,
                      const sva_fp8_tensors* out, void* stream);
 
 /* Block-sparse attention on quantised inputs, with the kept-block lists of
- * sva_select_blocks (kmax <= 2047, else SVA_ERR_UNSUPPORTED).  The
- * unnormalised probabilities are rounded to e4m3 before the PV product and l
- * sums those rounded weights.  out: bf16 or f32 [B, H, N, D] as
+ * sva_select_blocks (kmax <= 2047, else SVA_ERR_UNSUPPORTED).  The softmax
+ * scale is the one the Q codes carry (prob->softmax_scale is not read here).
+ * The unnormalised probabilities are rounded to e4m3 before the PV product and
+ * l sums those rounded weights.  out: bf16 or f32 [B, H, N, D] as
  * prob->out_dtype; lse (optional) f32 [B, H, N], natural log.  k_mean is not
  * read. */
 int sva_sparse_attention_fp8(const sva_problem* prob, const sva_fp8_tensors* in, const int32_t* kv_idx,

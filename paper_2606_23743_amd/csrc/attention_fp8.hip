@@ -11,14 +11,22 @@
 // PV matrix instruction each:
 //   S^T = K Q^T   mfma_scale_f32_32x32x64_f8f6f4, two 32-key tiles, the block
 //                 exponents of K and Q applied by the instruction's scales.
+//                 Q carries the softmax scale in base 2 (the quantiser folds
+//                 c*log2(e) into it), so s is the logit in base-2 units.
 //                 K rows are read in the order pi(r) = 16*((r>>2)&1) +
 //                 4*(r>>3) + (r&3), so register j of tile t of lane (n, h) is
 //                 key 32t + 16h + j: the lane's 32 probabilities are two runs
 //                 of 16 consecutive keys.
-//   p = exp2(c*log2e*s - m + 6)   with m the first chunk's row maximum,
-//                 moved up to a chunk's maximum (O and l rescaled) before any
-//                 chunk whose maximum exceeds it by more than 2.75 (log2
-//                 units).  So p <= 2^8.75 < 448 fits e4m3, and the offset puts
+//   p = exp2(s - m + 6)   with m the floor of the first chunk's row maximum,
+//                 moved up to the floor of a chunk's maximum (O and l scaled
+//                 by the power of two, exactly) before any chunk whose maximum
+//                 exceeds it by more than 2.75.  m is an integer, so the
+//                 offset rides on the conversion: exp2(s) is converted with
+//                 v_cvt_scalef32_pk_fp8_f32, which divides by the power of two
+//                 2^(m - 6) before rounding, and no per-element subtraction is
+//                 needed.  (A wave with a row whose |m| exceeds 100, where
+//                 exp2(s) could leave float32's range, subtracts instead.)
+//                 So p <= 2^8.75 < 448 fits e4m3, and the offset puts
 //                 the weights near the maximum high in e4m3's range: only
 //                 weights below 2^-16 of the maximum fall under its smallest
 //                 subnormal (with no offset every weight below 2^-10 would
@@ -47,10 +55,12 @@ using namespace attn;
 
 typedef __attribute__((ext_vector_type(8))) int i32x8;
 typedef __attribute__((ext_vector_type(4))) int i32x4;
+typedef __attribute__((ext_vector_type(2))) short s16x2;
 
 constexpr int kListSlots = kFp8MaxList + 1;  // LDS list entries; the last slot holds the count
-constexpr float kShift = 6.0f;           // log2 offset of the probabilities (see above)
+constexpr int kShift = 6;                // log2 offset of the probabilities (see above)
 constexpr float kGuard = 2.75f;          // allowed excess of a chunk maximum over m
+constexpr float kFastRange = 100.0f;     // |m| up to this: exp2(s) stays normal float32
 
 __device__ __forceinline__ int pi_row(int r) { return 16 * ((r >> 2) & 1) + 4 * (r >> 3) + (r & 3); }
 
@@ -92,7 +102,6 @@ void attn_fp8_kernel(Fp8AttnArgs a) {
   const int hf = lane >> 5;
   const int l32 = lane & 31;
   const int N = a.N, nB = a.nB, Np = a.Np;
-  const float sl2 = a.scale_log2;
 
   const int row = __builtin_amdgcn_readfirstlane(xcd_remap(blockIdx.x, a.n_rows));  // (b*H + h)*nB + i
   const int bh = row / nB;
@@ -195,7 +204,15 @@ void attn_fp8_kernel(Fp8AttnArgs a) {
   const int voff0 = l32 * CK + v_slot(l32, hf) * 16;        // channel l32 (+32*dt: same slot pattern)
   const int voff1 = l32 * CK + v_slot(l32, 2 + hf) * 16;
 
-  float m_ref = 0.0f;                        // reference max (log2 units)
+  float m_ref = 0.0f;                        // reference max (log2 units, an integer)
+  float cvt_scale = 1.0f;                    // 2^(m_ref - kShift): the conversion divides by it
+  bool fast = true;                          // every row of the wave has |m_ref| <= kFastRange
+  auto set_ref = [&](float m) {
+    m_ref = m;
+    // (clamped: a row beyond the fast range never uses its scale)
+    cvt_scale = __builtin_amdgcn_ldexpf(1.0f, (int)__builtin_fminf(__builtin_fmaxf(m, -120.0f), 120.0f) - kShift);
+    fast = __builtin_amdgcn_ballot_w64(!(__builtin_fabsf(m) <= kFastRange)) == 0;
+  };
   f32x16 oacc[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x16{};
@@ -244,37 +261,58 @@ void attn_fp8_kernel(Fp8AttnArgs a) {
     const u32x2 sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
     return max3(__uint_as_float(sw[0]), __uint_as_float(sw[1]), __uint_as_float(sw[1]));
   };
-  // before a chunk's probabilities: keep p = exp2(s*sl2 - m_ref + kShift) <= 2^(kShift + kGuard)
+  // before a chunk's probabilities: keep p = exp2(s - m_ref + kShift) <= 2^(kShift + kGuard)
   auto guard = [&](const f32x16 (&sc)[2]) {
-    const float over = row_max(sc) * sl2 - m_ref;
+    const float over = row_max(sc) - m_ref;
     if (__builtin_amdgcn_ballot_w64(over > kGuard) != 0) {
       asm volatile("");
-      const float mn = over > kGuard ? m_ref + over : m_ref;
-      const float f = __builtin_amdgcn_exp2f(m_ref - mn);
+      const float mn = over > kGuard ? __builtin_floorf(m_ref + over) : m_ref;
+      // exact power of two (below 2^-256 it is zero, as exp2 would give)
+      const float f = __builtin_amdgcn_ldexpf(1.0f, (int)__builtin_fmaxf(m_ref - mn, -256.0f));
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[dt][r] *= f;
 #pragma unroll
       for (int r = 0; r < 16; ++r) lacc[r] *= f;
-      m_ref = mn;
+      set_ref(mn);
     }
   };
+  // e4m3 weights of a chunk.  Fast form: exp2(s), divided by 2^(m_ref - kShift)
+  // inside the conversion.  Otherwise exp2(s - m_ref + kShift), converted.
+  // The first conversion's other half is overwritten by the second, so any
+  // register serves as its old value: one of its own inputs, so that no move
+  // is needed.
   auto softmax = [&](const f32x16 (&sc)[2], i32x8& pop) {
+    if (fast) {
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+      for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[t][4 * e + 0], sl2, kShift - m_ref));
-        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[t][4 * e + 1], sl2, kShift - m_ref));
-        const float p2 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[t][4 * e + 2], sl2, kShift - m_ref));
-        const float p3 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[t][4 * e + 3], sl2, kShift - m_ref));
-        // the first conversion's other half is overwritten by the second, so
-        // any register serves as its old value (no zeroing move)
-        int wv = __builtin_amdgcn_cvt_pk_fp8_f32(p0, p1, (int)__float_as_uint(p2), false);
-        wv = __builtin_amdgcn_cvt_pk_fp8_f32(p2, p3, wv, true);
-        pop[4 * t + e] = wv;
-      }
+        for (int e = 0; e < 4; ++e) {
+          const float p0 = __builtin_amdgcn_exp2f(sc[t][4 * e + 0]);
+          const float p1 = __builtin_amdgcn_exp2f(sc[t][4 * e + 1]);
+          const float p2 = __builtin_amdgcn_exp2f(sc[t][4 * e + 2]);
+          const float p3 = __builtin_amdgcn_exp2f(sc[t][4 * e + 3]);
+          s16x2 wv = __builtin_bit_cast(s16x2, __float_as_uint(p0));
+          wv = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(wv, p0, p1, cvt_scale, false);
+          wv = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(wv, p2, p3, cvt_scale, true);
+          pop[4 * t + e] = __builtin_bit_cast(int, wv);
+        }
+    } else {
+      const float off = (float)kShift - m_ref;
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float p0 = __builtin_amdgcn_exp2f(sc[t][4 * e + 0] + off);
+          const float p1 = __builtin_amdgcn_exp2f(sc[t][4 * e + 1] + off);
+          const float p2 = __builtin_amdgcn_exp2f(sc[t][4 * e + 2] + off);
+          const float p3 = __builtin_amdgcn_exp2f(sc[t][4 * e + 3] + off);
+          int wv = __builtin_amdgcn_cvt_pk_fp8_f32(p0, p1, (int)__float_as_uint(p2), false);
+          wv = __builtin_amdgcn_cvt_pk_fp8_f32(p2, p3, wv, true);
+          pop[4 * t + e] = wv;
+        }
+    }
   };
   auto pv = [&](const i32x8& pop, int st) {
     const unsigned char* vt = &Vs[0][0] + st * TB;
@@ -316,7 +354,7 @@ void attn_fp8_kernel(Fp8AttnArgs a) {
       qk(sa, 0, e0 & 255);
       const int valid = __builtin_amdgcn_readfirstlane(N - (e0 >> 8) * S);
       if (valid < CK) mask_tail(sa, valid);
-      m_ref = row_max(sa) * sl2;             // chunk 0 of a block holds a valid key
+      set_ref(__builtin_floorf(row_max(sa)));   // chunk 0 of a block holds a valid key
     }
     // Four stages: after the barrier of step g, chunk g-1's stage is free (its
     // K was read at step g-2, its V at g-1) and receives chunk g+3; the wait is
@@ -384,7 +422,7 @@ void attn_fp8_kernel(Fp8AttnArgs a) {
         }
       }
     if (a.lse && hf == 0)
-      a.lse[(size_t)bh * N + qr] = has ? (m_ref - kShift + __log2f(l_tot)) * 0.69314718055994530942f : -INFINITY;
+      a.lse[(size_t)bh * N + qr] = has ? (m_ref - (float)kShift + __log2f(l_tot)) * 0.69314718055994530942f : -INFINITY;
   }
 }
 

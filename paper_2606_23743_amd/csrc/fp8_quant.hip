@@ -8,10 +8,11 @@
 //   stats  the float64 channel sums of K over all N tokens (mean rounded once
 //          to bf16: the smoothing vector) and the channel maxima of |V| (V's
 //          per-channel exponents): segment partials, then a fixed-order sum.
-//   Q, K   one workgroup per (tensor, b, h, block): K first subtracts the
-//          smoothing vector in float32; the block's largest magnitude sets
-//          its exponent; codes are written [B, H, Np, DP] (Np = nB * S, rows
-//          past N zero).
+//   Q, K   one workgroup per (tensor, b, h, block): Q is first multiplied by
+//          the softmax scale in base 2 (float32), so the code product is the
+//          logit in base-2 units; K subtracts the smoothing vector in float32;
+//          the block's largest magnitude sets its exponent; codes are written
+//          [B, H, Np, DP] (Np = nB * S, rows past N zero).
 //   V      one workgroup per (b, h, block): codes with the channel exponents,
 //          transposed through LDS into 64-key tiles [B, H, Np/64, DP, 64], the
 //          layout the attention kernel stages directly.
@@ -150,6 +151,7 @@ __global__ __launch_bounds__(kThreads) void fp8_quant_qk_kernel(Fp8QuantArgs a) 
   const int r0 = threadIdx.x / TPR, c = threadIdx.x % TPR;
   const bool live = c < D / 8;                // padding lanes write zero codes
   float sub[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  const float mul = is_k ? 1.0f : a.q_mul;
   if (is_k && live) {
     const uint4 mw = *reinterpret_cast<const uint4*>(a.k_mean + (size_t)bh * D + c * 8);
     const float mv[8] = {lo16(mw.x), hi16(mw.x), lo16(mw.y), hi16(mw.y), lo16(mw.z), hi16(mw.z), lo16(mw.w), hi16(mw.w)};
@@ -166,7 +168,8 @@ __global__ __launch_bounds__(kThreads) void fp8_quant_qk_kernel(Fp8QuantArgs a) 
     const float v[8] = {lo16(w.x), hi16(w.x), lo16(w.y), hi16(w.y), lo16(w.z), hi16(w.z), lo16(w.w), hi16(w.w)};
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      x[p][e] = (live && r < valid) ? v[e] - sub[e] : 0.0f;   // float32 difference (K), exact copy (Q)
+      // K: float32 difference (sub is zero for Q); Q: float32 product (mul is 1 for K)
+      x[p][e] = (live && r < valid) ? __builtin_fmaf(v[e], mul, -sub[e]) : 0.0f;
       amax = fmaxf(amax, fabsf(x[p][e]));
     }
   }

@@ -138,7 +138,6 @@ sva::Fp8AttnArgs fp8_attn_args(const Dims& d, const sva_fp8_tensors* t, const in
   a.kmax = kmax;
   a.out = out;
   a.lse = lse;
-  a.scale_log2 = (float)(d.scale * 1.4426950408889634);
   return a;
 }
 }  // namespace
@@ -387,6 +386,7 @@ int sva_quantize_fp8(const sva_problem* prob, const void* q, const void* k, cons
   a.k_exp = out->k_exp;
   a.v_exp = out->v_exp;
   a.k_mean = static_cast<uint16_t*>(out->k_mean);
+  a.q_mul = (float)(d.scale * 1.4426950408889634);   // the softmax scale in base 2, carried by Q
   return hip_status(sva::launch_quantize_fp8(d, a, static_cast<hipStream_t>(stream)));
 }
 

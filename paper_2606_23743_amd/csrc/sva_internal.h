@@ -48,6 +48,7 @@ struct Fp8QuantArgs {
   int32_t* v_exp;
   uint16_t* k_mean;   // bf16 [B, H, D]
   int N, nB, Np, n_rows;
+  float q_mul;        // c * log2(e) in float32: Q is multiplied by it before quantising
 };
 hipError_t launch_quantize_fp8(const Dims& d, const Fp8QuantArgs& a, hipStream_t stream);
 
@@ -63,7 +64,6 @@ struct Fp8AttnArgs {
   void* out;
   float* lse;
   int N, nB, Np, kmax, n_rows;
-  float scale_log2;   // c * log2(e)
 };
 // Largest kept-block list (and nB for the dense form) the fp8 kernel holds.
 constexpr int kFp8MaxList = 2047;

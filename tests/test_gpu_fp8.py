@@ -1,8 +1,10 @@
 """GPU parity of fp8 (e4m3) quantisation and attention against the oracle.
 
 Quantisation decides integers (codes, exponents) from exact comparisons and
-one float32 subtraction, the same on both sides: codes, exponents and the
-bf16 smoothing vector must be bit-equal.
+one float32 product (Q times the softmax scale in base 2) or subtraction (K
+minus its smoothing vector), the same on both sides: codes, exponents and the
+bf16 smoothing vector must be bit-equal.  Q's codes carry the softmax scale,
+so the oracle's logits are ln(2) times the dequantised products.
 
 Attention: the oracle computes softmax attention of the dequantised Q, K, V
 in float64.  The GPU also rounds each unnormalised probability p to e4m3
@@ -54,7 +56,7 @@ def _check_quant(wl, bits, quant, heads=None):
     for b, h in heads:
         sl = slice(b, b + 1), slice(h, h + 1)
         x = {n: oracle.bf16_bits_to_f64(bits[n][sl]) for n in ("q", "k", "v")}
-        ref = of8.quantize_qkv(x["q"], x["k"], x["v"], S)
+        ref = of8.quantize_qkv(x["q"], x["k"], x["v"], S, lam=of8.softmax_scale_log2(D))
         assert np.array_equal(qe[b, h], ref["q_exp"][0, 0]), (b, h)
         assert np.array_equal(ke[b, h], ref["k_exp"][0, 0]), (b, h)
         assert np.array_equal(ve[b, h, :D], ref["v_exp"][0, 0]) and not ve[b, h, D:].any(), (b, h)
@@ -72,11 +74,13 @@ def _check_quant(wl, bits, quant, heads=None):
 
 def _dequantised(bits, S, b, h):
     x = {n: oracle.bf16_bits_to_f64(bits[n][b:b + 1, h:h + 1]) for n in ("q", "k", "v")}
-    return of8.quantize_qkv(x["q"], x["k"], x["v"], S)
+    return of8.quantize_qkv(x["q"], x["k"], x["v"], S, lam=of8.softmax_scale_log2(x["q"].shape[-1]))
 
 
 def _check_attention(got, got_lse, quant_ref, kept_row_lists, S, scale, rows, out_bf16=True):
-    """got: [N, D] float64 GPU output of one head; rows: query block ids to check.
+    """got: [N, D] float64 GPU output of one head; rows: query block ids to check;
+    scale: the logit scale of the dequantised products (LN2: Q carries the
+    softmax scale in base 2).
     Per weight p (oracle units, row maximum 1) the GPU's rounding errs by at
     most e = max(2^-4 p, min(p, 2^-16)): 3 mantissa bits, and e4m3 spacing
     2^-9 below 2^-6, where the GPU holds p times 2^(6 + k), 0 <= k <= 2.75
@@ -162,10 +166,10 @@ def test_fp8_quantise_and_attend(name, B, H, D, grid, S, keep):
         for h in range(H):
             ref = _dequantised(bits, S, b, h)
             rows = range(nb)
-            rms, pred = _check_attention(o[b, h], _np(lse)[b, h], ref, kept[b][h], S, scale_of(wl), rows)
+            rms, pred = _check_attention(o[b, h], _np(lse)[b, h], ref, kept[b][h], S, of8.LN2, rows)
             assert rms <= 2.0 * pred + 5e-4, (b, h, rms, pred)
             drms, dpred = _check_attention(do[b, h], _np(dlse)[b, h], ref, [list(range(nb))] * nb, S,
-                                           scale_of(wl), rows)
+                                           of8.LN2, rows)
             assert drms <= 2.0 * dpred + 5e-4, (b, h, drms, dpred)
             say(f"[fp8 {name}] b{b} h{h}: sparse rms {rms:.2e} (model {pred:.2e}), dense rms {drms:.2e} "
                 f"(model {dpred:.2e})")
@@ -201,9 +205,44 @@ def test_fp8_guard_rescales_with_rising_logits(S, D, step):
     o = _np(out.float()).astype(np.float64)
     assert np.isfinite(o).all()
     ref = _dequantised(new_bits, S, 0, 0)
-    span = np.abs(c * (ref["q_hat"][0, 0] @ ref["k_hat"][0, 0].T)).max() * np.log2(np.e)
-    assert span > 2.0 * abs(step), span                       # the regime this test is about
-    rms, pred = _check_attention(o[0, 0], _np(lse)[0, 0], ref, rows, S, c, range(nblk))
+    span = np.abs(ref["q_hat"][0, 0] @ ref["k_hat"][0, 0].T).max()      # base-2 logits
+    assert span >= 1.9 * abs(step), span                      # the regime this test is about
+    rms, pred = _check_attention(o[0, 0], _np(lse)[0, 0], ref, rows, S, of8.LN2, range(nblk))
+    assert rms <= 2.0 * pred + 5e-4, (rms, pred)
+
+
+@pytest.mark.parametrize("S,D,sign", [(128, 128, 1.0), (128, 128, -1.0), (64, 64, 1.0), (64, 112, -1.0)])
+def test_fp8_far_logits_take_the_explicit_path(S, D, sign):
+    """Base-2 logits near +-160, where exp2(s) alone would leave float32's
+    range: block 0 at sign*160, four blocks at -sign*40 (K's mean stays zero,
+    so smoothing keeps them).  With sign +1 every row's reference is near 160
+    and the wave subtracts it before exp2; with sign -1 it starts near -160
+    (the same explicit form), then the next block moves it to about 40 (O and
+    l scaled by about 2^-200) and the scaled conversion takes over."""
+    nblk = 5
+    wl = workloads.small_case(f"far_{S}_{D}", 1, 1, D, (1, nblk * S // 16, 16), S, "topk", topk=nblk, seed=43)
+    bits = inputs.generate(wl)
+    f = {n: inputs.bf16_bits_to_f32(bits[n]).copy() for n in ("q", "k", "v")}
+    c = scale_of(wl)
+    f["q"][0, 0] = 1.0
+    for b in range(nblk):
+        val = sign * (160.0 if b == 0 else -40.0) / (np.log2(np.e) * c * D)
+        f["k"][0, 0, b * S:(b + 1) * S] = val + 0.05 * f["k"][0, 0, b * S:(b + 1) * S]
+    new_bits = {n: inputs._round_bf16(f[n]) for n in f}
+    dev = device_inputs(new_bits)
+    prob = sva.problem_for(wl)
+    quant = sva.quantize_fp8(prob, dev["q"], dev["k"], dev["v"])
+    rows = [list(range(nblk)) for _ in range(nblk)]
+    idx = torch.from_numpy(np.array(rows, dtype=np.int32).reshape(1, 1, nblk, nblk)).cuda()
+    cnt = torch.from_numpy(np.full((1, 1, nblk), nblk, dtype=np.int32)).cuda()
+    out, lse = sva.sparse_attention_fp8(prob, quant, idx, cnt, want_lse=True)
+    torch.cuda.synchronize()
+    o = _np(out.float()).astype(np.float64)
+    assert np.isfinite(o).all() and np.isfinite(_np(lse)).all()
+    ref = _dequantised(new_bits, S, 0, 0)
+    logits = ref["q_hat"][0, 0] @ ref["k_hat"][0, 0].T                 # base-2 logits
+    assert np.abs(logits[:, :S]).min() > 120.0, np.abs(logits[:, :S]).min()   # the regime
+    rms, pred = _check_attention(o[0, 0], _np(lse)[0, 0], ref, rows, S, of8.LN2, range(nblk))
     assert rms <= 2.0 * pred + 5e-4, (rms, pred)
 
 
@@ -230,7 +269,7 @@ def test_fp8_f32_output_and_empty_rows():
     assert not o32[0, 1].any() and torch.all(torch.isinf(lse[0, 1]))   # no usable block: zeros, -inf
     ref = _dequantised(bits, 128, 0, 0)
     rms, pred = _check_attention(_np(o32[0, 0]).astype(np.float64), _np(lse)[0, 0], ref, [[0]] * nb, 128,
-                                 scale_of(wl), range(nb), out_bf16=False)
+                                 of8.LN2, range(nb), out_bf16=False)
     assert rms <= 2.0 * pred + 1e-4
 
 
@@ -269,8 +308,9 @@ def test_fp8_full_size_sampled():
     say(f"[fp8 {wl.name}] checking")
     for h in (0, H - 1):
         _check_quant(wl, bits, quant, heads=[(0, h)])
+    lam = of8.softmax_scale_log2(wl.head_dim)
     for h in range(H):
-        x = oracle.bf16_bits_to_f64(bits["q"][0, h])
+        x = of8.fold_scale(oracle.bf16_bits_to_f64(bits["q"][0, h]), lam)
         amax = [np.abs(x[i * S:min(N, (i + 1) * S)]).max() for i in range(nb)]
         assert np.array_equal(_np(quant["q_exp"])[0, h], [of8.scale_exponent(a) for a in amax]), h
     rng = np.random.default_rng(7)
@@ -278,7 +318,7 @@ def test_fp8_full_size_sampled():
     for h in heads:
         ref = _dequantised(bits, S, 0, h)
         rows = sorted(rng.choice(nb, 5, replace=False).tolist()) + [nb - 1]
-        rms, pred = _check_attention(o[0, h], _np(lse)[0, h], ref, kept_h[h], S, scale_of(wl), rows)
+        rms, pred = _check_attention(o[0, h], _np(lse)[0, h], ref, kept_h[h], S, of8.LN2, rows)
         say(f"[fp8 {wl.name}] head {h}: rms {rms:.2e} (model {pred:.2e})")
         assert rms <= 2.0 * pred + 5e-4
     del dev, quant, out, lse

@@ -6,6 +6,7 @@ import numpy as np
 import pytest
 
 import oracle
+import oracle.fp8_attention as of8
 import paper_2606_23743_amd as sva
 from paper_2606_23743_amd import inputs, workloads
 
@@ -73,7 +74,7 @@ def test_selection_and_attention_at_2048_blocks(wl):
         assert np.all(np.abs(lse.cpu().numpy()[0, 0, sl] - rlse[0, 0, sl]) <= parity.LSE_TOL), i
     qref = _dequantised(bits, wl.block, 0, 0)
     rms, pred = _check_attention(out8.float().cpu().numpy().astype(np.float64)[0, 0], lse8.cpu().numpy()[0, 0],
-                                 qref, kept[0][0], wl.block, scale_of(wl), rows)
+                                 qref, kept[0][0], wl.block, of8.LN2, rows)
     assert rms <= 2.0 * pred + 5e-4, (rms, pred)
     say(f"[limits {wl.name}] fp8 rms {rms:.2e} (model {pred:.2e})")
 
@@ -91,6 +92,6 @@ def test_fp8_dense_at_2047_blocks():
     rows = [0, 1023, 2046]
     every = [list(range(2047))] * 2047
     rms, pred = _check_attention(out8.float().cpu().numpy().astype(np.float64)[0, 0], lse8.cpu().numpy()[0, 0],
-                                 qref, every, wl.block, scale_of(wl), rows)
+                                 qref, every, wl.block, of8.LN2, rows)
     assert rms <= 2.0 * pred + 5e-4, (rms, pred)
     say(f"[limits dense fp8 nB=2047] rms {rms:.2e} (model {pred:.2e})")
