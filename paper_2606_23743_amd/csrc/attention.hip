@@ -332,6 +332,14 @@ hipError_t launch_attention_rescaling(const Dims& d, bool sparse, const AttnArgs
 hipError_t launch_attention(const Dims& d, bool sparse, const uint16_t* q, const uint16_t* k,
                             const uint16_t* v, const int32_t* kv_idx, const int32_t* kv_count,
                             int kmax, void* out, float* lse, hipStream_t stream) {
+  // Dense attention does not depend on the block size: at S = 64 it runs as
+  // 128-token query tiles (four waves share every staged key chunk instead of
+  // two; the same keys, in the same 32-key chunks and order).
+  Dims dd = d;
+  if (!sparse && d.S == 64) {
+    dd.S = 128;
+    dd.nB = (d.N + 127) / 128;
+  }
   AttnArgs a;
   a.q = q;
   a.k = k;
@@ -340,15 +348,15 @@ hipError_t launch_attention(const Dims& d, bool sparse, const uint16_t* q, const
   a.kv_count = kv_count;
   a.out = out;
   a.lse = lse;
-  a.N = d.N;
-  a.nB = d.nB;
+  a.N = dd.N;
+  a.nB = dd.nB;
   a.kmax = kmax;
-  a.n_rows = d.B * d.H * d.nB;
-  a.scale_log2 = (float)(d.scale * 1.4426950408889634);
+  a.n_rows = dd.B * dd.H * dd.nB;
+  a.scale_log2 = (float)(dd.scale * 1.4426950408889634);
   // fixed-reference-max kernel, then the rescaling kernel for any block it marked
-  hipError_t e = launch_attention_q32(d, sparse, a, stream);
+  hipError_t e = launch_attention_q32(dd, sparse, a, stream);
   if (e != hipSuccess) return e;
-  return launch_attention_rescaling(d, sparse, a, stream);
+  return launch_attention_rescaling(dd, sparse, a, stream);
 }
 
 }  // namespace sva

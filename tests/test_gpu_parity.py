@@ -205,8 +205,12 @@ def test_constant_values_and_fp32_output():
     assert mx <= 1e-2 and mean <= 1e-3, (mx, mean)
 
 
-def test_keep_all_equals_dense_and_determinism():
-    wl, bits, dev, prob = _small(seed=13, D=128, S=128, grid=(3, 10, 13))
+@pytest.mark.parametrize("S", [128, 64])
+def test_keep_all_equals_dense_and_determinism(S):
+    """Keep-all lists against dense attention, bit for bit (at S = 64 dense
+    attention runs as 128-token query tiles: the same keys in the same chunks
+    and order), and repeat runs bit for bit."""
+    wl, bits, dev, prob = _small(seed=13, D=128, S=S, grid=(3, 10, 13))
     nb = sva.num_blocks(prob)
     qp, kp = sva.pool_blocks(prob, dev["q"], dev["k"])
     idx, cnt, _ = sva.select_blocks(prob, sva.select_topk(1.0), qp, kp)
