@@ -1,0 +1,426 @@
+// Block-sparse attention for 64-token blocks, two neighbouring query blocks
+// per workgroup (Section 4.2.2: kept blocks computed exactly).
+//
+// Neighbouring query blocks of a video keep almost the same key blocks (for
+// the block-64 layers the union of two neighbours' lists is 55-70% of their
+// combined length).  A workgroup takes query blocks 2p and 2p+1 with four
+// waves of 32 queries (waves 0, 1: block 2p; waves 2, 3: block 2p+1) and walks
+// the union of the two kept lists: every key chunk is staged in LDS once for
+// both blocks, and each wave computes only on the key blocks its own query
+// block keeps.  The stage pipeline is the one of the 128-token kernel: 32-key
+// chunks, four LDS stages, loads three chunks ahead, so one loop iteration
+// covers two union entries (four chunks) and every stage index is a constant.
+//
+// The union is built in LDS from two bitmaps over the key blocks, which needs
+// lists that are strictly increasing and in range, as the selection kernel
+// writes them.  A pair with any other list (out-of-range entries, repeats,
+// another order) is marked (NaN first output element of both blocks) and the
+// per-iteration rescaling kernel that runs next recomputes it with the general
+// list semantics.  Per chunk, the arithmetic of a wave is that of the
+// 32-query kernel (Sᵀ = K·Qᵀ, fixed reference maximum from the wave's first
+// chunk, P rounded to bf16 with l summed from it, Oᵀ += Vᵀ·Pᵀ).
+#include <type_traits>
+
+#include "attn_common.h"
+
+namespace sva {
+namespace {
+
+using namespace attn;
+
+constexpr int kPairMaxBlocks = 4096;         // key blocks a pair's bitmaps and union hold
+
+template <int D, bool OUT_F32>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void attn_pair_kernel(AttnArgs a, int n_pairs) {
+  using G = Geo<D>;
+  constexpr int S = 64;                      // tokens per (query and key) block
+  constexpr int NW = 4;                      // waves per workgroup
+  constexpr int CK = 32;                     // keys per staged chunk
+  constexpr int NST = 4;                     // LDS stages (two union entries)
+  constexpr int PD = NST - 1;                // prefetch distance, in chunks
+  constexpr int CT = CK * G::RB;             // bytes of one chunk tile (K or V)
+  constexpr int NUW = CT / 1024 / NW;        // direct-load pieces per wave per tile
+  constexpr int kWords = kPairMaxBlocks / 32;
+  static_assert(NUW >= 1, "tile split");
+
+  __shared__ __attribute__((aligned(1024))) unsigned char Ks[NST][CT];
+  __shared__ __attribute__((aligned(1024))) unsigned char Vs[NST][CT];
+  __shared__ uint16_t ulist[kPairMaxBlocks];  // (block << 2) | (kept by 2p) | (kept by 2p+1) << 1
+  __shared__ uint32_t bm[2][kWords];
+  __shared__ int n_union, list_bad, wg_bad;
+
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int hf = lane >> 5;
+  const int l32 = lane & 31;
+  const int g16 = lane >> 4;
+  const int n16 = lane & 15;
+  const int N = a.N, nB = a.nB;
+  const float sl2 = a.scale_log2;
+
+  const int npb = (nB + 1) / 2;              // pairs per (b, h)
+  const int pr = __builtin_amdgcn_readfirstlane(xcd_remap(blockIdx.x, n_pairs));
+  const int bh = pr / npb;
+  const int p = pr - bh * npb;
+  const int qsel = w >> 1;                   // 0: block 2p, 1: block 2p+1
+  const int qb = 2 * p + qsel;               // this wave's query block (may be nB: none)
+  const bool has_b = 2 * p + 1 < nB;
+  const int row0 = bh * nB + 2 * p;          // row of block 2p; 2p+1 is row0 + 1
+  const size_t head = (size_t)bh * N * D;
+  const uint16_t* Qh = a.q + head;
+  const uint16_t* Kh = a.k + head;
+  const uint16_t* Vh = a.v + head;
+
+  // ---- the union of the two kept lists ----
+  const int words = (nB + 31) >> 5;
+  for (int t = threadIdx.x; t < 2 * kWords; t += 256) (&bm[0][0])[t] = 0u;
+  if (threadIdx.x == 0) {
+    list_bad = 0;
+    wg_bad = 0;
+  }
+  __syncthreads();
+  int cnt2[2];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    cnt2[s] = 0;
+    if (s == 0 || has_b) cnt2[s] = min(max(a.kv_count[row0 + s], 0), a.kmax);
+  }
+  bool bad = false;
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int32_t* idx = a.kv_idx + (size_t)(row0 + s) * a.kmax;
+    for (int t = threadIdx.x; t < cnt2[s]; t += 256) {
+      const int j = idx[t];
+      const bool ok = j >= 0 && j < nB && (t + 1 == cnt2[s] || j < idx[t + 1]);
+      if (ok) atomicOr(&bm[s][j >> 5], 1u << (j & 31));
+      else bad = true;
+    }
+  }
+  if (__builtin_amdgcn_ballot_w64(bad) != 0 && lane == 0) atomicOr(&list_bad, 1);
+  __syncthreads();
+  if (list_bad) {                            // general lists: recomputed by the rescaling kernel
+    if (threadIdx.x < 2 && (threadIdx.x == 0 || has_b)) {
+      const size_t first = head + (size_t)(2 * p + threadIdx.x) * S * D;
+      if constexpr (OUT_F32) static_cast<float*>(a.out)[first] = __builtin_nanf("");
+      else static_cast<uint16_t*>(a.out)[first] = 0x7FC0;
+    }
+    return;
+  }
+  if (w == 0) {                              // compaction in block order, 64 words per step
+    int base = 0;
+    for (int w0 = 0; w0 < words; w0 += 64) {
+      const int wd = w0 + lane;
+      const uint32_t ba = wd < words ? bm[0][wd] : 0u;
+      const uint32_t bb = wd < words ? bm[1][wd] : 0u;
+      uint32_t u = ba | bb;
+      const int c = __builtin_popcount(u);
+      int incl = c;                          // inclusive prefix over the lanes
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const int y = __shfl_up(incl, off, 64);
+        if (lane >= off) incl += y;
+      }
+      int pos = base + incl - c;
+      while (u != 0) {
+        const int k = __builtin_ctz(u);
+        u &= u - 1;
+        const int j = wd * 32 + k;
+        ulist[pos++] = (uint16_t)((j << 2) | ((ba >> k) & 1u) | (((bb >> k) & 1u) << 1));
+      }
+      base += __shfl(incl, 63, 64);
+    }
+    if (lane == 0) n_union = base;
+  }
+  __syncthreads();
+  const int U = n_union;
+  auto ent = [&](int e) -> int {             // union entry e (block 0, kept by neither, past the end)
+    return __builtin_amdgcn_readfirstlane(e < U ? (int)ulist[e] : 0);
+  };
+  auto active = [&](int u) -> bool { return ((u >> qsel) & 1) != 0; };
+  auto key0_of = [&](int u, int c2) -> int { return (u >> 2) * S + c2 * CK; };
+
+  // ---- Q^T operand: query qb*S + (w&1)*32 + l32, d = s*16 + hf*8 + 0..7 ----
+  const int qr = qb * S + (w & 1) * 32 + l32;
+  bf16x8 qop[G::DQ];
+#pragma unroll
+  for (int s = 0; s < G::DQ; ++s) {
+    if (qb < nB && qr < N) qop[s] = *reinterpret_cast<const bf16x8*>(Qh + (size_t)qr * D + s * 16 + hf * 8);
+    else qop[s] = bf16x8{};
+  }
+
+  // ---- direct global -> LDS fetch of one chunk (this wave's 1 KB pieces),
+  // as in the 32-query kernel: a partial last chunk clamps its rows, a chunk
+  // wholly past the end reads chunk 0 ----
+  const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc((void*)Kh, (short)0, N * D * 2, 0x00020000);
+  const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc((void*)Vh, (short)0, N * D * 2, 0x00020000);
+  int kgv[NUW], vgv[NUW];
+#pragma unroll
+  for (int v = 0; v < NUW; ++v) {
+    const int r = (w * NUW + v) * G::RPI + lane / G::NCH;
+    const int pc = lane % G::NCH;
+    int ck = swz_k<G::NCH>(r, pc), cv = swz_v<G::NCH>(r, pc);
+    if (ck >= G::DCH) ck = 0;
+    if (cv >= G::DCH) cv = 0;
+    kgv[v] = (r * D + ck * 8) * 2;
+    vgv[v] = (r * D + cv * 8) * 2;
+  }
+  typedef __attribute__((address_space(3))) unsigned char lds_u8;
+  const unsigned ks_base = __builtin_amdgcn_readfirstlane((unsigned)(size_t)(lds_u8*)&Ks[0][0]);
+  const unsigned vs_base = __builtin_amdgcn_readfirstlane((unsigned)(size_t)(lds_u8*)&Vs[0][0]);
+  auto bll = [&](const __amdgpu_buffer_rsrc_t& rs, unsigned lds_addr, int voff, int soff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_u8*)(size_t)__builtin_amdgcn_readfirstlane(lds_addr), 16,
+                                             voff, __builtin_amdgcn_readfirstlane(soff), 0, 0);
+  };
+  auto fetch_one = [&](auto tk, int st, int key0) {
+    constexpr bool TK = decltype(tk)::value;
+    const __amdgpu_buffer_rsrc_t& rs = TK ? krs : vrs;
+    const unsigned base = (TK ? ks_base : vs_base) + st * CT;
+    key0 = __builtin_amdgcn_readfirstlane(key0);
+    if (key0 + CK <= N) {
+#pragma unroll
+      for (int v = 0; v < NUW; ++v)
+        bll(rs, base + (w * NUW + v) * 1024, TK ? kgv[v] : vgv[v], key0 * D * 2);
+    } else {
+      if (key0 >= N) key0 = 0;
+      const int valid = N - key0;
+      int ln = lane;
+      asm volatile("" : "+v"(ln));
+      const int pc = ln % G::NCH;
+#pragma unroll
+      for (int v = 0; v < NUW; ++v) {
+        const int uu = w * NUW + v;
+        const int r = uu * G::RPI + ln / G::NCH;
+        const int rs_ = r < valid ? r : 0;
+        int c = TK ? swz_k<G::NCH>(r, pc) : swz_v<G::NCH>(r, pc);
+        if (c >= G::DCH) c = 0;
+        bll(rs, base + uu * 1024, (rs_ * D + c * 8) * 2, key0 * D * 2);
+      }
+    }
+  };
+  auto fetch = [&](int st, int key0) {
+    fetch_one(std::true_type{}, st, key0);
+    fetch_one(std::false_type{}, st, key0);
+  };
+
+  int koff[G::DQ];
+#pragma unroll
+  for (int s = 0; s < G::DQ; ++s) koff[s] = l32 * G::RB + (swz_k<G::NCH>(l32, 2 * s + hf) << 4);
+  int voff[G::DT];
+  {
+    const int vr = hf * 4 + (n16 >> 2);
+#pragma unroll
+    for (int dt = 0; dt < G::DT; ++dt) {
+      const int c = dt * 4 + (g16 & 1) * 2 + ((n16 & 3) >> 1);
+      voff[dt] = vr * G::RB + (swz_v<G::NCH>(vr, c) << 4) + (n16 & 1) * 8;
+    }
+  }
+
+  float m_ref = 0.0f;
+  float l_part = 0.0f;
+  bool ref_set = false;                      // wave-uniform: the reference is taken
+  f32x16 oacc[G::DT];
+#pragma unroll
+  for (int dt = 0; dt < G::DT; ++dt) oacc[dt] = f32x16{};
+
+  auto qk = [&](f32x16& sacc, const unsigned char* kt) {
+    sacc = f32x16{};
+#pragma unroll
+    for (int s = 0; s < G::DQ; ++s) {
+      const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kt + koff[s]);
+      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[s], sacc, 0, 0, 0);
+    }
+  };
+  auto mask_tail = [&](f32x16& sacc, int valid) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int key = (r >> 2) * 8 + hf * 4 + (r & 3);
+      if (key >= valid) sacc[r] = -INFINITY;
+    }
+  };
+  auto set_ref = [&](const f32x16& sacc) {
+    float mx = sacc[0];
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[r]);
+    m_ref = swap_halves_max(mx) * sl2;
+  };
+  auto softmax = [&](const f32x16& sacc, bf16x8 (&pop)[2]) {
+    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+    float lsum = l_part;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      u32x4 wv;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kk * 8 + 2 * e], sl2, -m_ref));
+        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kk * 8 + 2 * e + 1], sl2, -m_ref));
+        const bf16x2 pb = cvt2(p0, p1);
+        lsum = __builtin_amdgcn_fdot2_f32_bf16(pb, ones, lsum, false);
+        wv[e] = __builtin_bit_cast(unsigned, pb);
+      }
+      pop[kk] = __builtin_bit_cast(bf16x8, wv);
+    }
+    l_part = lsum;
+  };
+  auto pv = [&](const bf16x8 (&pop)[2], const unsigned char* vt) {
+#pragma unroll
+    for (int dt = 0; dt < G::DT; ++dt) {
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        const unsigned char* pp = vt + voff[dt] + kk * 16 * G::RB;
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(pp));
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(pp + 8 * G::RB));
+        const u32x2 lw = __builtin_bit_cast(u32x2, lo);
+        const u32x2 hw = __builtin_bit_cast(u32x2, hi);
+        const u32x4 vw = {lw[0], lw[1], hw[0], hw[1]};
+        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vw), pop[kk], oacc[dt], 0, 0, 0);
+      }
+    }
+  };
+  auto rescale_if_large = [&]() {
+    if (__builtin_amdgcn_ballot_w64(l_part > 0x1p64f) != 0) {
+      asm volatile("");
+      const float l_tot = swap_halves_sum(l_part);
+      const int e = l_tot > 0x1p64f ? __builtin_amdgcn_frexp_expf(l_tot) : 0;
+      const float f = __builtin_amdgcn_ldexpf(1.0f, -e);
+      l_part *= f;
+#pragma unroll
+      for (int dt = 0; dt < G::DT; ++dt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[dt][r] *= f;
+      m_ref += (float)e;
+    }
+  };
+
+  // ---- pipeline over the union, two entries (four chunks) per iteration ----
+  // Chunk c of an iteration: entry u0 (c = 0, 1) or u1 (c = 2, 3), half c % 2,
+  // in stage c.  After the barrier of chunk c the stage of chunk c-1 is free
+  // and receives the chunk three ahead (u1's second half, then u2's halves and
+  // u3's first).  Each chunk issues one load group (past the end: block 0, in
+  // bounds), so the wait count is a constant, as in the 32-query kernel.
+  int u0 = ent(0), u1 = ent(1), u2 = ent(2), u3 = ent(3);
+  f32x16 sacc = f32x16{};
+  if (U > 0) {
+    fetch(0, key0_of(u0, 0));
+    fetch(1, key0_of(u0, 1));
+    fetch(2, key0_of(u1, 0));
+    wait_vmcnt<2 * NUW * (PD - 1)>();
+    wg_barrier();
+    if (active(u0)) {
+      qk(sacc, &Ks[0][0]);
+      const int valid = __builtin_amdgcn_readfirstlane(N - key0_of(u0, 0));
+      if (valid < CK) mask_tail(sacc, valid);
+      set_ref(sacc);                         // chunk 0 of a block holds a valid key
+      ref_set = true;
+    }
+  }
+  for (int e = 0; e < U; e += 2) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      wait_vmcnt_lds_idle<2 * NUW * (PD - 2)>();     // chunk c+1 landed
+      wg_barrier();
+      if (c == 0) fetch(3, key0_of(u1, 1));
+      else if (c == 1) fetch(0, key0_of(u2, 0));
+      else if (c == 2) fetch(1, key0_of(u2, 1));
+      else fetch(2, key0_of(u3, 0));
+      const int uc = c < 2 ? u0 : u1;                 // this chunk's entry
+      const int un = c == 0 ? u0 : (c < 3 ? u1 : u2); // the next chunk's entry
+      const int nkey0 = key0_of(un, (c + 1) & 1);
+      f32x16 snext = f32x16{};
+      bf16x8 pop[2];
+      if (active(un)) qk(snext, &Ks[(c + 1) & 3][0]);
+      if (active(uc)) {
+        if (!ref_set) {
+          set_ref(sacc);
+          ref_set = true;
+        }
+        softmax(sacc, pop);
+        pv(pop, &Vs[c][0]);
+      }
+      const int nvalid = __builtin_amdgcn_readfirstlane(N - nkey0);
+      if (nvalid < CK && active(un)) {
+        asm volatile("");
+        mask_tail(snext, nvalid);
+      }
+      sacc = snext;
+      if (c & 1) rescale_if_large();                 // after each 64-key block
+    }
+    u0 = u2;
+    u1 = u3;
+    u2 = ent(e + 4);
+    u3 = ent(e + 5);
+  }
+  wait_vmcnt<0>();           // no load may still target this workgroup's LDS
+
+  // ---- epilogue: overflow check, then O = O^T / l and LSE ----
+  const float l_tot = swap_halves_sum(l_part);
+  bool over = !(l_tot < 0x1p100f);
+#pragma unroll
+  for (int dt = 0; dt < G::DT; ++dt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) over |= !__builtin_isfinite(oacc[dt][r]);
+  if (__builtin_amdgcn_ballot_w64(over) != 0 && lane == 0) atomicOr(&wg_bad, 1);
+  __syncthreads();
+  if (wg_bad) {
+    if (threadIdx.x < 2 && (threadIdx.x == 0 || has_b)) {
+      const size_t first = head + (size_t)(2 * p + threadIdx.x) * S * D;
+      if constexpr (OUT_F32) static_cast<float*>(a.out)[first] = __builtin_nanf("");
+      else static_cast<uint16_t*>(a.out)[first] = 0x7FC0;
+    }
+    return;
+  }
+  const bool has = ref_set && l_tot > 0.0f;
+  const float inv = has ? 1.0f / l_tot : 0.0f;
+  if (qb < nB && qr < N) {
+    const size_t obase = head + (size_t)qr * D;
+#pragma unroll
+    for (int dt = 0; dt < G::DT; ++dt)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int d = dt * 32 + r4 * 8 + hf * 4;
+        if (d < D) {
+          const float o0 = oacc[dt][r4 * 4 + 0] * inv, o1 = oacc[dt][r4 * 4 + 1] * inv;
+          const float o2 = oacc[dt][r4 * 4 + 2] * inv, o3 = oacc[dt][r4 * 4 + 3] * inv;
+          if constexpr (OUT_F32) {
+            *reinterpret_cast<float4*>(static_cast<float*>(a.out) + obase + d) = make_float4(o0, o1, o2, o3);
+          } else {
+            const bf16x2 x = cvt2(o0, o1), y = cvt2(o2, o3);
+            const bf16x4 o = {x[0], x[1], y[0], y[1]};
+            *reinterpret_cast<bf16x4*>(static_cast<uint16_t*>(a.out) + obase + d) = o;
+          }
+        }
+      }
+    if (a.lse && hf == 0)
+      a.lse[(size_t)bh * N + qr] = has ? (m_ref + __log2f(l_tot)) * 0.69314718055994530942f : -INFINITY;
+  }
+}
+
+template <int D>
+hipError_t launch_pair(const Dims& d, const AttnArgs& a, hipStream_t stream) {
+  const int n_pairs = d.B * d.H * ((d.nB + 1) / 2);
+  dim3 grid(n_pairs), block(256);
+  if (d.out_f32) hipLaunchKernelGGL((attn_pair_kernel<D, true>), grid, block, 0, stream, a, n_pairs);
+  else hipLaunchKernelGGL((attn_pair_kernel<D, false>), grid, block, 0, stream, a, n_pairs);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+// Pairs pay off when neighbours share most of their blocks, which goes with
+// dense lists: measured on the block-64 layers, lists of 30% or more of the
+// blocks ran 3-23% faster in pairs, 25% ran level and 10% ran 17% slower (the
+// waves of a block that does not keep an entry sit idle while it is staged).
+bool pair_attention_fits(const Dims& d, int kmax) {
+  return d.S == 64 && d.nB <= kPairMaxBlocks && 25LL * kmax >= 7LL * d.nB;
+}
+
+hipError_t launch_attention_pair(const Dims& d, const AttnArgs& a, hipStream_t stream) {
+  switch (d.D) {
+    case 64: return launch_pair<64>(d, a, stream);
+    case 112: return launch_pair<112>(d, a, stream);
+    case 128: return launch_pair<128>(d, a, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace sva

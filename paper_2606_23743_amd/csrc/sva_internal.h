@@ -33,6 +33,13 @@ hipError_t launch_attention_rescaling(const Dims& d, bool sparse, const AttnArgs
 // attention_q32.hip.
 hipError_t launch_attention_q32(const Dims& d, bool sparse, const AttnArgs& a, hipStream_t stream);
 
+// Sparse attention for 64-token blocks, two neighbouring query blocks per
+// workgroup walking the union of their lists; attention_pair.hip.  Used when
+// pair_attention_fits (S = 64, at most 4096 key blocks, lists of at least 28%
+// of the blocks).
+bool pair_attention_fits(const Dims& d, int kmax);
+hipError_t launch_attention_pair(const Dims& d, const AttnArgs& a, hipStream_t stream);
+
 // fp8 (e4m3) quantisation and attention; fp8_quant.hip, attention_fp8.hip.
 // Codes: q8, k8 [B, H, Np, D]; v8 [B, H, Np/64, D, 64] (Np = nB * S, padding
 // rows zero).  Exponents: q_exp, k_exp [B, H, nB]; v_exp [B, H, D].
