@@ -328,14 +328,22 @@ void attn_pair_kernel(AttnArgs a, int n_pairs) {
       const int nkey0 = key0_of(un, (c + 1) & 1);
       f32x16 snext = f32x16{};
       bf16x8 pop[2];
-      if (active(un)) qk(snext, &Ks[(c + 1) & 3][0]);
-      if (active(uc)) {
-        if (!ref_set) {
-          set_ref(sacc);
-          ref_set = true;
-        }
+      if (active(uc) && !ref_set) {                    // the wave's first chunk
+        set_ref(sacc);
+        ref_set = true;
+      }
+      if (active(un) && active(uc)) {
+        // the common case in one basic block, so that the next chunk's S
+        // products interleave with this chunk's softmax
+        qk(snext, &Ks[(c + 1) & 3][0]);
         softmax(sacc, pop);
         pv(pop, &Vs[c][0]);
+      } else {
+        if (active(un)) qk(snext, &Ks[(c + 1) & 3][0]);
+        if (active(uc)) {
+          softmax(sacc, pop);
+          pv(pop, &Vs[c][0]);
+        }
       }
       const int nvalid = __builtin_amdgcn_readfirstlane(N - nkey0);
       if (nvalid < CK && active(un)) {
@@ -406,21 +414,19 @@ hipError_t launch_pair(const Dims& d, const AttnArgs& a, hipStream_t stream) {
 
 }  // namespace
 
-// Pairs pay off when neighbours share most of their blocks, which goes with
-// dense lists: measured on the block-64 layers, lists of 30% or more of the
-// blocks ran 3-23% faster in pairs, 25% ran level and 10% ran 17% slower (the
-// waves of a block that does not keep an entry sit idle while it is staged).
+// Pairs pay off when neighbours share enough of their blocks, which goes with
+// denser lists.  Measured at D = 128 on the block-64 layers: rows of 18-100%
+// of the blocks ran 6-33% faster in pairs, 12% ran 2.5% slower and 10% 8%
+// slower (the waves of a block that does not keep an entry sit idle while it
+// is staged).  At D = 112 (the 2B-class layer) the single-block kernel already
+// runs near the dense rate and pairs were level or slower at every density.
 bool pair_attention_fits(const Dims& d, int kmax) {
-  return d.S == 64 && d.nB <= kPairMaxBlocks && 25LL * kmax >= 7LL * d.nB;
+  return d.S == 64 && d.D == 128 && d.nB <= kPairMaxBlocks && 20LL * kmax >= 3LL * d.nB;
 }
 
 hipError_t launch_attention_pair(const Dims& d, const AttnArgs& a, hipStream_t stream) {
-  switch (d.D) {
-    case 64: return launch_pair<64>(d, a, stream);
-    case 112: return launch_pair<112>(d, a, stream);
-    case 128: return launch_pair<128>(d, a, stream);
-    default: return hipErrorInvalidValue;
-  }
+  if (d.D != 128) return hipErrorInvalidValue;
+  return launch_pair<128>(d, a, stream);
 }
 
 }  // namespace sva

@@ -35,8 +35,8 @@ hipError_t launch_attention_q32(const Dims& d, bool sparse, const AttnArgs& a, h
 
 // Sparse attention for 64-token blocks, two neighbouring query blocks per
 // workgroup walking the union of their lists; attention_pair.hip.  Used when
-// pair_attention_fits (S = 64, at most 4096 key blocks, lists of at least 28%
-// of the blocks).
+// pair_attention_fits (S = 64, D = 128, at most 4096 key blocks, rows of at
+// least 15% of the blocks).
 bool pair_attention_fits(const Dims& d, int kmax);
 hipError_t launch_attention_pair(const Dims& d, const AttnArgs& a, hipStream_t stream);
 

@@ -226,9 +226,9 @@ def test_keep_all_equals_dense_and_determinism(S):
 
 
 def test_block_pairs_match_single_blocks():
-    """At block 64, rows of at least 28% of the blocks (kmax) run as pairs of
-    neighbouring query blocks over the union of their lists; shorter rows one
-    block at a time.  The same lists in longer rows (padded with -1 past the
+    """At block 64 and D = 128, rows of at least 15% of the blocks (kmax) run
+    as pairs of neighbouring query blocks over the union of their lists;
+    shorter rows one block at a time.  The same lists in longer rows (padded with -1 past the
     counts) take the pair path: outputs and LSE must match bit for bit, with an
     odd block count (the last pair has one block)."""
     wl, bits, dev, prob = _small(seed=16, D=128, S=64, grid=(3, 10, 13), H=2)
@@ -236,7 +236,7 @@ def test_block_pairs_match_single_blocks():
     assert nb % 2 == 1
     qp, kp = sva.pool_blocks(prob, dev["q"], dev["k"])
     idx, cnt, _ = sva.select_blocks(prob, sva.select_topk(topk=1), qp, kp)
-    assert idx.shape[-1] * 25 < 7 * nb                      # single-block path
+    assert idx.shape[-1] * 20 < 3 * nb                      # single-block path
     wide = torch.full((1, 2, nb, nb), -1, dtype=torch.int32, device="cuda")
     wide[..., :idx.shape[-1]] = idx
     o1, l1 = sva.sparse_attention(prob, dev["q"], dev["k"], dev["v"], idx, cnt, want_lse=True)
