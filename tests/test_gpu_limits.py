@@ -79,6 +79,42 @@ def test_selection_and_attention_at_2048_blocks(wl):
     say(f"[limits {wl.name}] fp8 rms {rms:.2e} (model {pred:.2e})")
 
 
+def test_block_pairs_at_4096_blocks():
+    """The block-pair kernel at its largest size: D = 128, 64-token blocks,
+    nB = 4096 (128 bitmap words, two compaction steps), rows of 16% of the
+    blocks from the oracle's selection (the selection kernel itself takes at
+    most 2048 blocks per row and says so); attention on sampled rows (first
+    and last pairs included) against the oracle."""
+    wl = SC("nb4096_pairs", 1, 1, 128, (4, 256, 256), 64, "topk", keep_ratio=0.16, seed=214)
+    bits = inputs.generate(wl)
+    dev = device_inputs(bits)
+    prob = sva.problem_for(wl)
+    nb = sva.num_blocks(prob)
+    assert nb == 4096
+    qp, kp = sva.pool_blocks(prob, dev["q"], dev["k"])
+    with pytest.raises(sva.SvaError) as err:
+        sva.select_blocks(prob, sva.select_for(wl), qp, kp)
+    assert err.value.status == 4                            # unsupported block count
+    f64 = {n: oracle.bf16_bits_to_f64(bits[n]) for n in ("q", "k", "v")}
+    scores = oracle.block_scores(oracle.pool_blocks(f64["q"], wl.block), oracle.pool_blocks(f64["k"], wl.block),
+                                 scale_of(wl))
+    kept, _ = oracle_select(wl, scores)
+    oidx, ocnt = _kept_arrays(kept, nb)
+    assert oidx.shape[-1] * 20 >= 3 * nb                    # the pair path
+    out, lse = sva.sparse_attention(prob, dev["q"], dev["k"], dev["v"], oidx, ocnt, want_lse=True)
+    torch.cuda.synchronize()
+    rows = [0, 1, 2047, 4094, 4095]
+    ref, rlse = oracle.block_sparse_attention(f64["q"], f64["k"], f64["v"], kept, wl.block, scale_of(wl),
+                                              rows=[(0, 0, i) for i in rows])
+    o = out.float().cpu().numpy()
+    for i in rows:
+        sl = slice(i * wl.block, (i + 1) * wl.block)
+        mx, mean = parity.attention_errors(o[0, 0, sl], ref[0, 0, sl], np.ones(ref[0, 0, sl].shape, dtype=bool))
+        assert mx <= parity.MAX_ABS and mean <= parity.MEAN_ABS, (i, mx, mean)
+        assert np.all(np.abs(lse.cpu().numpy()[0, 0, sl] - rlse[0, 0, sl]) <= parity.LSE_TOL), i
+    say(f"[limits nb4096 pairs] rows {rows} within the parity bounds")
+
+
 def test_fp8_dense_at_2047_blocks():
     wl = SC("nb2047_dense", 1, 1, 64, (23, 89, 64), 64, "topk", topk=1, seed=213)
     bits = inputs.generate(wl)
