@@ -340,6 +340,39 @@ def test_gradual_logit_growth_is_exact(S, D):
         assert np.all(err <= parity.LSE_TOL + 1e-5 * np.abs(rlse)), err.max()
 
 
+def test_block_pair_overflow_is_recomputed():
+    """The block-64 pair kernel (D = 128) with a later kept block whose logits
+    exceed the first chunk's reference by about 1000 (log2 units): the pair
+    is marked and recomputed with per-iteration rescaling, and every query
+    block matches the oracle."""
+    S, D = 64, 128
+    wl = SC("overflow_pairs", 1, 1, D, (4, 8, 16), S, "topk", topk=2, seed=33)   # N = 512, 8 blocks
+    bits = inputs.generate(wl)
+    f = {n: inputs.bf16_bits_to_f32(bits[n]).copy() for n in ("q", "k", "v")}
+    f["k"][0, 0, 0:64] *= 1e-3
+    f["q"][0, 0, 128:256] = 8.0                      # query blocks 2 and 3
+    f["k"][0, 0, 384:512] = 8.0                      # key blocks 6 and 7
+    new_bits = {n: inputs._round_bf16(f[n]) for n in f}
+    dev = device_inputs(new_bits)
+    prob = sva.problem_for(wl)
+    rows = [[0, 1], [1, 2], [0, 6], [0, 7], [3, 4], [4, 5], [5, 6], [6, 7]]
+    idx = np.array(rows, dtype=np.int32).reshape(1, 1, 8, 2)
+    cnt = np.full((1, 1, 8), 2, dtype=np.int32)
+    assert 2 * 20 >= 3 * 8                          # the pair path
+    out, lse = sva.sparse_attention(prob, dev["q"], dev["k"], dev["v"], torch.from_numpy(idx).cuda(),
+                                    torch.from_numpy(cnt).cuda(), want_lse=True)
+    torch.cuda.synchronize()
+    f64 = {n: oracle.bf16_bits_to_f64(new_bits[n]) for n in ("q", "k", "v")}
+    ref, rlse = oracle.block_sparse_attention(f64["q"], f64["k"], f64["v"], [[rows]], S, scale_of(wl))
+    assert rlse.max() > 400.0                        # the regime this test is about
+    o = out.float().cpu().numpy()
+    assert np.isfinite(o).all()
+    mx, mean = parity.attention_errors(o, ref, np.ones(ref.shape, dtype=bool))
+    assert mx <= parity.MAX_ABS and mean <= parity.MEAN_ABS, (mx, mean)
+    err = np.abs(lse.cpu().numpy() - rlse)
+    assert np.all(err <= parity.LSE_TOL + 1e-5 * np.abs(rlse)), err.max()
+
+
 @pytest.mark.parametrize("S,D", [(128, 128), (128, 112), (128, 64)])
 def test_logit_growth_beyond_fixed_reference_is_exact(S, D):
     """Block-size-128 kernels fix the softmax reference max from the first key
