@@ -57,6 +57,7 @@ CASES = [
     ("d64_s64_short", 1, 2, 64, (1, 1, 40), 64),
     ("d128_s64", 1, 3, 128, (4, 6, 10), 64),
     ("d64_s128", 2, 1, 64, (5, 3, 20), 128),
+    ("d128_s64_h10", 2, 10, 128, (2, 5, 13), 64),     # a full and a partial group of 8 heads
 ]
 
 
