@@ -19,9 +19,7 @@
 // list semantics.  Per chunk, the arithmetic of a wave is that of the
 // 32-query kernel (Sᵀ = K·Qᵀ, fixed reference maximum from the wave's first
 // chunk, P rounded to bf16 with l summed from it, Oᵀ += Vᵀ·Pᵀ).
-#include <type_traits>
-
-#include "attn_common.h"
+#include "attn_wave32.h"
 
 namespace sva {
 namespace {
@@ -54,8 +52,6 @@ void attn_pair_kernel(AttnArgs a, int n_pairs) {
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int hf = lane >> 5;
   const int l32 = lane & 31;
-  const int g16 = lane >> 4;
-  const int n16 = lane & 15;
   const int N = a.N, nB = a.nB;
   const float sl2 = a.scale_log2;
 
@@ -100,11 +96,8 @@ void attn_pair_kernel(AttnArgs a, int n_pairs) {
   if (__builtin_amdgcn_ballot_w64(bad) != 0 && lane == 0) atomicOr(&list_bad, 1);
   __syncthreads();
   if (list_bad) {                            // general lists: recomputed by the rescaling kernel
-    if (threadIdx.x < 2 && (threadIdx.x == 0 || has_b)) {
-      const size_t first = head + (size_t)(2 * p + threadIdx.x) * S * D;
-      if constexpr (OUT_F32) static_cast<float*>(a.out)[first] = __builtin_nanf("");
-      else static_cast<uint16_t*>(a.out)[first] = 0x7FC0;
-    }
+    if (threadIdx.x < 2 && (threadIdx.x == 0 || has_b))
+      mark_block<OUT_F32>(a.out, head + (size_t)(2 * p + threadIdx.x) * S * D);
     return;
   }
   if (w == 0) {                              // compaction in block order, 64 words per step
@@ -140,81 +133,18 @@ void attn_pair_kernel(AttnArgs a, int n_pairs) {
   auto active = [&](int u) -> bool { return ((u >> qsel) & 1) != 0; };
   auto key0_of = [&](int u, int c2) -> int { return (u >> 2) * S + c2 * CK; };
 
-  // ---- Q^T operand: query qb*S + (w&1)*32 + l32, d = s*16 + hf*8 + 0..7 ----
+  // ---- Q^T operand: query qb*S + (w&1)*32 + l32 ----
   const int qr = qb * S + (w & 1) * 32 + l32;
   bf16x8 qop[G::DQ];
-#pragma unroll
-  for (int s = 0; s < G::DQ; ++s) {
-    if (qb < nB && qr < N) qop[s] = *reinterpret_cast<const bf16x8*>(Qh + (size_t)qr * D + s * 16 + hf * 8);
-    else qop[s] = bf16x8{};
-  }
+  load_q<D>(qop, Qh, qr, qb < nB && qr < N, hf);
 
-  // ---- direct global -> LDS fetch of one chunk (this wave's 1 KB pieces),
-  // as in the 32-query kernel: a partial last chunk clamps its rows, a chunk
-  // wholly past the end reads chunk 0 ----
-  const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc((void*)Kh, (short)0, N * D * 2, 0x00020000);
-  const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc((void*)Vh, (short)0, N * D * 2, 0x00020000);
-  int kgv[NUW], vgv[NUW];
-#pragma unroll
-  for (int v = 0; v < NUW; ++v) {
-    const int r = (w * NUW + v) * G::RPI + lane / G::NCH;
-    const int pc = lane % G::NCH;
-    int ck = swz_k<G::NCH>(r, pc), cv = swz_v<G::NCH>(r, pc);
-    if (ck >= G::DCH) ck = 0;
-    if (cv >= G::DCH) cv = 0;
-    kgv[v] = (r * D + ck * 8) * 2;
-    vgv[v] = (r * D + cv * 8) * 2;
-  }
-  typedef __attribute__((address_space(3))) unsigned char lds_u8;
-  const unsigned ks_base = __builtin_amdgcn_readfirstlane((unsigned)(size_t)(lds_u8*)&Ks[0][0]);
-  const unsigned vs_base = __builtin_amdgcn_readfirstlane((unsigned)(size_t)(lds_u8*)&Vs[0][0]);
-  auto bll = [&](const __amdgpu_buffer_rsrc_t& rs, unsigned lds_addr, int voff, int soff) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_u8*)(size_t)__builtin_amdgcn_readfirstlane(lds_addr), 16,
-                                             voff, __builtin_amdgcn_readfirstlane(soff), 0, 0);
-  };
-  auto fetch_one = [&](auto tk, int st, int key0) {
-    constexpr bool TK = decltype(tk)::value;
-    const __amdgpu_buffer_rsrc_t& rs = TK ? krs : vrs;
-    const unsigned base = (TK ? ks_base : vs_base) + st * CT;
-    key0 = __builtin_amdgcn_readfirstlane(key0);
-    if (key0 + CK <= N) {
-#pragma unroll
-      for (int v = 0; v < NUW; ++v)
-        bll(rs, base + (w * NUW + v) * 1024, TK ? kgv[v] : vgv[v], key0 * D * 2);
-    } else {
-      if (key0 >= N) key0 = 0;
-      const int valid = N - key0;
-      int ln = lane;
-      asm volatile("" : "+v"(ln));
-      const int pc = ln % G::NCH;
-#pragma unroll
-      for (int v = 0; v < NUW; ++v) {
-        const int uu = w * NUW + v;
-        const int r = uu * G::RPI + ln / G::NCH;
-        const int rs_ = r < valid ? r : 0;
-        int c = TK ? swz_k<G::NCH>(r, pc) : swz_v<G::NCH>(r, pc);
-        if (c >= G::DCH) c = 0;
-        bll(rs, base + uu * 1024, (rs_ * D + c * 8) * 2, key0 * D * 2);
-      }
-    }
-  };
-  auto fetch = [&](int st, int key0) {
-    fetch_one(std::true_type{}, st, key0);
-    fetch_one(std::false_type{}, st, key0);
-  };
+  // direct global -> LDS loads of this wave's pieces of a chunk
+  ChunkLoader<D, NUW, CT> ld;
+  loader_init(ld, Kh, Vh, N, &Ks[0][0], &Vs[0][0], w, lane);
+  auto fetch = [&](int st, int key0) { load_chunk(ld, st, key0); };
 
-  int koff[G::DQ];
-#pragma unroll
-  for (int s = 0; s < G::DQ; ++s) koff[s] = l32 * G::RB + (swz_k<G::NCH>(l32, 2 * s + hf) << 4);
-  int voff[G::DT];
-  {
-    const int vr = hf * 4 + (n16 >> 2);
-#pragma unroll
-    for (int dt = 0; dt < G::DT; ++dt) {
-      const int c = dt * 4 + (g16 & 1) * 2 + ((n16 & 3) >> 1);
-      voff[dt] = vr * G::RB + (swz_v<G::NCH>(vr, c) << 4) + (n16 & 1) * 8;
-    }
-  }
+  int koff[G::DQ], voff[G::DT];
+  operand_offsets<D>(lane, koff, voff);
 
   float m_ref = 0.0f;
   float l_part = 0.0f;
@@ -223,74 +153,9 @@ void attn_pair_kernel(AttnArgs a, int n_pairs) {
 #pragma unroll
   for (int dt = 0; dt < G::DT; ++dt) oacc[dt] = f32x16{};
 
-  auto qk = [&](f32x16& sacc, const unsigned char* kt) {
-    sacc = f32x16{};
-#pragma unroll
-    for (int s = 0; s < G::DQ; ++s) {
-      const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kt + koff[s]);
-      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[s], sacc, 0, 0, 0);
-    }
-  };
-  auto mask_tail = [&](f32x16& sacc, int valid) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int key = (r >> 2) * 8 + hf * 4 + (r & 3);
-      if (key >= valid) sacc[r] = -INFINITY;
-    }
-  };
-  auto set_ref = [&](const f32x16& sacc) {
-    float mx = sacc[0];
-#pragma unroll
-    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[r]);
-    m_ref = swap_halves_max(mx) * sl2;
-  };
-  auto softmax = [&](const f32x16& sacc, bf16x8 (&pop)[2]) {
-    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-    float lsum = l_part;
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      u32x4 wv;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kk * 8 + 2 * e], sl2, -m_ref));
-        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kk * 8 + 2 * e + 1], sl2, -m_ref));
-        const bf16x2 pb = cvt2(p0, p1);
-        lsum = __builtin_amdgcn_fdot2_f32_bf16(pb, ones, lsum, false);
-        wv[e] = __builtin_bit_cast(unsigned, pb);
-      }
-      pop[kk] = __builtin_bit_cast(bf16x8, wv);
-    }
-    l_part = lsum;
-  };
-  auto pv = [&](const bf16x8 (&pop)[2], const unsigned char* vt) {
-#pragma unroll
-    for (int dt = 0; dt < G::DT; ++dt) {
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-        const unsigned char* pp = vt + voff[dt] + kk * 16 * G::RB;
-        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(pp));
-        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(pp + 8 * G::RB));
-        const u32x2 lw = __builtin_bit_cast(u32x2, lo);
-        const u32x2 hw = __builtin_bit_cast(u32x2, hi);
-        const u32x4 vw = {lw[0], lw[1], hw[0], hw[1]};
-        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vw), pop[kk], oacc[dt], 0, 0, 0);
-      }
-    }
-  };
-  auto rescale_if_large = [&]() {
-    if (__builtin_amdgcn_ballot_w64(l_part > 0x1p64f) != 0) {
-      asm volatile("");
-      const float l_tot = swap_halves_sum(l_part);
-      const int e = l_tot > 0x1p64f ? __builtin_amdgcn_frexp_expf(l_tot) : 0;
-      const float f = __builtin_amdgcn_ldexpf(1.0f, -e);
-      l_part *= f;
-#pragma unroll
-      for (int dt = 0; dt < G::DT; ++dt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[dt][r] *= f;
-      m_ref += (float)e;
-    }
-  };
+  auto qk = [&](f32x16& sacc, const unsigned char* kt) { qk_chunk<D>(sacc, kt, koff, qop); };
+  auto softmax = [&](const f32x16& sacc, bf16x8 (&pop)[2]) { softmax_chunk(sacc, pop, l_part, m_ref, sl2); };
+  auto pv = [&](const bf16x8 (&pop)[2], const unsigned char* vt) { pv_chunk<D>(pop, vt, voff, oacc); };
 
   // ---- pipeline over the union, two entries (four chunks) per iteration ----
   // Chunk c of an iteration: entry u0 (c = 0, 1) or u1 (c = 2, 3), half c % 2,
@@ -309,8 +174,8 @@ void attn_pair_kernel(AttnArgs a, int n_pairs) {
     if (active(u0)) {
       qk(sacc, &Ks[0][0]);
       const int valid = __builtin_amdgcn_readfirstlane(N - key0_of(u0, 0));
-      if (valid < CK) mask_tail(sacc, valid);
-      set_ref(sacc);                         // chunk 0 of a block holds a valid key
+      if (valid < CK) mask_tail(sacc, valid, hf);
+      m_ref = chunk_reference(sacc, sl2);    // chunk 0 of a block holds a valid key
       ref_set = true;
     }
   }
@@ -329,7 +194,7 @@ void attn_pair_kernel(AttnArgs a, int n_pairs) {
       f32x16 snext = f32x16{};
       bf16x8 pop[2];
       if (active(uc) && !ref_set) {                    // the wave's first chunk
-        set_ref(sacc);
+        m_ref = chunk_reference(sacc, sl2);
         ref_set = true;
       }
       if (active(un) && active(uc)) {
@@ -348,10 +213,10 @@ void attn_pair_kernel(AttnArgs a, int n_pairs) {
       const int nvalid = __builtin_amdgcn_readfirstlane(N - nkey0);
       if (nvalid < CK && active(un)) {
         asm volatile("");
-        mask_tail(snext, nvalid);
+        mask_tail(snext, nvalid, hf);
       }
       sacc = snext;
-      if (c & 1) rescale_if_large();                 // after each 64-key block
+      if (c & 1) rescale_if_large<D>(l_part, m_ref, oacc);                 // after each 64-key block
     }
     u0 = u2;
     u1 = u3;
@@ -362,45 +227,17 @@ void attn_pair_kernel(AttnArgs a, int n_pairs) {
 
   // ---- epilogue: overflow check, then O = O^T / l and LSE ----
   const float l_tot = swap_halves_sum(l_part);
-  bool over = !(l_tot < 0x1p100f);
-#pragma unroll
-  for (int dt = 0; dt < G::DT; ++dt)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) over |= !__builtin_isfinite(oacc[dt][r]);
+  const bool over = overflowed<D>(l_tot, oacc);
   if (__builtin_amdgcn_ballot_w64(over) != 0 && lane == 0) atomicOr(&wg_bad, 1);
   __syncthreads();
   if (wg_bad) {
-    if (threadIdx.x < 2 && (threadIdx.x == 0 || has_b)) {
-      const size_t first = head + (size_t)(2 * p + threadIdx.x) * S * D;
-      if constexpr (OUT_F32) static_cast<float*>(a.out)[first] = __builtin_nanf("");
-      else static_cast<uint16_t*>(a.out)[first] = 0x7FC0;
-    }
+    if (threadIdx.x < 2 && (threadIdx.x == 0 || has_b))
+      mark_block<OUT_F32>(a.out, head + (size_t)(2 * p + threadIdx.x) * S * D);
     return;
   }
   const bool has = ref_set && l_tot > 0.0f;
-  const float inv = has ? 1.0f / l_tot : 0.0f;
-  if (qb < nB && qr < N) {
-    const size_t obase = head + (size_t)qr * D;
-#pragma unroll
-    for (int dt = 0; dt < G::DT; ++dt)
-#pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        const int d = dt * 32 + r4 * 8 + hf * 4;
-        if (d < D) {
-          const float o0 = oacc[dt][r4 * 4 + 0] * inv, o1 = oacc[dt][r4 * 4 + 1] * inv;
-          const float o2 = oacc[dt][r4 * 4 + 2] * inv, o3 = oacc[dt][r4 * 4 + 3] * inv;
-          if constexpr (OUT_F32) {
-            *reinterpret_cast<float4*>(static_cast<float*>(a.out) + obase + d) = make_float4(o0, o1, o2, o3);
-          } else {
-            const bf16x2 x = cvt2(o0, o1), y = cvt2(o2, o3);
-            const bf16x4 o = {x[0], x[1], y[0], y[1]};
-            *reinterpret_cast<bf16x4*>(static_cast<uint16_t*>(a.out) + obase + d) = o;
-          }
-        }
-      }
-    if (a.lse && hf == 0)
-      a.lse[(size_t)bh * N + qr] = has ? (m_ref + __log2f(l_tot)) * 0.69314718055994530942f : -INFINITY;
-  }
+  if (qb < nB && qr < N)
+    store_query<D, OUT_F32>(a.out, a.lse, head + (size_t)qr * D, (size_t)bh * N + qr, oacc, l_tot, m_ref, has, hf);
 }
 
 template <int D>

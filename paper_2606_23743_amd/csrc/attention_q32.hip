@@ -26,9 +26,7 @@
 // logits jump by more than ~2^63 over the running sum inside one block) is
 // marked (NaN first element) and recomputed by the per-iteration rescaling
 // kernel that runs next.
-#include <type_traits>
-
-#include "attn_common.h"
+#include "attn_wave32.h"
 
 namespace sva {
 namespace {
@@ -57,8 +55,6 @@ void attn_q32_kernel(AttnArgs a) {
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int hf = lane >> 5;
   const int l32 = lane & 31;
-  const int g16 = lane >> 4;
-  const int n16 = lane & 15;
   const int N = a.N, nB = a.nB;
   const float sl2 = a.scale_log2;
 
@@ -75,14 +71,10 @@ void attn_q32_kernel(AttnArgs a) {
   const uint16_t* Kh = a.k + head;
   const uint16_t* Vh = a.v + head;
 
-  // ---- Q^T operand: query i*S + w*32 + l32, d = s*16 + hf*8 + 0..7 ----
+  // ---- Q^T operand: query i*S + w*32 + l32 ----
   const int qr = i * S + w * 32 + l32;
   bf16x8 qop[G::DQ];
-#pragma unroll
-  for (int s = 0; s < G::DQ; ++s) {
-    if (qr < N) qop[s] = *reinterpret_cast<const bf16x8*>(Qh + (size_t)qr * D + s * 16 + hf * 8);
-    else qop[s] = bf16x8{};
-  }
+  load_q<D>(qop, Qh, qr, qr < N, hf);
 
   // ---- the kept-block list ----
   // Read through the constant address space: uniform reads become scalar
@@ -104,87 +96,15 @@ void attn_q32_kernel(AttnArgs a) {
     return it;
   };
 
-  // ---- direct global -> LDS fetch of one chunk (this wave's 1 KB pieces) ----
-  // Piece u covers chunk rows u*RPI .. u*RPI + RPI - 1; lane L fills row
-  // u*RPI + L/NCH at position L % NCH, i.e. global piece (L % NCH) ^ swizzle(row).
-  // A wave always loads the same pieces, so its per-lane byte offsets are
-  // fixed and the chunk's key offset is the scalar offset.  Every address
-  // formed lies inside the head's rows: full chunks by construction, the
-  // sequence's last partial chunk by clamping rows past the end to its first
-  // row, and a chunk wholly past the end (the rest of a partial block, or a
-  // pipeline slot with nothing left to load) by reading chunk 0 instead.
-  const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc((void*)Kh, (short)0, N * D * 2, 0x00020000);
-  const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc((void*)Vh, (short)0, N * D * 2, 0x00020000);
-  int kgv[NUW], vgv[NUW];
-#pragma unroll
-  for (int v = 0; v < NUW; ++v) {
-    const int r = (w * NUW + v) * G::RPI + lane / G::NCH;
-    const int p = lane % G::NCH;
-    int ck = swz_k<G::NCH>(r, p), cv = swz_v<G::NCH>(r, p);
-    if (ck >= G::DCH) ck = 0;                        // padding pieces: any in-row address
-    if (cv >= G::DCH) cv = 0;
-    kgv[v] = (r * D + ck * 8) * 2;
-    vgv[v] = (r * D + cv * 8) * 2;
-  }
-  typedef __attribute__((address_space(3))) unsigned char lds_u8;
-  const unsigned ks_base = __builtin_amdgcn_readfirstlane((unsigned)(size_t)(lds_u8*)&Ks[0][0]);
-  const unsigned vs_base = __builtin_amdgcn_readfirstlane((unsigned)(size_t)(lds_u8*)&Vs[0][0]);
-  auto bll = [&](const __amdgpu_buffer_rsrc_t& rs, unsigned lds_addr, int voff, int soff) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_u8*)(size_t)__builtin_amdgcn_readfirstlane(lds_addr), 16,
-                                             voff, __builtin_amdgcn_readfirstlane(soff), 0, 0);
-  };
-  // One tensor's pieces of one chunk into stage st (TK: K, else V).
-  auto fetch_one = [&](auto tk, int st, int key0) {
-    constexpr bool TK = decltype(tk)::value;
-    const __amdgpu_buffer_rsrc_t& rs = TK ? krs : vrs;
-    const unsigned base = (TK ? ks_base : vs_base) + st * CT;
-    key0 = __builtin_amdgcn_readfirstlane(key0);
-    if (key0 + CK <= N) {
-#pragma unroll
-      for (int v = 0; v < NUW; ++v)
-        bll(rs, base + (w * NUW + v) * 1024, TK ? kgv[v] : vgv[v], key0 * D * 2);
-    } else {
-      // The lane id goes through an empty asm so this rare path's per-lane
-      // values are recomputed here rather than hoisted and kept live.
-      if (key0 >= N) key0 = 0;
-      const int valid = N - key0;
-      int ln = lane;
-      asm volatile("" : "+v"(ln));
-      const int p = ln % G::NCH;
-#pragma unroll
-      for (int v = 0; v < NUW; ++v) {
-        const int u = w * NUW + v;
-        const int r = u * G::RPI + ln / G::NCH;
-        const int rs_ = r < valid ? r : 0;
-        int c = TK ? swz_k<G::NCH>(r, p) : swz_v<G::NCH>(r, p);
-        if (c >= G::DCH) c = 0;
-        bll(rs, base + u * 1024, (rs_ * D + c * 8) * 2, key0 * D * 2);
-      }
-    }
-  };
-  auto fetch_k = [&](int st, int key0) { fetch_one(std::true_type{}, st, key0); };
-  auto fetch_v = [&](int st, int key0) { fetch_one(std::false_type{}, st, key0); };
-  auto fetch = [&](int st, int key0) {
-    fetch_k(st, key0);
-    fetch_v(st, key0);
-  };
+  // direct global -> LDS loads of this wave's pieces of a chunk
+  ChunkLoader<D, NUW, CT> ld;
+  loader_init(ld, Kh, Vh, N, &Ks[0][0], &Vs[0][0], w, lane);
+  auto fetch_k = [&](int st, int key0) { load_tile<true>(ld, st, key0); };
+  auto fetch_v = [&](int st, int key0) { load_tile<false>(ld, st, key0); };
+  auto fetch = [&](int st, int key0) { load_chunk(ld, st, key0); };
 
-  // Per-lane LDS offsets.  K operand, step s: row l32 of the tile, piece
-  // 2s + hf.  V transpose reads: row (kk*16 + hf*4 + n16/4 [+8]), piece
-  // dt*4 + (g16&1)*2 + (n16&3)/2; only dt interacts with the swizzle.  The
-  // stage and the kk / +8 row offsets are immediates.
-  int koff[G::DQ];
-#pragma unroll
-  for (int s = 0; s < G::DQ; ++s) koff[s] = l32 * G::RB + (swz_k<G::NCH>(l32, 2 * s + hf) << 4);
-  int voff[G::DT];
-  {
-    const int vr = hf * 4 + (n16 >> 2);
-#pragma unroll
-    for (int dt = 0; dt < G::DT; ++dt) {
-      const int c = dt * 4 + (g16 & 1) * 2 + ((n16 & 3) >> 1);
-      voff[dt] = vr * G::RB + (swz_v<G::NCH>(vr, c) << 4) + (n16 & 1) * 8;
-    }
-  }
+  int koff[G::DQ], voff[G::DT];
+  operand_offsets<D>(lane, koff, voff);
 
   float m_ref = 0.0f;        // reference max (log2 units), fixed by the first chunk
   float l_part = 0.0f;       // this lane's half of the row sum
@@ -192,77 +112,9 @@ void attn_q32_kernel(AttnArgs a) {
 #pragma unroll
   for (int dt = 0; dt < G::DT; ++dt) oacc[dt] = f32x16{};
 
-  auto qk = [&](f32x16& sacc, const unsigned char* kt) {
-    sacc = f32x16{};
-#pragma unroll
-    for (int s = 0; s < G::DQ; ++s) {
-      const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kt + koff[s]);
-      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[s], sacc, 0, 0, 0);
-    }
-  };
-  auto mask_tail = [&](f32x16& sacc, int valid) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int key = (r >> 2) * 8 + hf * 4 + (r & 3);
-      if (key >= valid) sacc[r] = -INFINITY;
-    }
-  };
-  auto softmax = [&](const f32x16& sacc, bf16x8 (&pop)[2]) {
-    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-    float lsum = l_part;
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      u32x4 wv;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kk * 8 + 2 * e], sl2, -m_ref));
-        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kk * 8 + 2 * e + 1], sl2, -m_ref));
-        const bf16x2 pb = cvt2(p0, p1);
-        lsum = __builtin_amdgcn_fdot2_f32_bf16(pb, ones, lsum, false);
-        wv[e] = __builtin_bit_cast(unsigned, pb);
-      }
-      pop[kk] = __builtin_bit_cast(bf16x8, wv);
-    }
-    l_part = lsum;
-  };
-  auto pv = [&](const bf16x8 (&pop)[2], const unsigned char* vt) {
-#pragma unroll
-    for (int dt = 0; dt < G::DT; ++dt) {
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-        // rows r and r + 8 have the same swizzle, so one offset serves both
-        const unsigned char* p = vt + voff[dt] + kk * 16 * G::RB;
-        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p));
-        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 8 * G::RB));
-        const u32x2 lw = __builtin_bit_cast(u32x2, lo);
-        const u32x2 hw = __builtin_bit_cast(u32x2, hi);
-        const u32x4 vw = {lw[0], lw[1], hw[0], hw[1]};
-        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vw), pop[kk], oacc[dt], 0, 0, 0);
-      }
-    }
-  };
-
-  // After every kept block: if a row sum has grown past 2^64 (the reference
-  // maximum was far below this row's logits), move the reference up by the
-  // sum's binary exponent and scale that query's O and l by the same power of
-  // two (exact).  p = exp2(s - m) can then only overflow if one block raises
-  // the logits by more than ~2^63 over the running sum; that rare case is
-  // caught by the final check.  Rows never come near 2^64 in practice, so this
-  // is one compare and a branch per block.
-  auto rescale_if_large = [&]() {
-    if (__builtin_amdgcn_ballot_w64(l_part > 0x1p64f) != 0) {
-      asm volatile("");
-      const float l_tot = swap_halves_sum(l_part);
-      const int e = l_tot > 0x1p64f ? __builtin_amdgcn_frexp_expf(l_tot) : 0;
-      const float f = __builtin_amdgcn_ldexpf(1.0f, -e);
-      l_part *= f;
-#pragma unroll
-      for (int dt = 0; dt < G::DT; ++dt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[dt][r] *= f;
-      m_ref += (float)e;
-    }
-  };
+  auto qk = [&](f32x16& sacc, const unsigned char* kt) { qk_chunk<D>(sacc, kt, koff, qop); };
+  auto softmax = [&](const f32x16& sacc, bf16x8 (&pop)[2]) { softmax_chunk(sacc, pop, l_part, m_ref, sl2); };
+  auto pv = [&](const bf16x8 (&pop)[2], const unsigned char* vt) { pv_chunk<D>(pop, vt, voff, oacc); };
 
   // ---- pipeline over (kept block, chunk) ----
   // Chunk c of every block lives in stage c (NST = NCK stages), so stages and
@@ -310,11 +162,8 @@ void attn_q32_kernel(AttnArgs a) {
       wg_barrier();
       qk(sacc, &Ks[0][0]);
       const int valid = __builtin_amdgcn_readfirstlane(N - j * S);
-      if (valid < CK) mask_tail(sacc, valid);
-      float mx = sacc[0];                 // chunk 0 holds a valid key: finite
-#pragma unroll
-      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[r]);
-      m_ref = swap_halves_max(mx) * sl2;
+      if (valid < CK) mask_tail(sacc, valid, hf);
+      m_ref = chunk_reference(sacc, sl2);   // chunk 0 holds a valid key: finite
     }
     while (it < count) {
       const int itnn = itn + 1;
@@ -335,11 +184,11 @@ void attn_q32_kernel(AttnArgs a) {
         const int nvalid = __builtin_amdgcn_readfirstlane(N - nkey0);
         if (nvalid < CK) {
           asm volatile("");        // keep this a real (rarely taken) branch, not select code
-          mask_tail(snext, nvalid);
+          mask_tail(snext, nvalid, hf);
         }
         sacc = snext;
       }
-      rescale_if_large();
+      rescale_if_large<D>(l_part, m_ref, oacc);
       advance_block(itnn, jnn);
     }
   } else {
@@ -357,11 +206,8 @@ void attn_q32_kernel(AttnArgs a) {
       wg_barrier();
       qk(sacc, &Ks[0][0]);
       const int valid = __builtin_amdgcn_readfirstlane(N - j * S);
-      if (valid < CK) mask_tail(sacc, valid);
-      float mx = sacc[0];                 // chunk 0 holds a valid key: finite
-#pragma unroll
-      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[r]);
-      m_ref = swap_halves_max(mx) * sl2;
+      if (valid < CK) mask_tail(sacc, valid, hf);
+      m_ref = chunk_reference(sacc, sl2);   // chunk 0 holds a valid key: finite
     }
     while (it < count) {
       const int itnn = itn + 1;
@@ -383,11 +229,11 @@ void attn_q32_kernel(AttnArgs a) {
         const int nvalid = __builtin_amdgcn_readfirstlane(N - nkey0);
         if (nvalid < CK) {
           asm volatile("");        // keep this a real (rarely taken) branch, not select code
-          mask_tail(snext, nvalid);
+          mask_tail(snext, nvalid, hf);
         }
         sacc = snext;
       }
-      rescale_if_large();
+      rescale_if_large<D>(l_part, m_ref, oacc);
       advance_block(itnn, jnn);
     }
   }
@@ -396,46 +242,17 @@ void attn_q32_kernel(AttnArgs a) {
   // ---- epilogue: overflow check, then O = O^T / l and LSE ----
   if (threadIdx.x == 0) wg_bad = 0;
   const float l_tot = swap_halves_sum(l_part);
-  bool bad = !(l_tot < 0x1p100f);
-#pragma unroll
-  for (int dt = 0; dt < G::DT; ++dt)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) bad |= !__builtin_isfinite(oacc[dt][r]);
+  const bool bad = overflowed<D>(l_tot, oacc);
   __syncthreads();
   if (__builtin_amdgcn_ballot_w64(bad) != 0 && lane == 0) atomicOr(&wg_bad, 1);
   __syncthreads();
   if (wg_bad) {
-    if (threadIdx.x == 0 && i * S < N) {
-      if constexpr (OUT_F32) static_cast<float*>(a.out)[head + (size_t)i * S * D] = __builtin_nanf("");
-      else static_cast<uint16_t*>(a.out)[head + (size_t)i * S * D] = 0x7FC0;
-    }
+    if (threadIdx.x == 0 && i * S < N) mark_block<OUT_F32>(a.out, head + (size_t)i * S * D);
     return;
   }
   const bool has = count > 0 && l_tot > 0.0f;
-  const float inv = has ? 1.0f / l_tot : 0.0f;
-  if (qr < N) {
-    const size_t obase = head + (size_t)qr * D;
-#pragma unroll
-    for (int dt = 0; dt < G::DT; ++dt)
-#pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        const int d = dt * 32 + r4 * 8 + hf * 4;
-        if (d < D) {
-          const float o0 = oacc[dt][r4 * 4 + 0] * inv, o1 = oacc[dt][r4 * 4 + 1] * inv;
-          const float o2 = oacc[dt][r4 * 4 + 2] * inv, o3 = oacc[dt][r4 * 4 + 3] * inv;
-          if constexpr (OUT_F32) {
-            *reinterpret_cast<float4*>(static_cast<float*>(a.out) + obase + d) = make_float4(o0, o1, o2, o3);
-          } else {
-            const bf16x2 x = cvt2(o0, o1), y = cvt2(o2, o3);
-            const bf16x4 o = {x[0], x[1], y[0], y[1]};
-            *reinterpret_cast<bf16x4*>(static_cast<uint16_t*>(a.out) + obase + d) = o;
-          }
-        }
-      }
-    if (a.lse && hf == 0) {
-      a.lse[(size_t)bh * N + qr] = has ? (m_ref + __log2f(l_tot)) * 0.69314718055994530942f : -INFINITY;
-    }
-  }
+  if (qr < N)
+    store_query<D, OUT_F32>(a.out, a.lse, head + (size_t)qr * D, (size_t)bh * N + qr, oacc, l_tot, m_ref, has, hf);
 }
 
 template <int D, int S>

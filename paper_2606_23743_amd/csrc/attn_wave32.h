@@ -1,0 +1,265 @@
+// Building blocks of the bf16 attention kernels with 32 queries per wave (one
+// query per lane pair): the direct global -> LDS chunk loads, the per-lane LDS
+// offsets of the operand reads, S^T = K Q^T and O^T += V^T P^T on
+// mfma_f32_32x32x16_bf16, the fixed-reference softmax and the output store.
+// The 128-token kernel (attention_q32.hip) and the block-pair kernel
+// (attention_pair.hip) run the same per-chunk arithmetic through these.
+#pragma once
+
+#include "attn_common.h"
+
+namespace sva {
+namespace attn {
+
+typedef __attribute__((address_space(3))) unsigned char lds_u8;
+
+// Direct global -> LDS loads of one 32-key chunk (K or V tile of CT bytes):
+// the NUW 1 KB pieces this wave fills.  Piece u covers tile rows u*RPI ..;
+// lane L fills row u*RPI + L/NCH at position L % NCH with the global piece the
+// swizzle maps there, so a wave's per-lane byte offsets are fixed and the
+// chunk's key offset is the scalar offset.  Every address lies inside the
+// head's rows: full chunks by construction, the sequence's last partial chunk
+// by clamping rows past the end to its first row, and a chunk wholly past the
+// end by reading chunk 0 instead.
+template <int D, int NUW, int CT>
+struct ChunkLoader {
+  __amdgpu_buffer_rsrc_t krs, vrs;
+  int kgv[NUW], vgv[NUW];
+  unsigned ks_base, vs_base;
+  int w, lane, N;
+};
+
+template <int D, int NUW, int CT>
+__device__ __forceinline__ void loader_init(ChunkLoader<D, NUW, CT>& f, const uint16_t* Kh, const uint16_t* Vh,
+                                            int N, const unsigned char* ks, const unsigned char* vs, int w,
+                                            int lane) {
+  using G = Geo<D>;
+  f.krs = __builtin_amdgcn_make_buffer_rsrc((void*)Kh, (short)0, N * D * 2, 0x00020000);
+  f.vrs = __builtin_amdgcn_make_buffer_rsrc((void*)Vh, (short)0, N * D * 2, 0x00020000);
+#pragma unroll
+  for (int v = 0; v < NUW; ++v) {
+    const int r = (w * NUW + v) * G::RPI + lane / G::NCH;
+    const int p = lane % G::NCH;
+    int ck = swz_k<G::NCH>(r, p), cv = swz_v<G::NCH>(r, p);
+    if (ck >= G::DCH) ck = 0;                        // padding pieces: any in-row address
+    if (cv >= G::DCH) cv = 0;
+    f.kgv[v] = (r * D + ck * 8) * 2;
+    f.vgv[v] = (r * D + cv * 8) * 2;
+  }
+  f.ks_base = __builtin_amdgcn_readfirstlane((unsigned)(size_t)(const lds_u8*)ks);
+  f.vs_base = __builtin_amdgcn_readfirstlane((unsigned)(size_t)(const lds_u8*)vs);
+  f.w = w;
+  f.lane = lane;
+  f.N = N;
+}
+
+__device__ __forceinline__ void buffer_to_lds(const __amdgpu_buffer_rsrc_t& rs, unsigned lds_addr, int voff, int soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_u8*)(size_t)__builtin_amdgcn_readfirstlane(lds_addr), 16, voff,
+                                           __builtin_amdgcn_readfirstlane(soff), 0, 0);
+}
+
+// one tensor's pieces (TK: K, else V) of the chunk starting at key0 into stage st
+template <bool TK, int D, int NUW, int CT>
+__device__ __forceinline__ void load_tile(const ChunkLoader<D, NUW, CT>& f, int st, int key0) {
+  using G = Geo<D>;
+  const __amdgpu_buffer_rsrc_t& rs = TK ? f.krs : f.vrs;
+  const unsigned base = (TK ? f.ks_base : f.vs_base) + st * CT;
+  key0 = __builtin_amdgcn_readfirstlane(key0);
+  if (key0 + 32 <= f.N) {
+#pragma unroll
+    for (int v = 0; v < NUW; ++v) buffer_to_lds(rs, base + (f.w * NUW + v) * 1024, TK ? f.kgv[v] : f.vgv[v], key0 * D * 2);
+  } else {
+    // The lane id goes through an empty asm so this rare path's per-lane
+    // values are recomputed here rather than hoisted and kept live.
+    if (key0 >= f.N) key0 = 0;
+    const int valid = f.N - key0;
+    int ln = f.lane;
+    asm volatile("" : "+v"(ln));
+    const int p = ln % G::NCH;
+#pragma unroll
+    for (int v = 0; v < NUW; ++v) {
+      const int u = f.w * NUW + v;
+      const int r = u * G::RPI + ln / G::NCH;
+      const int rs_ = r < valid ? r : 0;
+      int c = TK ? swz_k<G::NCH>(r, p) : swz_v<G::NCH>(r, p);
+      if (c >= G::DCH) c = 0;
+      buffer_to_lds(rs, base + u * 1024, (rs_ * D + c * 8) * 2, key0 * D * 2);
+    }
+  }
+}
+
+template <int D, int NUW, int CT>
+__device__ __forceinline__ void load_chunk(const ChunkLoader<D, NUW, CT>& f, int st, int key0) {
+  load_tile<true>(f, st, key0);
+  load_tile<false>(f, st, key0);
+}
+
+// Per-lane LDS offsets.  K operand, step s: row l32 of the tile, piece
+// 2s + hf.  V transpose reads: row (kk*16 + hf*4 + n16/4 [+8]), piece
+// dt*4 + (g16&1)*2 + (n16&3)/2; only dt interacts with the swizzle.  The
+// stage and the kk / +8 row offsets are immediates.
+template <int D>
+__device__ __forceinline__ void operand_offsets(int lane, int (&koff)[Geo<D>::DQ], int (&voff)[Geo<D>::DT]) {
+  using G = Geo<D>;
+  const int hf = lane >> 5, l32 = lane & 31, g16 = lane >> 4, n16 = lane & 15;
+#pragma unroll
+  for (int s = 0; s < G::DQ; ++s) koff[s] = l32 * G::RB + (swz_k<G::NCH>(l32, 2 * s + hf) << 4);
+  const int vr = hf * 4 + (n16 >> 2);
+#pragma unroll
+  for (int dt = 0; dt < G::DT; ++dt) {
+    const int c = dt * 4 + (g16 & 1) * 2 + ((n16 & 3) >> 1);
+    voff[dt] = vr * G::RB + (swz_v<G::NCH>(vr, c) << 4) + (n16 & 1) * 8;
+  }
+}
+
+// Q^T operand of query qr: d = s*16 + hf*8 + 0..7 (zero when the query is absent)
+template <int D>
+__device__ __forceinline__ void load_q(bf16x8 (&qop)[Geo<D>::DQ], const uint16_t* Qh, int qr, bool present, int hf) {
+#pragma unroll
+  for (int s = 0; s < Geo<D>::DQ; ++s) {
+    if (present) qop[s] = *reinterpret_cast<const bf16x8*>(Qh + (size_t)qr * D + s * 16 + hf * 8);
+    else qop[s] = bf16x8{};
+  }
+}
+
+// S^T of a chunk: lane (query) l32, register r holds key (r/4)*8 + hf*4 + r%4
+template <int D>
+__device__ __forceinline__ void qk_chunk(f32x16& sacc, const unsigned char* kt, const int (&koff)[Geo<D>::DQ],
+                                         const bf16x8 (&qop)[Geo<D>::DQ]) {
+  sacc = f32x16{};
+#pragma unroll
+  for (int s = 0; s < Geo<D>::DQ; ++s) {
+    const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kt + koff[s]);
+    sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[s], sacc, 0, 0, 0);
+  }
+}
+
+__device__ __forceinline__ void mask_tail(f32x16& sacc, int valid, int hf) {
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int key = (r >> 2) * 8 + hf * 4 + (r & 3);
+    if (key >= valid) sacc[r] = -INFINITY;
+  }
+}
+
+// the reference maximum (log2 units) from a chunk that holds a valid key
+__device__ __forceinline__ float chunk_reference(const f32x16& sacc, float sl2) {
+  float mx = sacc[0];
+#pragma unroll
+  for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[r]);
+  return swap_halves_max(mx) * sl2;
+}
+
+// p = exp2(c*log2e*s - m) rounded to bf16; l sums the rounded weights
+__device__ __forceinline__ void softmax_chunk(const f32x16& sacc, bf16x8 (&pop)[2], float& l_part, float m_ref,
+                                              float sl2) {
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  float lsum = l_part;
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) {
+    u32x4 wv;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kk * 8 + 2 * e], sl2, -m_ref));
+      const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kk * 8 + 2 * e + 1], sl2, -m_ref));
+      const bf16x2 pb = cvt2(p0, p1);
+      lsum = __builtin_amdgcn_fdot2_f32_bf16(pb, ones, lsum, false);
+      wv[e] = __builtin_bit_cast(unsigned, pb);
+    }
+    pop[kk] = __builtin_bit_cast(bf16x8, wv);
+  }
+  l_part = lsum;
+}
+
+// O^T += V^T P^T: P from the S^T registers, V^T by transpose reads
+template <int D>
+__device__ __forceinline__ void pv_chunk(const bf16x8 (&pop)[2], const unsigned char* vt, const int (&voff)[Geo<D>::DT],
+                                         f32x16 (&oacc)[Geo<D>::DT]) {
+  using G = Geo<D>;
+#pragma unroll
+  for (int dt = 0; dt < G::DT; ++dt) {
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      // rows r and r + 8 have the same swizzle, so one offset serves both
+      const unsigned char* p = vt + voff[dt] + kk * 16 * G::RB;
+      const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p));
+      const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 8 * G::RB));
+      const u32x2 lw = __builtin_bit_cast(u32x2, lo);
+      const u32x2 hw = __builtin_bit_cast(u32x2, hi);
+      const u32x4 vw = {lw[0], lw[1], hw[0], hw[1]};
+      oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vw), pop[kk], oacc[dt], 0, 0, 0);
+    }
+  }
+}
+
+// After every kept block: if a row sum has grown past 2^64 (the reference
+// maximum was far below this row's logits), move the reference up by the
+// sum's binary exponent and scale that query's O and l by the same power of
+// two (exact).  p = exp2(s - m) can then only overflow if one block raises the
+// logits by more than ~2^63 over the running sum; that rare case is caught by
+// the final check.  Rows never come near 2^64 in practice, so this is one
+// compare and a branch per block.
+template <int D>
+__device__ __forceinline__ void rescale_if_large(float& l_part, float& m_ref, f32x16 (&oacc)[Geo<D>::DT]) {
+  if (__builtin_amdgcn_ballot_w64(l_part > 0x1p64f) != 0) {
+    asm volatile("");
+    const float l_tot = swap_halves_sum(l_part);
+    const int e = l_tot > 0x1p64f ? __builtin_amdgcn_frexp_expf(l_tot) : 0;
+    const float f = __builtin_amdgcn_ldexpf(1.0f, -e);
+    l_part *= f;
+#pragma unroll
+    for (int dt = 0; dt < Geo<D>::DT; ++dt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) oacc[dt][r] *= f;
+    m_ref += (float)e;
+  }
+}
+
+// a row that would need the per-iteration rescaling: sum past 2^100 or a
+// non-finite accumulator
+template <int D>
+__device__ __forceinline__ bool overflowed(float l_tot, const f32x16 (&oacc)[Geo<D>::DT]) {
+  bool bad = !(l_tot < 0x1p100f);
+#pragma unroll
+  for (int dt = 0; dt < Geo<D>::DT; ++dt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) bad |= !__builtin_isfinite(oacc[dt][r]);
+  return bad;
+}
+
+// the NaN mark on a query block's first output element (recomputed later)
+template <bool OUT_F32>
+__device__ __forceinline__ void mark_block(void* out, size_t first) {
+  if constexpr (OUT_F32) static_cast<float*>(out)[first] = __builtin_nanf("");
+  else static_cast<uint16_t*>(out)[first] = 0x7FC0;
+}
+
+// O = O^T / l of query qr (row base obase) and its LSE; zeros and -inf when
+// the row attended to nothing
+template <int D, bool OUT_F32>
+__device__ __forceinline__ void store_query(void* out, float* lse, size_t obase, size_t lse_at,
+                                            const f32x16 (&oacc)[Geo<D>::DT], float l_tot, float m_ref, bool has,
+                                            int hf) {
+  const float inv = has ? 1.0f / l_tot : 0.0f;
+#pragma unroll
+  for (int dt = 0; dt < Geo<D>::DT; ++dt)
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4) {
+      const int d = dt * 32 + r4 * 8 + hf * 4;
+      if (d < D) {
+        const float o0 = oacc[dt][r4 * 4 + 0] * inv, o1 = oacc[dt][r4 * 4 + 1] * inv;
+        const float o2 = oacc[dt][r4 * 4 + 2] * inv, o3 = oacc[dt][r4 * 4 + 3] * inv;
+        if constexpr (OUT_F32) {
+          *reinterpret_cast<float4*>(static_cast<float*>(out) + obase + d) = make_float4(o0, o1, o2, o3);
+        } else {
+          const bf16x2 x = cvt2(o0, o1), y = cvt2(o2, o3);
+          const bf16x4 o = {x[0], x[1], y[0], y[1]};
+          *reinterpret_cast<bf16x4*>(static_cast<uint16_t*>(out) + obase + d) = o;
+        }
+      }
+    }
+  if (lse && hf == 0) lse[lse_at] = has ? (m_ref + __log2f(l_tot)) * 0.69314718055994530942f : -INFINITY;
+}
+
+}  // namespace attn
+}  // namespace sva
