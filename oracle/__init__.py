@@ -10,7 +10,8 @@ norm"; Appendix A.2.2 lists fused QKNorm+RoPE in the LTX-2.3 stack) is in
 qknorm_rope.py with its own readings; feat_norm token pruning (Section 4.2.3;
 Appendix A.2.2 keeps 50% of video tokens by that score) in token_prune.py;
 8-bit attention (Section 4.2.4 points to the SageAttention series) in
-fp8_attention.py.
+fp8_attention.py; the first-order remainder of non-kept blocks (Section 4.2.2)
+in remainder.py.
 
 What the paper fixes (Section 4.2.2, "Sparse Attention"; Appendix A.2.2, the
 LTX-2.3 pipeline): attention over the spatiotemporal token set is replaced by a
@@ -51,8 +52,14 @@ Parity status per function:
   fp8_attention.fp8_block_sparse_attention
                               pinned (smoothing invariance, exactly representable
                                       inputs equal plain attention)
-  The paper's own routing rule and its Taylor remainder for non-kept blocks:
-                              parity unpinned (not defined in the paper's text).
+  remainder.block_moments     pinned (brute force over tokens, independent identity)
+  remainder.remainder_attention
+                              pinned to its reading (exact on constant-key blocks,
+                                      dense when all kept, constant values,
+                                      second-order error convergence)
+  The paper's own routing rule and its formula for the first-order remainder of
+  non-kept blocks: parity unpinned (neither is written out in the paper's text;
+  remainder.py implements a first-order expansion about the block means).
 """
 from .blocks import bf16_bits_to_f64, num_blocks, block_bounds, pool_blocks
 from .select import (block_scores, topk_count, select_topk, first_frame_blocks,

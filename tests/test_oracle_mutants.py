@@ -323,3 +323,58 @@ def test_fp8_mutant_is_caught(name, attr, fn, pins, monkeypatch):
     for pin in pins:
         with pytest.raises((AssertionError, ValueError)):
             pin()
+
+
+# ---- first-order remainder of dropped blocks ----
+import oracle.remainder as orem  # noqa: E402
+
+from . import test_oracle_remainder as TR  # noqa: E402
+
+
+def _moment_times_query_transposed(mom, qr):
+    return np.einsum("jde,nd->nje", mom, qr)
+
+
+def _no_first_order(mom, qr):
+    return np.zeros((qr.shape[0], mom.shape[0], mom.shape[1]))
+
+
+def _moment_sign_flipped(mom, qr):
+    return -np.einsum("jed,nd->nje", mom, qr)
+
+
+def _block_counts_ignored(count):
+    return np.zeros_like(count)
+
+
+def _moments_not_centred(k, v, block):
+    kbar, vbar, _ = _ORIG_BLOCK_MOMENTS(k, v, block)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    b = oblk.block_bounds(k.shape[-2], block)
+    m = np.stack([np.matmul(np.swapaxes(v[..., a:e, :], -1, -2), k[..., a:e, :]) for a, e in b], axis=-3)
+    return kbar, vbar, m
+
+
+_ORIG_BLOCK_MOMENTS = orem.block_moments
+
+REM_MUTANTS = [
+    ("moment applied transposed", "moment_times_query", _moment_times_query_transposed,
+     [lambda: TR.test_error_is_second_order(True), lambda: TR.test_error_is_second_order(False)]),
+    ("first-order term dropped", "moment_times_query", _no_first_order,
+     [lambda: TR.test_error_is_second_order(True), lambda: TR.test_error_is_second_order(False)]),
+    ("first-order term with the wrong sign", "moment_times_query", _moment_sign_flipped,
+     [lambda: TR.test_error_is_second_order(True)]),
+    ("dropped block counted as one token", "log_token_count", _block_counts_ignored,
+     [lambda: TR.test_constant_key_blocks_equal_dense(37, 8), lambda: TR.test_constant_key_blocks_equal_dense(9, 4)]),
+    ("moments about zero, not the block mean", "block_moments", _moments_not_centred,
+     [lambda: TR.test_moments_bruteforce_and_identity(), lambda: TR.test_constant_key_blocks_equal_dense(40, 8)]),
+]
+
+
+@pytest.mark.parametrize("name,attr,fn,pins", REM_MUTANTS, ids=[m[0] for m in REM_MUTANTS])
+def test_remainder_mutant_is_caught(name, attr, fn, pins, monkeypatch):
+    monkeypatch.setattr(orem, attr, fn)
+    for pin in pins:
+        with pytest.raises(AssertionError):
+            pin()
