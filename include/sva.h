@@ -188,6 +188,64 @@ int sva_sparse_attention(const sva_problem* prob, const void* q, const void* k,
 int sva_dense_attention(const sva_problem* prob, const void* q, const void* k,
                         const void* v, void* out, float* lse, void* stream);
 
+/* ---- First-order remainder of the dropped blocks (Section 4.2.2: the
+ * non-critical blocks are compensated by a first-order Taylor approximation
+ * instead of dropped; the paper gives no formula, so this is the reading
+ * implemented).  For query q of query block i and a key block j that row i
+ * does not keep (n_j valid tokens, block means qbar_i, kbar_j, vbar_j), every
+ * exp(c q.k_t) of the block is expanded to first order about the means:
+ *   exp(c q.k_t) ~ exp(c q.kbar_j) + exp(c qbar_i.kbar_j) c q.(k_t - kbar_j)
+ * so the block adds n_j exp(c q.kbar_j) to the row sum and
+ * n_j exp(c q.kbar_j) vbar_j + exp(c qbar_i.kbar_j) c M_j q to the numerator,
+ * with the block moment M_j[e][d] = sum_t V[t][e] (K[t][d] - kbar_j[d]).  A
+ * block is dropped for row i when no in-range entry of the row's list names
+ * it.  The result is exact where every key of a dropped block equals the
+ * block mean, equals dense attention when every block is kept, and otherwise
+ * differs from dense attention by second-order terms in the deviations of
+ * queries and keys from their block means.  Requires nB <= SVA_REMAINDER_MAX_BLOCKS. ---- */
+#define SVA_REMAINDER_MAX_BLOCKS 4096
+
+/* Device workspace that sva_sparse_attention_remainder needs, in bytes
+ * (about B*H*(N*D*4 + nB*D*D*4) + smaller parts; 5.7 GB for B=1, H=48,
+ * N=111600, D=128, S=128).  Host only. */
+int sva_remainder_workspace(const sva_problem* prob, size_t* bytes);
+
+/* The block means and moments of the remainder.
+ *   k, v     : bf16 [B, H, N, D] device
+ *   kbar     : bf16 [B, H, nB, D] device, written: mean of K over the block's
+ *              valid tokens (float32 sum, rounded once)
+ *   vbar     : bf16 [B, H, nB, D] device, written: the same for V
+ *   moments  : bf16 [B, H, nB, D, D] device, written: M_j[e][d] (d fastest),
+ *              from K - kbar rounded to bf16 (kbar in float32), products
+ *              accumulated in float32, rounded once
+ * All pointers 16-byte aligned. */
+int sva_block_moments(const sva_problem* prob, const void* k, const void* v, void* kbar,
+                      void* vbar, void* moments, void* stream);
+
+/* Attention over the kept blocks plus the first-order remainder of the dropped
+ * ones.  Arguments as for sva_sparse_attention, plus:
+ *   q_pool, k_pool : float32 [B, H, nB, D] device, the block means from
+ *                    sva_pool_blocks (or sva_qknorm_rope_pool); 16-byte aligned
+ *   workspace      : device memory of at least sva_remainder_workspace bytes,
+ *                    256-byte aligned, owned by the caller; its contents on
+ *                    entry do not matter and on return are unspecified
+ *   out, lse       : the compensated output and its log-sum-exp (lse may be
+ *                    NULL), written for every valid token
+ * Steps (all on `stream`): the kept blocks exactly with a float32 output into
+ * the workspace; the block moments; the weights exp(c qbar_i.kbar_j - r_i) of
+ * the dropped blocks with r_i = max_j c qbar_i.kbar_j; T_i = sum of those
+ * weights times M_j; then per query block an online softmax over the pooled
+ * keys of its dropped blocks (bf16 MFMA, weights n_j), plus exp(r_i) c T_i q,
+ * merged with the kept part and normalised once.  The reference of each row's
+ * softmax starts at max(LSE of the kept part, r_i), so the output is finite as
+ * long as a query's largest logit against the kept keys or a dropped block's
+ * mean key is within about 80 (natural-log units) of r_i. */
+int sva_sparse_attention_remainder(const sva_problem* prob, const void* q, const void* k,
+                                   const void* v, const float* q_pool, const float* k_pool,
+                                   const int32_t* kv_idx, const int32_t* kv_count, int32_t kmax,
+                                   void* workspace, size_t workspace_bytes, void* out, float* lse,
+                                   void* stream);
+
 /* ---- feat_norm token pruning (Section 4.2.3 token pruning; Appendix A.2.2
  * keeps 50% of the video tokens by the feat_norm saliency score in the LTX-2.3
  * refinement stage; the paper prints no formula, so this is the reading

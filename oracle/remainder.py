@@ -88,13 +88,15 @@ def dropped_blocks(kept_row, n_blocks: int):
     return [j for j in range(n_blocks) if j not in named]
 
 
-def remainder_attention(q, k, v, kept, block: int, scale: float, rows=None):
+def remainder_attention(q, k, v, kept, block: int, scale: float, rows=None, first_order: bool = True):
     """Attention over the kept blocks plus the first-order remainder of the
     dropped ones (the definition in the module docstring).
 
-    q, k, v : float64 [B, H, N, D]
-    kept    : kept[b][h][i] = iterable of KV block indices
-    rows    : optional iterable of (b, h, i); other query blocks stay NaN
+    q, k, v     : float64 [B, H, N, D]
+    kept        : kept[b][h][i] = iterable of KV block indices
+    rows        : optional iterable of (b, h, i); other query blocks stay NaN
+    first_order : False leaves out the c M_j q terms (zero order only), which
+                  gives the size of the first-order part as a difference
     returns (out float64 [B, H, N, D], lse float64 [B, H, N])
     """
     q = np.asarray(q, dtype=np.float64)
@@ -129,8 +131,9 @@ def remainder_attention(q, k, v, kept, block: int, scale: float, rows=None):
         den = wa.sum(axis=1) + wz.sum(axis=1)
         num = wa @ v[b, h, key_tok] + wz @ vbar[b, h, drop]
         # first-order values: sum_j wf[n, j] * c * M_j q_n
-        mq = moment_times_query(mom[b, h, drop], qr)           # [n, J, D]
-        num = num + scale * np.einsum("nj,nje->ne", wf, mq)
+        if first_order:
+            mq = moment_times_query(mom[b, h, drop], qr)       # [n, J, D]
+            num = num + scale * np.einsum("nj,nje->ne", wf, mq)
         out[b, h, qa:qb] = num / den[:, None]
         lse[b, h, qa:qb] = ref[:, 0] + np.log(den)
     return out, lse

@@ -11,7 +11,8 @@ from ._lib import (SvaError, Problem, SelectParams, RopeParams, load, problem, p
                    qknorm_rope_pool, select_blocks, sparse_attention, dense_attention,
                    status_string, LIB_PATH, Tokens, tokens, token_keep_count, token_select,
                    token_gather, token_scatter, token_select_workspace, Fp8Tensors, fp8_padded_len, fp8_code_dim,
-                   quantize_fp8, sparse_attention_fp8, dense_attention_fp8)
+                   quantize_fp8, sparse_attention_fp8, dense_attention_fp8, remainder_workspace,
+                   block_moments, sparse_attention_remainder)
 
 __all__ = [
     "workloads", "SvaError", "Problem", "SelectParams", "RopeParams", "load", "problem",
@@ -19,5 +20,6 @@ __all__ = [
     "pool_blocks", "qknorm_rope_pool", "select_blocks", "sparse_attention", "dense_attention",
     "status_string", "LIB_PATH", "Tokens", "tokens", "token_keep_count", "token_select",
     "token_gather", "token_scatter", "token_select_workspace", "Fp8Tensors", "fp8_padded_len", "fp8_code_dim",
-    "quantize_fp8", "sparse_attention_fp8", "dense_attention_fp8",
+    "quantize_fp8", "sparse_attention_fp8", "dense_attention_fp8", "remainder_workspace",
+    "block_moments", "sparse_attention_remainder",
 ]

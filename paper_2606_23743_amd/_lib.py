@@ -76,6 +76,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "sva_select_blocks": [P, S, vp, vp, ctypes.c_int32, vp, vp, vp, vp],
         "sva_sparse_attention": [P, vp, vp, vp, vp, vp, ctypes.c_int32, vp, vp, vp],
         "sva_dense_attention": [P, vp, vp, vp, vp, vp, vp],
+        "sva_remainder_workspace": [P, ctypes.POINTER(ctypes.c_size_t)],
+        "sva_block_moments": [P, vp, vp, vp, vp, vp, vp],
+        "sva_sparse_attention_remainder": [P, vp, vp, vp, vp, vp, vp, vp, ctypes.c_int32, vp,
+                                           ctypes.c_size_t, vp, vp, vp],
         "sva_token_keep_count": [ctypes.POINTER(Tokens), ctypes.c_double, i32p],
         "sva_token_select_workspace": [ctypes.POINTER(Tokens), ctypes.POINTER(ctypes.c_size_t)],
         "sva_token_select": [ctypes.POINTER(Tokens), ctypes.c_double, vp, vp, vp, vp, vp,
@@ -299,6 +303,67 @@ def sparse_attention(prob: Problem, q, k, v, kv_idx, kv_count, out=None, want_ls
     _check(load().sva_sparse_attention(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(kv_idx),
                                        _ptr(kv_count), int(kmax), _ptr(out), _ptr(lse), _stream(stream)),
            "sva_sparse_attention")
+    return out, lse
+
+
+def remainder_workspace(prob: Problem) -> int:
+    out = ctypes.c_size_t(0)
+    _check(load().sva_remainder_workspace(ctypes.byref(prob), ctypes.byref(out)), "sva_remainder_workspace")
+    return out.value
+
+
+def block_moments(prob: Problem, k, v, kbar=None, vbar=None, moments=None, stream=None) -> Tuple:
+    """sva_block_moments: (kbar bf16 [B, H, nB, D], vbar bf16 [B, H, nB, D],
+    moments bf16 [B, H, nB, D, D] with M[e][d] = sum_t V[t][e] (K[t][d] - kbar[d]))."""
+    torch = _torch()
+    nb = num_blocks(prob)
+    shp = _qkv_shape(prob)
+    B, H, _, D = shp
+    for t, n in ((k, "k"), (v, "v")):
+        _need(t, torch.bfloat16, shp, n)
+    if kbar is None:
+        kbar = torch.empty((B, H, nb, D), dtype=torch.bfloat16, device=k.device)
+    if vbar is None:
+        vbar = torch.empty((B, H, nb, D), dtype=torch.bfloat16, device=k.device)
+    if moments is None:
+        moments = torch.empty((B, H, nb, D, D), dtype=torch.bfloat16, device=k.device)
+    _need(kbar, torch.bfloat16, (B, H, nb, D), "kbar")
+    _need(vbar, torch.bfloat16, (B, H, nb, D), "vbar")
+    _need(moments, torch.bfloat16, (B, H, nb, D, D), "moments")
+    _check(load().sva_block_moments(ctypes.byref(prob), _ptr(k), _ptr(v), _ptr(kbar), _ptr(vbar), _ptr(moments),
+                                    _stream(stream)), "sva_block_moments")
+    return kbar, vbar, moments
+
+
+def sparse_attention_remainder(prob: Problem, q, k, v, q_pool, k_pool, kv_idx, kv_count, out=None,
+                               want_lse: bool = False, lse=None, workspace=None, stream=None) -> Tuple:
+    """sva_sparse_attention_remainder: the kept blocks exactly plus the
+    first-order remainder of the dropped ones.  workspace: a uint8 device
+    tensor of remainder_workspace bytes (allocated when None)."""
+    torch = _torch()
+    nb = num_blocks(prob)
+    shp = _qkv_shape(prob)
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        _need(t, torch.bfloat16, shp, n)
+    _need(q_pool, torch.float32, (prob.batch, prob.heads, nb, prob.head_dim), "q_pool")
+    _need(k_pool, torch.float32, (prob.batch, prob.heads, nb, prob.head_dim), "k_pool")
+    kmax = kv_idx.shape[-1]
+    _need(kv_idx, torch.int32, (prob.batch, prob.heads, nb, kmax), "kv_idx")
+    _need(kv_count, torch.int32, (prob.batch, prob.heads, nb), "kv_count")
+    out = _out_tensor(prob, q, out)
+    if want_lse and lse is None:
+        lse = torch.empty(shp[:3], dtype=torch.float32, device=q.device)
+    if lse is not None:
+        _need(lse, torch.float32, shp[:3], "lse")
+    ws_bytes = remainder_workspace(prob)
+    if workspace is None:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
+    if workspace.dtype != torch.uint8 or not workspace.is_cuda or workspace.numel() < ws_bytes:
+        raise ValueError(f"workspace must be a uint8 device tensor of at least {ws_bytes} bytes")
+    _check(load().sva_sparse_attention_remainder(
+        ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(q_pool), _ptr(k_pool), _ptr(kv_idx), _ptr(kv_count),
+        int(kmax), _ptr(workspace), int(workspace.numel()), _ptr(out), _ptr(lse), _stream(stream)),
+        "sva_sparse_attention_remainder")
     return out, lse
 
 

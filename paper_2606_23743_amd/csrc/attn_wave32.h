@@ -94,22 +94,48 @@ __device__ __forceinline__ void load_chunk(const ChunkLoader<D, NUW, CT>& f, int
   load_tile<false>(f, st, key0);
 }
 
-// Per-lane LDS offsets.  K operand, step s: row l32 of the tile, piece
-// 2s + hf.  V transpose reads: row (kk*16 + hf*4 + n16/4 [+8]), piece
+// Per-lane LDS offset of the transpose reads of column tile dt (columns
+// dt*32 ..) of a V-swizzled tile: row (kk*16 + hf*4 + n16/4 [+8]), piece
 // dt*4 + (g16&1)*2 + (n16&3)/2; only dt interacts with the swizzle.  The
 // stage and the kk / +8 row offsets are immediates.
 template <int D>
+__device__ __forceinline__ int tr_offset(int lane, int dt) {
+  using G = Geo<D>;
+  const int hf = lane >> 5, g16 = lane >> 4, n16 = lane & 15;
+  const int vr = hf * 4 + (n16 >> 2);
+  const int c = dt * 4 + (g16 & 1) * 2 + ((n16 & 3) >> 1);
+  return vr * G::RB + (swz_v<G::NCH>(vr, c) << 4) + (n16 & 1) * 8;
+}
+
+// Per-lane LDS offsets.  K operand, step s: row l32 of the tile, piece
+// 2s + hf.  V transpose reads: tr_offset.
+template <int D>
 __device__ __forceinline__ void operand_offsets(int lane, int (&koff)[Geo<D>::DQ], int (&voff)[Geo<D>::DT]) {
   using G = Geo<D>;
-  const int hf = lane >> 5, l32 = lane & 31, g16 = lane >> 4, n16 = lane & 15;
+  const int hf = lane >> 5, l32 = lane & 31;
 #pragma unroll
   for (int s = 0; s < G::DQ; ++s) koff[s] = l32 * G::RB + (swz_k<G::NCH>(l32, 2 * s + hf) << 4);
-  const int vr = hf * 4 + (n16 >> 2);
 #pragma unroll
-  for (int dt = 0; dt < G::DT; ++dt) {
-    const int c = dt * 4 + (g16 & 1) * 2 + ((n16 & 3) >> 1);
-    voff[dt] = vr * G::RB + (swz_v<G::NCH>(vr, c) << 4) + (n16 & 1) * 8;
-  }
+  for (int dt = 0; dt < G::DT; ++dt) voff[dt] = tr_offset<D>(lane, dt);
+}
+
+// Transpose read of a V-swizzled [32 rows][RB] tile: lane l gets column
+// dt*32 + l%32 (through voff = tr_offset(lane, dt)) at the 8 rows of key half
+// kk in the order of a softmax_chunk register group (rows kk*16 + hf*4 + 0..3,
+// then kk*16 + 8 + hf*4 + 0..3).  The same register serves as the A operand
+// (row m = the column) or the B operand (column n = the column) of an MFMA
+// whose contraction runs over the tile's rows.
+template <int D>
+__device__ __forceinline__ bf16x8 tr_operand(const unsigned char* tile, int voff, int kk) {
+  using G = Geo<D>;
+  // rows r and r + 8 have the same swizzle, so one offset serves both
+  const unsigned char* p = tile + voff + kk * 16 * G::RB;
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p));
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 8 * G::RB));
+  const u32x2 lw = __builtin_bit_cast(u32x2, lo);
+  const u32x2 hw = __builtin_bit_cast(u32x2, hi);
+  const u32x4 vw = {lw[0], lw[1], hw[0], hw[1]};
+  return __builtin_bit_cast(bf16x8, vw);
 }
 
 // Q^T operand of query qr: d = s*16 + hf*8 + 0..7 (zero when the query is absent)
@@ -175,21 +201,11 @@ __device__ __forceinline__ void softmax_chunk(const f32x16& sacc, bf16x8 (&pop)[
 template <int D>
 __device__ __forceinline__ void pv_chunk(const bf16x8 (&pop)[2], const unsigned char* vt, const int (&voff)[Geo<D>::DT],
                                          f32x16 (&oacc)[Geo<D>::DT]) {
-  using G = Geo<D>;
 #pragma unroll
-  for (int dt = 0; dt < G::DT; ++dt) {
+  for (int dt = 0; dt < Geo<D>::DT; ++dt)
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      // rows r and r + 8 have the same swizzle, so one offset serves both
-      const unsigned char* p = vt + voff[dt] + kk * 16 * G::RB;
-      const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p));
-      const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 8 * G::RB));
-      const u32x2 lw = __builtin_bit_cast(u32x2, lo);
-      const u32x2 hw = __builtin_bit_cast(u32x2, hi);
-      const u32x4 vw = {lw[0], lw[1], hw[0], hw[1]};
-      oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vw), pop[kk], oacc[dt], 0, 0, 0);
-    }
-  }
+    for (int kk = 0; kk < 2; ++kk)
+      oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand<D>(vt, voff[dt], kk), pop[kk], oacc[dt], 0, 0, 0);
 }
 
 // After every kept block: if a row sum has grown past 2^64 (the reference

@@ -1,0 +1,568 @@
+// First-order remainder of the key blocks a query block does not keep
+// (Section 4.2.2: the non-critical blocks are compensated to first order
+// instead of dropped).
+//
+// For query q of query block i and a dropped key block j (n_j valid tokens,
+// means kbar_j and vbar_j, moment M_j[e][d] = sum_t v_t[e] (k_t - kbar_j)[d]),
+// the block's exponentials are expanded to first order about the block means:
+//   row sum    += n_j exp(c q.kbar_j)
+//   numerator  += n_j exp(c q.kbar_j) vbar_j + exp(c qbar_i.kbar_j) c M_j q
+// on top of the exact sums over the kept keys.  Four kernels:
+//   rem_moments_kernel  one workgroup per key block: kbar, vbar (bf16) and M
+//                       (bf16, [e][d]) as V^T (K - kbar) on MFMA, both
+//                       operands by transpose reads of LDS tiles
+//   rem_weights_kernel  per query block i: r_i = max_j c qbar_i.kbar_j and
+//                       E[i][j] = exp(c qbar_i.kbar_j - r_i) for the dropped j,
+//                       0 for kept and padding columns (bf16)
+//   rem_gemm_kernel     T_i = sum_j E[i][j] M_j: per head one GEMM of E
+//                       [nB x nB] with the flattened moments [nB x D*D] (MFMA,
+//                       M tiles staged in LDS by direct loads, E from global)
+//   rem_attn_kernel     per query block: an online softmax over the nB pooled
+//                       keys kbar_j with weight n_j (kept and padding blocks
+//                       masked), values vbar_j; then exp(r_i) c T_i q, and the
+//                       merge with the kept-block result (float32 O and LSE)
+#include "attn_wave32.h"
+
+namespace sva {
+namespace {
+
+using namespace attn;
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.69314718055994530942f;
+
+__device__ __forceinline__ uint16_t bf16_bits(float x) { return __builtin_bit_cast(uint16_t, (__bf16)x); }
+
+// ---------------------------------------------------------------------------
+// Block means and moments.  One workgroup (4 waves) per (b, h, key block j);
+// rows j >= nB (padding up to `rows`) are written as zeros.  The block's K and
+// V are staged as 32-row V-swizzled tiles; K is replaced in place by K - kbar
+// (rows past the block's end stay zero).  M = V^T (K - kbar): the A operand is
+// the transpose read of the V tile at column tile et, the B operand the same
+// read of the centred K tile at column tile dt, so M[e][d] lands with d along
+// the lanes.  Wave w takes the (et, dt) tiles with (et*DT + dt) % 4 == w.
+// ---------------------------------------------------------------------------
+template <int D, int S>
+__global__ __launch_bounds__(256) void rem_moments_kernel(RemMomentArgs a) {
+  using G = Geo<D>;
+  constexpr int NT = 256;
+  constexpr int NCHK = S / 32;               // 32-row tiles per block
+  constexpr int CT = 32 * G::RB;
+  constexpr int PIECES = S * G::DCH;         // 16-byte pieces of one tensor's block
+  constexpr int TILES = G::DT * G::DT;
+  constexpr int TPW = (TILES + 3) / 4;       // output tiles per wave
+  __shared__ __attribute__((aligned(1024))) unsigned char Kt[NCHK][CT];
+  __shared__ __attribute__((aligned(1024))) unsigned char Vt[NCHK][CT];
+  __shared__ float kmean[D];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int hf = lane >> 5, l32 = lane & 31;
+  const int item = blockIdx.x;               // bh * rows + j
+  const int bh = item / a.rows;
+  const int j = item - bh * a.rows;
+  const size_t dd = (size_t)D * D;
+  uint16_t* kbar = a.kbar + (size_t)item * D;
+  uint16_t* vbar = a.vbar + (size_t)item * D;
+  uint16_t* mom = a.mom + (size_t)item * dd;
+  if (j >= a.nB) {
+    for (int t = tid; t < D; t += NT) {
+      kbar[t] = 0;
+      vbar[t] = 0;
+    }
+    for (int t = tid; t < (int)(dd / 8); t += NT) reinterpret_cast<uint4*>(mom)[t] = make_uint4(0, 0, 0, 0);
+    return;
+  }
+  const int t0 = j * S;
+  const int n = min(S, a.N - t0);
+  const uint16_t* Kb = a.k + ((size_t)bh * a.N + t0) * D;
+  const uint16_t* Vb = a.v + ((size_t)bh * a.N + t0) * D;
+  auto tile_off = [](int t, int c) { return (t >> 5) * CT + (t & 31) * G::RB + (swz_v<G::NCH>(t & 31, c) << 4); };
+
+  for (int p = tid; p < PIECES; p += NT) {
+    const int t = p / G::DCH, c = p - (p / G::DCH) * G::DCH;
+    uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
+    if (t < n) {
+      kv = *reinterpret_cast<const uint4*>(Kb + (size_t)t * D + c * 8);
+      vv = *reinterpret_cast<const uint4*>(Vb + (size_t)t * D + c * 8);
+    }
+    *reinterpret_cast<uint4*>(&Kt[0][0] + tile_off(t, c)) = kv;
+    *reinterpret_cast<uint4*>(&Vt[0][0] + tile_off(t, c)) = vv;
+  }
+  __syncthreads();
+
+  // means over the valid tokens, float32; threads 0..D-1 take K, D..2D-1 V
+  if (tid < 2 * D) {
+    const bool isk = tid < D;
+    const int d = isk ? tid : tid - D;
+    const unsigned char* base = isk ? &Kt[0][0] : &Vt[0][0];
+    float s = 0.0f;
+    for (int t = 0; t < n; ++t) {
+      const uint16_t x = *reinterpret_cast<const uint16_t*>(base + tile_off(t, d >> 3) + (d & 7) * 2);
+      s += __uint_as_float((unsigned)x << 16);
+    }
+    s /= (float)n;
+    if (isk) {
+      kmean[d] = s;
+      kbar[d] = bf16_bits(s);
+    } else {
+      vbar[d] = bf16_bits(s);
+    }
+  }
+  __syncthreads();
+
+  // K - kbar in place, rounded to bf16 (rows past the block's end stay zero)
+  for (int p = tid; p < PIECES; p += NT) {
+    const int t = p / G::DCH, c = p - (p / G::DCH) * G::DCH;
+    if (t >= n) continue;
+    uint4* slot = reinterpret_cast<uint4*>(&Kt[0][0] + tile_off(t, c));
+    const bf16x8 x = __builtin_bit_cast(bf16x8, *slot);
+    u32x4 y;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float a0 = (float)x[2 * e] - kmean[c * 8 + 2 * e];
+      const float a1 = (float)x[2 * e + 1] - kmean[c * 8 + 2 * e + 1];
+      y[e] = __builtin_bit_cast(unsigned, cvt2(a0, a1));
+    }
+    *slot = __builtin_bit_cast(uint4, y);
+  }
+  __syncthreads();
+
+  f32x16 acc[TPW];
+#pragma unroll
+  for (int x = 0; x < TPW; ++x) acc[x] = f32x16{};
+#pragma unroll
+  for (int x = 0; x < TPW; ++x) {
+    const int tile = w + 4 * x;
+    if (tile < TILES) {
+      const int et = tile / G::DT, dt = tile - (tile / G::DT) * G::DT;
+      const int ea = tr_offset<D>(lane, et), db = tr_offset<D>(lane, dt);
+#pragma unroll
+      for (int ch = 0; ch < NCHK; ++ch)
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+          acc[x] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand<D>(&Vt[ch][0], ea, kk),
+                                                           tr_operand<D>(&Kt[ch][0], db, kk), acc[x], 0, 0, 0);
+    }
+  }
+#pragma unroll
+  for (int x = 0; x < TPW; ++x) {
+    const int tile = w + 4 * x;
+    if (tile < TILES) {
+      const int et = tile / G::DT, dt = tile - (tile / G::DT) * G::DT;
+      const int d = dt * 32 + l32;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int e = et * 32 + (r >> 2) * 8 + hf * 4 + (r & 3);
+        if (e < D && d < D) mom[(size_t)e * D + d] = bf16_bits(acc[x][r]);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// First-order weights.  kRemRows query blocks of one head per workgroup: the
+// kept sets as LDS bitmaps, then two passes over the key blocks (row maxima,
+// then the weights), each thread taking key blocks tid, tid + 256, ...
+// ---------------------------------------------------------------------------
+constexpr int kRemRows = 8;
+
+template <int D>
+__global__ __launch_bounds__(256) void rem_weights_kernel(RemWeightArgs a) {
+  constexpr int NT = 256;
+  constexpr int kWords = kRemMaxBlocks / 32;
+  __shared__ float qs[kRemRows][D];
+  __shared__ uint32_t bm[kRemRows][kWords];
+  __shared__ float red[kRemRows][4];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int nB = a.nB, nBp = a.nBp;
+  const int groups = (nB + kRemRows - 1) / kRemRows;
+  const int bh = blockIdx.x / groups;
+  const int i0 = (blockIdx.x - bh * groups) * kRemRows;
+  for (int t = tid; t < kRemRows * D; t += NT) {
+    const int ri = t / D, d = t - (t / D) * D;
+    qs[ri][d] = i0 + ri < nB ? a.q_pool[((size_t)bh * nB + i0 + ri) * D + d] : 0.0f;
+  }
+  for (int t = tid; t < kRemRows * kWords; t += NT) (&bm[0][0])[t] = 0u;
+  __syncthreads();
+  for (int ri = 0; ri < kRemRows && i0 + ri < nB; ++ri) {
+    const int row = bh * nB + i0 + ri;
+    const int cnt = min(max(a.kv_count[row], 0), a.kmax);
+    const int32_t* idx = a.kv_idx + (size_t)row * a.kmax;
+    for (int t = tid; t < cnt; t += NT) {
+      const int j = idx[t];
+      if (j >= 0 && j < nB) atomicOr(&bm[ri][j >> 5], 1u << (j & 31));
+    }
+  }
+  __syncthreads();
+
+  const float c = a.scale;
+  const float* kp = a.k_pool + (size_t)bh * nB * D;
+  auto scores = [&](int j, float (&s)[kRemRows]) {
+#pragma unroll
+    for (int ri = 0; ri < kRemRows; ++ri) s[ri] = 0.0f;
+    const float4* kr = reinterpret_cast<const float4*>(kp + (size_t)j * D);
+    for (int d4 = 0; d4 < D / 4; ++d4) {
+      const float4 kv = kr[d4];
+#pragma unroll
+      for (int ri = 0; ri < kRemRows; ++ri) {
+        s[ri] = fmaf(qs[ri][4 * d4 + 0], kv.x, s[ri]);
+        s[ri] = fmaf(qs[ri][4 * d4 + 1], kv.y, s[ri]);
+        s[ri] = fmaf(qs[ri][4 * d4 + 2], kv.z, s[ri]);
+        s[ri] = fmaf(qs[ri][4 * d4 + 3], kv.w, s[ri]);
+      }
+    }
+#pragma unroll
+    for (int ri = 0; ri < kRemRows; ++ri) s[ri] *= c;
+  };
+
+  float mx[kRemRows];
+#pragma unroll
+  for (int ri = 0; ri < kRemRows; ++ri) mx[ri] = -INFINITY;
+  for (int j = tid; j < nB; j += NT) {
+    float s[kRemRows];
+    scores(j, s);
+#pragma unroll
+    for (int ri = 0; ri < kRemRows; ++ri) mx[ri] = fmaxf(mx[ri], s[ri]);
+  }
+#pragma unroll
+  for (int ri = 0; ri < kRemRows; ++ri) {
+    float m = mx[ri];
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
+    if (lane == 0) red[ri][w] = m;
+  }
+  __syncthreads();
+  float rmax[kRemRows];
+#pragma unroll
+  for (int ri = 0; ri < kRemRows; ++ri) rmax[ri] = fmaxf(fmaxf(red[ri][0], red[ri][1]), fmaxf(red[ri][2], red[ri][3]));
+  if (tid < kRemRows && i0 + tid < nB) {
+    float rv = rmax[0];
+#pragma unroll
+    for (int ri = 1; ri < kRemRows; ++ri)
+      if (ri == tid) rv = rmax[ri];
+    a.r[(size_t)bh * nBp + i0 + tid] = rv;
+  }
+
+  for (int j = tid; j < nBp; j += NT) {
+    float s[kRemRows] = {};
+    if (j < nB) scores(j, s);
+#pragma unroll
+    for (int ri = 0; ri < kRemRows; ++ri) {
+      if (i0 + ri >= nB) break;
+      const bool kept = j >= nB || ((bm[ri][j >> 5] >> (j & 31)) & 1u);
+      const float e = kept ? 0.0f : exp2f((s[ri] - rmax[ri]) * kLog2e);
+      a.E[((size_t)bh * nBp + i0 + ri) * nBp + j] = bf16_bits(e);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// T_i = sum_j E[i][j] M_j, per head: C [nB x D*D] = E [nB x nBp] . M [nBp x D*D].
+// A workgroup takes 128 columns (one LDS tile row of 256 bytes) and 128 rows
+// i (32 per wave); per 32-row chunk of M the tile is staged by direct loads
+// (double-buffered) and each wave accumulates T^T += M_tile^T E^T with the
+// PV step of the attention kernels (the E values take the place of P).
+// Workgroups of one column tile are consecutive in XCD order, so the M tile
+// they share is fetched into one L2.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void rem_gemm_kernel(RemGemmArgs a) {
+  using G = Geo<128>;
+  constexpr int CT = 32 * G::RB;             // 32 rows x 128 columns of bf16
+  constexpr int NUW = CT / 1024 / 4;         // direct-load pieces per wave
+  __shared__ __attribute__((aligned(1024))) unsigned char Ms[2][CT];
+
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int hf = lane >> 5, l32 = lane & 31;
+  const int DD = a.DD, nB = a.nB, nBp = a.nBp;
+  const int nct = DD / 128, nrg = (nB + 127) / 128;
+  const int id = __builtin_amdgcn_readfirstlane(xcd_remap(blockIdx.x, a.n_wg));
+  const int rg = id % nrg;
+  const int tt = id / nrg;
+  const int ct = tt % nct;
+  const int bh = tt / nct;
+  const int c0 = ct * 128;
+  const int i = rg * 128 + w * 32 + l32;
+  const bool live = i < nB;
+  const uint16_t* Mh = a.mom + (size_t)bh * nBp * DD;
+  const uint16_t* Er = a.E + ((size_t)bh * nBp + (live ? i : 0)) * nBp;
+
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc((void*)Mh, (short)0, nBp * DD * 2, 0x00020000);
+  int mv[NUW];
+#pragma unroll
+  for (int v = 0; v < NUW; ++v) {
+    const int r = (w * NUW + v) * G::RPI + lane / G::NCH;
+    const int c = swz_v<G::NCH>(r, lane % G::NCH);
+    mv[v] = (r * DD + c0 + c * 8) * 2;
+  }
+  const unsigned ms_base = __builtin_amdgcn_readfirstlane((unsigned)(size_t)(const lds_u8*)&Ms[0][0]);
+  auto load_m = [&](int st, int j0) {
+#pragma unroll
+    for (int v = 0; v < NUW; ++v) buffer_to_lds(rs, ms_base + st * CT + (w * NUW + v) * 1024, mv[v], j0 * DD * 2);
+  };
+  // E values of row i in the order of a softmax_chunk register group
+  auto load_e = [&](bf16x8 (&e)[2], int j0) {
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      if (live) {
+        const uint16_t* p = Er + j0 + kk * 16 + hf * 4;
+        const u32x2 lo = *reinterpret_cast<const u32x2*>(p);
+        const u32x2 hi = *reinterpret_cast<const u32x2*>(p + 8);
+        const u32x4 x = {lo[0], lo[1], hi[0], hi[1]};
+        e[kk] = __builtin_bit_cast(bf16x8, x);
+      } else {
+        e[kk] = bf16x8{};
+      }
+    }
+  };
+
+  int koff[G::DQ], voff[G::DT];
+  operand_offsets<128>(lane, koff, voff);
+  f32x16 acc[G::DT];
+#pragma unroll
+  for (int dt = 0; dt < G::DT; ++dt) acc[dt] = f32x16{};
+  const int nch = nBp / 32;
+  bf16x8 ecur[2], enext[2] = {bf16x8{}, bf16x8{}};
+  load_m(0, 0);
+  load_e(ecur, 0);
+  for (int ch = 0; ch < nch; ++ch) {
+    wait_vmcnt_lds_idle<0>();                // this wave's loads of chunk ch landed
+    wg_barrier();                            // every wave's; chunk ch-1's stage is free
+    if (ch + 1 < nch) {
+      load_m((ch + 1) & 1, (ch + 1) * 32);
+      load_e(enext, (ch + 1) * 32);
+    }
+    pv_chunk<128>(ecur, &Ms[ch & 1][0], voff, acc);
+    ecur[0] = enext[0];
+    ecur[1] = enext[1];
+  }
+  wait_vmcnt<0>();
+  if (live) {
+    uint16_t* Tr = a.T + ((size_t)bh * nBp + i) * DD + c0;
+#pragma unroll
+    for (int dt = 0; dt < G::DT; ++dt)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int col = dt * 32 + r4 * 8 + hf * 4;
+        const bf16x2 x = cvt2(acc[dt][r4 * 4 + 0], acc[dt][r4 * 4 + 1]);
+        const bf16x2 y = cvt2(acc[dt][r4 * 4 + 2], acc[dt][r4 * 4 + 3]);
+        const bf16x4 o = {x[0], x[1], y[0], y[1]};
+        *reinterpret_cast<bf16x4*>(Tr + col) = o;
+      }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Remainder attention and merge.  One workgroup (S/32 waves of 32 queries) per
+// query block, as the 32-query sparse kernel.  The pooled keys kbar_j of the
+// head are walked in 32-row chunks (double-buffered direct loads): S^T = Kbar
+// Q^T, logit + log2 n_j in log2 units (-inf for kept and padding blocks), P
+// rounded to bf16 with l summed from it, O^T += Vbar^T P^T.  The reference
+// starts at max(LSE of the kept part, r_i) (log2 units) and moves up only
+// when a chunk's maximum passes it by more than 8, so it is rarely moved.  At
+// the end the first-order term exp(r_i) c T_i q is one MFMA pass with T_i rows
+// from global memory and Q^T from registers, and the kept-block result (O and
+// LSE in float32) is added with its weight exp(LSE) before the division.
+// ---------------------------------------------------------------------------
+template <int D, int S, bool OUT_F32>
+__global__ __launch_bounds__(2 * S) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void rem_attn_kernel(RemAttnArgs a) {
+  using G = Geo<D>;
+  constexpr int NW = S / 32;
+  constexpr int CT = 32 * G::RB;
+  constexpr int NUW = CT / 1024 / NW;
+  constexpr int kWords = kRemMaxBlocks / 32;
+  static_assert(NUW >= 1, "tile split");
+  __shared__ __attribute__((aligned(1024))) unsigned char Ks[2][CT];
+  __shared__ __attribute__((aligned(1024))) unsigned char Vs[2][CT];
+  __shared__ uint32_t bm[kWords];
+
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int hf = lane >> 5, l32 = lane & 31;
+  const int N = a.N, nB = a.nB, nBp = a.nBp;
+  const int row = __builtin_amdgcn_readfirstlane(xcd_remap(blockIdx.x, a.n_rows));
+  const int bh = row / nB;
+  const int i = row - bh * nB;
+
+  for (int t = threadIdx.x; t < nBp / 32; t += 2 * S) bm[t] = 0u;
+  __syncthreads();
+  {
+    const int cnt = min(max(a.kv_count[row], 0), a.kmax);
+    const int32_t* idx = a.kv_idx + (size_t)row * a.kmax;
+    for (int t = threadIdx.x; t < cnt; t += 2 * S) {
+      const int j = idx[t];
+      if (j >= 0 && j < nB) atomicOr(&bm[j >> 5], 1u << (j & 31));
+    }
+  }
+  __syncthreads();
+
+  const int qr = i * S + w * 32 + l32;
+  const bool present = qr < N;
+  bf16x8 qop[G::DQ];
+  load_q<D>(qop, a.q + (size_t)bh * N * D, qr, present, hf);
+
+  ChunkLoader<D, NUW, CT> ld;
+  loader_init(ld, a.kbar + (size_t)bh * nBp * D, a.vbar + (size_t)bh * nBp * D, nBp, &Ks[0][0], &Vs[0][0], w,
+              lane);
+  int koff[G::DQ], voff[G::DT];
+  operand_offsets<D>(lane, koff, voff);
+
+  const float sl2 = a.scale_log2;
+  const float r2 = a.r[(size_t)bh * nBp + i] * kLog2e;   // block-score maximum, log2 units
+  const float lse_a = present ? a.lse_a[(size_t)bh * N + qr] : -INFINITY;
+  float m_ref = fmaxf(lse_a * kLog2e, r2);
+  float l_part = 0.0f;
+  f32x16 oacc[G::DT];
+#pragma unroll
+  for (int dt = 0; dt < G::DT; ++dt) oacc[dt] = f32x16{};
+  const float log2_s = S == 128 ? 7.0f : 6.0f;
+  const float log2_last = __log2f((float)(N - (nB - 1) * S));
+
+  const int nch = nBp / 32;
+  load_chunk(ld, 0, 0);
+  for (int ch = 0; ch < nch; ++ch) {
+    wait_vmcnt_lds_idle<0>();
+    wg_barrier();
+    if (ch + 1 < nch) load_chunk(ld, (ch + 1) & 1, (ch + 1) * 32);
+    const uint32_t word = bm[ch];
+    f32x16 sacc;
+    qk_chunk<D>(sacc, &Ks[ch & 1][0], koff, qop);
+    float mx = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int jj = (r >> 2) * 8 + hf * 4 + (r & 3);
+      const int j = ch * 32 + jj;
+      const bool off = j >= nB || ((word >> jj) & 1u);
+      sacc[r] = off ? -INFINITY : __builtin_fmaf(sacc[r], sl2, j == nB - 1 ? log2_last : log2_s);
+      mx = fmaxf(mx, sacc[r]);
+    }
+    mx = swap_halves_max(mx);
+    if (__builtin_amdgcn_ballot_w64(mx > m_ref + 8.0f) != 0) {
+      if (mx > m_ref + 8.0f) {
+        const float f = __builtin_amdgcn_exp2f(m_ref - mx);
+        l_part *= f;
+#pragma unroll
+        for (int dt = 0; dt < G::DT; ++dt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[dt][r] *= f;
+        m_ref = mx;
+      }
+    }
+    bf16x8 pop[2];
+    softmax_chunk(sacc, pop, l_part, m_ref, 1.0f);
+    pv_chunk<D>(pop, &Vs[ch & 1][0], voff, oacc);
+  }
+  wait_vmcnt<0>();
+
+  // first-order term: oacc += c exp2(r2 - m_ref) (T_i q), T_i rows e from global
+  const uint16_t* Ti = a.T + ((size_t)bh * nBp + i) * D * D;
+  const float f1 = a.scale * __builtin_amdgcn_exp2f(r2 - m_ref);
+#pragma unroll
+  for (int dt = 0; dt < G::DT; ++dt) {
+    const int e = dt * 32 + l32;
+    f32x16 tacc = f32x16{};
+#pragma unroll
+    for (int s = 0; s < G::DQ; ++s) {
+      const bf16x8 top = e < D ? *reinterpret_cast<const bf16x8*>(Ti + (size_t)e * D + s * 16 + hf * 8) : bf16x8{};
+      tacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(top, qop[s], tacc, 0, 0, 0);
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[dt][r] = __builtin_fmaf(f1, tacc[r], oacc[dt][r]);
+  }
+
+  // merge with the kept-block result and normalise
+  const float l_tot = swap_halves_sum(l_part);
+  const float l_a = __builtin_amdgcn_exp2f(lse_a * kLog2e - m_ref);
+  const float den = l_tot + l_a;
+  const float inv = 1.0f / den;
+  if (!present) return;
+  const size_t obase = ((size_t)bh * N + qr) * D;
+#pragma unroll
+  for (int dt = 0; dt < G::DT; ++dt)
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4) {
+      const int d = dt * 32 + r4 * 8 + hf * 4;
+      if (d < D) {
+        const float4 oa = *reinterpret_cast<const float4*>(a.o_a + obase + d);
+        const float o0 = __builtin_fmaf(l_a, oa.x, oacc[dt][r4 * 4 + 0]) * inv;
+        const float o1 = __builtin_fmaf(l_a, oa.y, oacc[dt][r4 * 4 + 1]) * inv;
+        const float o2 = __builtin_fmaf(l_a, oa.z, oacc[dt][r4 * 4 + 2]) * inv;
+        const float o3 = __builtin_fmaf(l_a, oa.w, oacc[dt][r4 * 4 + 3]) * inv;
+        if constexpr (OUT_F32) {
+          *reinterpret_cast<float4*>(static_cast<float*>(a.out) + obase + d) = make_float4(o0, o1, o2, o3);
+        } else {
+          const bf16x2 x = cvt2(o0, o1), y = cvt2(o2, o3);
+          const bf16x4 o = {x[0], x[1], y[0], y[1]};
+          *reinterpret_cast<bf16x4*>(static_cast<uint16_t*>(a.out) + obase + d) = o;
+        }
+      }
+    }
+  if (a.lse && hf == 0) a.lse[(size_t)bh * N + qr] = (m_ref + __log2f(den)) * kLn2;
+}
+
+template <int D, int S>
+hipError_t launch_moments_ds(const Dims& d, const RemMomentArgs& a, hipStream_t stream) {
+  const int n = d.B * d.H * a.rows;
+  hipLaunchKernelGGL((rem_moments_kernel<D, S>), dim3(n), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+template <int D, int S>
+hipError_t launch_rem_attn_ds(const Dims& d, const RemAttnArgs& a, hipStream_t stream) {
+  dim3 grid(a.n_rows), block(2 * S);
+  if (d.out_f32) hipLaunchKernelGGL((rem_attn_kernel<D, S, true>), grid, block, 0, stream, a);
+  else hipLaunchKernelGGL((rem_attn_kernel<D, S, false>), grid, block, 0, stream, a);
+  return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_weights_d(const Dims& d, const RemWeightArgs& a, hipStream_t stream) {
+  const int n = d.B * d.H * ((d.nB + kRemRows - 1) / kRemRows);
+  hipLaunchKernelGGL((rem_weights_kernel<D>), dim3(n), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int rem_padded_blocks(int nB) { return (nB + 31) / 32 * 32; }
+
+hipError_t launch_block_moments(const Dims& d, const RemMomentArgs& a, hipStream_t stream) {
+  switch (d.D * 1000 + d.S) {
+    case 64128: return launch_moments_ds<64, 128>(d, a, stream);
+    case 112128: return launch_moments_ds<112, 128>(d, a, stream);
+    case 128128: return launch_moments_ds<128, 128>(d, a, stream);
+    case 64064: return launch_moments_ds<64, 64>(d, a, stream);
+    case 112064: return launch_moments_ds<112, 64>(d, a, stream);
+    case 128064: return launch_moments_ds<128, 64>(d, a, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_remainder(const Dims& d, const RemWeightArgs& wa, const RemGemmArgs& ga, const RemAttnArgs& aa,
+                            hipStream_t stream) {
+  hipError_t e;
+  switch (d.D) {
+    case 64: e = launch_weights_d<64>(d, wa, stream); break;
+    case 112: e = launch_weights_d<112>(d, wa, stream); break;
+    case 128: e = launch_weights_d<128>(d, wa, stream); break;
+    default: return hipErrorInvalidValue;
+  }
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(rem_gemm_kernel, dim3(ga.n_wg), dim3(256), 0, stream, ga);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  switch (d.D * 1000 + d.S) {
+    case 64128: return launch_rem_attn_ds<64, 128>(d, aa, stream);
+    case 112128: return launch_rem_attn_ds<112, 128>(d, aa, stream);
+    case 128128: return launch_rem_attn_ds<128, 128>(d, aa, stream);
+    case 64064: return launch_rem_attn_ds<64, 64>(d, aa, stream);
+    case 112064: return launch_rem_attn_ds<112, 64>(d, aa, stream);
+    case 128064: return launch_rem_attn_ds<128, 64>(d, aa, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace sva

@@ -99,6 +99,43 @@ int check_select(const sva_select_params* s, const Dims& d, SelectRule* r) {
 
 int hip_status(hipError_t e) { return e == hipSuccess ? SVA_OK : SVA_ERR_HIP; }
 
+static_assert(sva::kRemMaxBlocks == SVA_REMAINDER_MAX_BLOCKS, "remainder block limit");
+
+// Byte offsets of the remainder workspace's parts, each 256-byte aligned.
+struct RemLayout {
+  size_t oa, lsea, kbar, vbar, mom, E, r, T, total;
+};
+
+RemLayout rem_layout(const Dims& d) {
+  const size_t bh = (size_t)d.B * d.H, N = d.N, D = d.D;
+  const size_t nbp = (size_t)sva::rem_padded_blocks(d.nB);
+  auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  RemLayout L{};
+  size_t off = 0;
+  L.oa = off;   off += up(bh * N * D * 4);
+  L.lsea = off; off += up(bh * N * 4);
+  L.kbar = off; off += up(bh * nbp * D * 2);
+  L.vbar = off; off += up(bh * nbp * D * 2);
+  L.mom = off;  off += up(bh * nbp * D * D * 2);
+  L.E = off;    off += up(bh * nbp * nbp * 2);
+  L.r = off;    off += up(bh * nbp * 4);
+  L.T = off;    off += up(bh * nbp * D * D * 2);
+  L.total = off;
+  return L;
+}
+
+int check_remainder(const sva_problem* prob, Dims* d) {
+  const int st = check_problem(prob, d);
+  if (st != SVA_OK) return st;
+  if (d->nB > sva::kRemMaxBlocks) return SVA_ERR_UNSUPPORTED;
+  const int64_t nbp = sva::rem_padded_blocks(d->nB);
+  const int64_t bh = (int64_t)d->B * d->H;
+  // grids: one workgroup per (b, h, padded block), and per (b, h, column tile, row group)
+  if (bh * nbp > INT32_MAX) return SVA_ERR_SHAPE;
+  if (bh * ((int64_t)d->D * d->D / 128) * ((d->nB + 127) / 128) > INT32_MAX) return SVA_ERR_SHAPE;
+  return SVA_OK;
+}
+
 }  // namespace
 
 // ---- fp8 (e4m3) quantisation and attention ----
@@ -332,6 +369,122 @@ int sva_sparse_attention(const sva_problem* prob, const void* q, const void* k, 
       d, true, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
       static_cast<const uint16_t*>(v), kv_idx, kv_count, kmax, out, lse,
       static_cast<hipStream_t>(stream)));
+}
+
+int sva_remainder_workspace(const sva_problem* prob, size_t* bytes) {
+  if (!bytes) return SVA_ERR_INVALID_ARG;
+  Dims d;
+  const int st = check_remainder(prob, &d);
+  if (st != SVA_OK) return st;
+  *bytes = rem_layout(d).total;
+  return SVA_OK;
+}
+
+int sva_block_moments(const sva_problem* prob, const void* k, const void* v, void* kbar, void* vbar,
+                      void* moments, void* stream) {
+  Dims d;
+  const int st = check_remainder(prob, &d);
+  if (st != SVA_OK) return st;
+  if (!k || !v || !kbar || !vbar || !moments) return SVA_ERR_INVALID_ARG;
+  if (!aligned(k, 16) || !aligned(v, 16) || !aligned(kbar, 16) || !aligned(vbar, 16) || !aligned(moments, 16))
+    return SVA_ERR_ALIGNMENT;
+  sva::RemMomentArgs a{};
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.kbar = static_cast<uint16_t*>(kbar);
+  a.vbar = static_cast<uint16_t*>(vbar);
+  a.mom = static_cast<uint16_t*>(moments);
+  a.N = d.N;
+  a.nB = d.nB;
+  a.rows = d.nB;
+  return hip_status(sva::launch_block_moments(d, a, static_cast<hipStream_t>(stream)));
+}
+
+int sva_sparse_attention_remainder(const sva_problem* prob, const void* q, const void* k, const void* v,
+                                   const float* q_pool, const float* k_pool, const int32_t* kv_idx,
+                                   const int32_t* kv_count, int32_t kmax, void* workspace,
+                                   size_t workspace_bytes, void* out, float* lse, void* stream) {
+  Dims d;
+  const int st = check_remainder(prob, &d);
+  if (st != SVA_OK) return st;
+  if (!q || !k || !v || !q_pool || !k_pool || !kv_idx || !kv_count || !workspace || !out)
+    return SVA_ERR_INVALID_ARG;
+  if (kmax < 1) return SVA_ERR_SHAPE;
+  if ((int64_t)d.B * d.H * d.nB * kmax > ((int64_t)1 << 40)) return SVA_ERR_SHAPE;
+  const RemLayout L = rem_layout(d);
+  if (workspace_bytes < L.total) return SVA_ERR_SHAPE;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) || !aligned(q_pool, 16) ||
+      !aligned(k_pool, 16) || !aligned(kv_idx, 4) || !aligned(kv_count, 4) || (lse && !aligned(lse, 4)) ||
+      !aligned(workspace, 256))
+    return SVA_ERR_ALIGNMENT;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  float* oa = reinterpret_cast<float*>(ws + L.oa);
+  float* lsea = reinterpret_cast<float*>(ws + L.lsea);
+  uint16_t* kbar = reinterpret_cast<uint16_t*>(ws + L.kbar);
+  uint16_t* vbar = reinterpret_cast<uint16_t*>(ws + L.vbar);
+  uint16_t* mom = reinterpret_cast<uint16_t*>(ws + L.mom);
+  const int nbp = sva::rem_padded_blocks(d.nB);
+
+  // the kept blocks exactly, in float32 (merged once, at the end)
+  Dims df = d;
+  df.out_f32 = true;
+  hipError_t e = sva::launch_attention(df, true, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                                       static_cast<const uint16_t*>(v), kv_idx, kv_count, kmax, oa, lsea, s);
+  if (e != hipSuccess) return SVA_ERR_HIP;
+
+  sva::RemMomentArgs ma{};
+  ma.k = static_cast<const uint16_t*>(k);
+  ma.v = static_cast<const uint16_t*>(v);
+  ma.kbar = kbar;
+  ma.vbar = vbar;
+  ma.mom = mom;
+  ma.N = d.N;
+  ma.nB = d.nB;
+  ma.rows = nbp;
+  if ((e = sva::launch_block_moments(d, ma, s)) != hipSuccess) return SVA_ERR_HIP;
+
+  sva::RemWeightArgs wa{};
+  wa.q_pool = q_pool;
+  wa.k_pool = k_pool;
+  wa.kv_idx = kv_idx;
+  wa.kv_count = kv_count;
+  wa.E = reinterpret_cast<uint16_t*>(ws + L.E);
+  wa.r = reinterpret_cast<float*>(ws + L.r);
+  wa.nB = d.nB;
+  wa.nBp = nbp;
+  wa.kmax = kmax;
+  wa.scale = (float)d.scale;
+
+  sva::RemGemmArgs ga{};
+  ga.E = wa.E;
+  ga.mom = mom;
+  ga.T = reinterpret_cast<uint16_t*>(ws + L.T);
+  ga.nB = d.nB;
+  ga.nBp = nbp;
+  ga.DD = d.D * d.D;
+  ga.n_wg = d.B * d.H * (ga.DD / 128) * ((d.nB + 127) / 128);
+
+  sva::RemAttnArgs aa{};
+  aa.q = static_cast<const uint16_t*>(q);
+  aa.kbar = kbar;
+  aa.vbar = vbar;
+  aa.kv_idx = kv_idx;
+  aa.kv_count = kv_count;
+  aa.T = ga.T;
+  aa.r = wa.r;
+  aa.o_a = oa;
+  aa.lse_a = lsea;
+  aa.out = out;
+  aa.lse = lse;
+  aa.N = d.N;
+  aa.nB = d.nB;
+  aa.nBp = nbp;
+  aa.kmax = kmax;
+  aa.n_rows = d.B * d.H * d.nB;
+  aa.scale = (float)d.scale;
+  aa.scale_log2 = (float)(d.scale * 1.4426950408889634);
+  return hip_status(sva::launch_remainder(d, wa, ga, aa, s));
 }
 
 int sva_dense_attention(const sva_problem* prob, const void* q, const void* k, const void* v,

@@ -76,6 +76,57 @@ struct Fp8AttnArgs {
 constexpr int kFp8MaxList = 2047;
 hipError_t launch_attention_fp8(const Dims& d, bool sparse, const Fp8AttnArgs& a, hipStream_t stream);
 
+// First-order remainder of the dropped key blocks; remainder.hip.  Block
+// arrays are padded to nBp = rem_padded_blocks(nB) rows (a multiple of 32;
+// padding rows zero).  Layouts per (b, h): kbar, vbar [nBp, D] bf16; moments
+// [nBp, D, D] bf16 with M[e][d] = sum_t V[t][e] (K[t][d] - kbar[d]); E [nBp,
+// nBp] bf16; r [nBp] float32; T [nBp, D, D] bf16.
+constexpr int kRemMaxBlocks = 4096;
+int rem_padded_blocks(int nB);
+struct RemMomentArgs {
+  const uint16_t* k;
+  const uint16_t* v;
+  uint16_t* kbar;
+  uint16_t* vbar;
+  uint16_t* mom;
+  int N, nB, rows;    // rows: blocks per head in the outputs (nB, or nBp when padded)
+};
+struct RemWeightArgs {
+  const float* q_pool;
+  const float* k_pool;
+  const int32_t* kv_idx;
+  const int32_t* kv_count;
+  uint16_t* E;
+  float* r;
+  int nB, nBp, kmax;
+  float scale;        // c
+};
+struct RemGemmArgs {
+  const uint16_t* E;
+  const uint16_t* mom;
+  uint16_t* T;
+  int nB, nBp, DD, n_wg;
+};
+struct RemAttnArgs {
+  const uint16_t* q;
+  const uint16_t* kbar;
+  const uint16_t* vbar;
+  const int32_t* kv_idx;
+  const int32_t* kv_count;
+  const uint16_t* T;
+  const float* r;
+  const float* o_a;   // kept-block attention, float32 [B, H, N, D]
+  const float* lse_a; // its LSE [B, H, N]
+  void* out;
+  float* lse;
+  int N, nB, nBp, kmax, n_rows;
+  float scale;        // c
+  float scale_log2;   // c * log2(e)
+};
+hipError_t launch_block_moments(const Dims& d, const RemMomentArgs& a, hipStream_t stream);
+hipError_t launch_remainder(const Dims& d, const RemWeightArgs& wa, const RemGemmArgs& ga,
+                            const RemAttnArgs& aa, hipStream_t stream);
+
 hipError_t launch_pool(const Dims& d, const uint16_t* q, const uint16_t* k, float* q_pool,
                        float* k_pool, hipStream_t stream);
 

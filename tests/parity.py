@@ -101,3 +101,37 @@ def attention_errors(gpu_out: np.ndarray, ref: np.ndarray, valid: np.ndarray):
     leading shape as ref without D)."""
     d = np.abs(gpu_out.astype(np.float64) - ref)[valid]
     return float(d.max()) if d.size else 0.0, float(d.mean()) if d.size else 0.0
+
+
+# ---- first-order remainder of dropped blocks ----
+# The output is no longer a convex combination of V rows: the first-order term
+# F = sum_j exp(c qbar.kbar_j) c M_j q can be several times larger than V.  It
+# is formed from three factors the GPU stores in bf16 (the weights E, the
+# moments M, their products T), each rounding adding at most 2^-9 relative,
+# so |F| 2^-7 bounds that part; a bf16 output adds its own rounding, at most
+# half a step (2^-9 |out|), bounded here by 2^-8 |out|.  The pooled keys enter
+# the logits rounded to bf16, which moves a logit c q.kbar_j by at most
+# c 2^-9 sum_d |q_d kbar_jd|; a log-sum-exp moves by at most its largest
+# logit's change, which is added to LSE_TOL.
+REM_F_REL = 2.0 ** -7
+REM_OUT_REL = 2.0 ** -8
+
+
+def remainder_errors(got, ref, first, bf16_out: bool):
+    """(worst excess over the elementwise bound, mean error, mean bound):
+    bound = MAX_ABS + 2^-7 |F| (+ 2^-8 |ref| for bf16 outputs); the mean of the
+    errors must stay under MEAN_ABS + the mean of 2^-8 |F| (+ 2^-9 |ref|)."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    f = np.abs(np.asarray(first, dtype=np.float64))
+    err = np.abs(got - ref)
+    bound = MAX_ABS + REM_F_REL * f + (REM_OUT_REL * np.abs(ref) if bf16_out else 0.0)
+    mean_bound = MEAN_ABS + np.mean(0.5 * REM_F_REL * f) + (0.5 * REM_OUT_REL * np.mean(np.abs(ref)) if bf16_out else 0.0)
+    return float(np.max(err - bound)), float(np.mean(err)), float(mean_bound)
+
+
+def remainder_lse_bound(q, kbar, scale):
+    """Per query: LSE_TOL + c 2^-9 max_j sum_d |q_d kbar_jd|."""
+    q = np.abs(np.asarray(q, dtype=np.float64))
+    kb = np.abs(np.asarray(kbar, dtype=np.float64))
+    return LSE_TOL + scale * 2.0 ** -9 * np.max(q @ kb.T, axis=1)

@@ -28,6 +28,7 @@ def test_every_declared_symbol_is_exported(lib):
                           "sva_token_select_workspace", "sva_fp8_padded_len", "sva_fp8_code_dim", "sva_quantize_fp8",
                           "sva_sparse_attention_fp8", "sva_dense_attention_fp8",
                           "sva_token_gather", "sva_token_scatter", "sva_status_string",
+                          "sva_remainder_workspace", "sva_block_moments", "sva_sparse_attention_remainder",
                           "sva_version"}
     for n in names:
         assert hasattr(lib, n), n
@@ -134,6 +135,39 @@ def test_compute_entry_points_reject_before_launch(lib):
         == _lib.SVA_ERR_ALIGNMENT
     assert lib.sva_dense_attention(ctypes.byref(p), A, A, A, None, None, None) == _lib.SVA_ERR_INVALID_ARG
     assert lib.sva_dense_attention(ctypes.byref(p), A, A, A, A, A + 2, None) == _lib.SVA_ERR_ALIGNMENT
+
+
+def _remainder_bytes(B, H, N, D, S):
+    up = lambda x: (x + 255) // 256 * 256
+    nbp = (-(-N // S) + 31) // 32 * 32
+    bh = B * H
+    return (up(bh * N * D * 4) + up(bh * N * 4) + 2 * up(bh * nbp * D * 2) + 2 * up(bh * nbp * D * D * 2)
+            + up(bh * nbp * nbp * 2) + up(bh * nbp * 4))
+
+
+def test_remainder_workspace_and_rejects_before_launch(lib):
+    for wl in (workloads.TINY, workloads.LARGE_64B, workloads.MID_22B):
+        p = sva.problem_for(wl)
+        ws = ctypes.c_size_t(0)
+        assert lib.sva_remainder_workspace(ctypes.byref(p), ctypes.byref(ws)) == _lib.SVA_OK
+        assert ws.value == _remainder_bytes(wl.batch, wl.heads, wl.seq_len, wl.head_dim, wl.block)
+    p = sva.problem_for(workloads.TINY)
+    need = ctypes.c_size_t(0)
+    lib.sva_remainder_workspace(ctypes.byref(p), ctypes.byref(need))
+    A = 1 << 20
+    f = lib.sva_sparse_attention_remainder
+    assert lib.sva_remainder_workspace(ctypes.byref(p), None) == _lib.SVA_ERR_INVALID_ARG
+    assert f(ctypes.byref(p), A, A, A, None, A, A, A, 4, A, need.value, A, None, None) == _lib.SVA_ERR_INVALID_ARG
+    assert f(ctypes.byref(p), A, A, A, A, A, A, A, 0, A, need.value, A, None, None) == _lib.SVA_ERR_SHAPE
+    assert f(ctypes.byref(p), A, A, A, A, A, A, A, 4, A, need.value - 1, A, None, None) == _lib.SVA_ERR_SHAPE
+    assert f(ctypes.byref(p), A, A, A, A, A, A, A, 4, A + 16, need.value, A, None, None) == _lib.SVA_ERR_ALIGNMENT
+    assert f(ctypes.byref(p), A, A, A, A + 4, A, A, A, 4, A, need.value, A, None, None) == _lib.SVA_ERR_ALIGNMENT
+    big = sva.problem(1, 1, 4097 * 64, 64, (1, 1, 4097 * 64), 64)
+    assert lib.sva_remainder_workspace(ctypes.byref(big), ctypes.byref(need)) == _lib.SVA_ERR_UNSUPPORTED
+    assert f(ctypes.byref(big), A, A, A, A, A, A, A, 4, A, 1 << 40, A, None, None) == _lib.SVA_ERR_UNSUPPORTED
+    assert lib.sva_block_moments(ctypes.byref(p), A, A, A, None, A, None) == _lib.SVA_ERR_INVALID_ARG
+    assert lib.sva_block_moments(ctypes.byref(p), A, A, A, A + 2, A, None) == _lib.SVA_ERR_ALIGNMENT
+    assert lib.sva_block_moments(ctypes.byref(big), A, A, A, A, A, None) == _lib.SVA_ERR_UNSUPPORTED
 
 
 def test_qknorm_rope_pool_rejects_before_launch(lib):

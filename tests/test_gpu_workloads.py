@@ -2,7 +2,8 @@
 benchmark times.  Pooled summaries are checked on every head, block masks on
 every row (near-tie rule), attention on sampled query blocks (first, last
 partial, and random ones) that the oracle computes one by one -- both with the
-oracle's own index lists and end to end with the GPU's.
+oracle's own index lists and end to end with the GPU's -- and the first-order
+remainder of the dropped blocks on the same sampled query blocks.
 """
 import math
 
@@ -10,6 +11,7 @@ import numpy as np
 import pytest
 
 import oracle
+import oracle.remainder as orem
 import paper_2606_23743_amd as sva
 from paper_2606_23743_amd import inputs, workloads
 
@@ -105,6 +107,30 @@ def _run(wl, ratios):
                 mx2, mean2 = parity.attention_errors(got2, ref[0, 0, a:e], np.ones(got2.shape, dtype=bool))
                 assert mx2 <= parity.MAX_ABS and mean2 <= parity.MEAN_ABS, ((b, h, i), mx2, mean2)
         say(f"[workload {wl.name} r={r}] attention ok on {len(rows)} sampled query blocks")
+
+        # first-order remainder of the dropped blocks, same lists and query blocks
+        rem, rem_lse = sva.sparse_attention_remainder(prob, dev["q"], dev["k"], dev["v"], qp, kp,
+                                                      torch.from_numpy(oidx).cuda(), torch.from_numpy(ocnt).cuda(),
+                                                      want_lse=True)
+        torch.cuda.synchronize()
+        for (b, h) in sorted({(b, h) for (b, h, _) in rows}):
+            mine = [i for (bb, hh, i) in rows if (bb, hh) == (b, h)]
+            q4, k4, v4 = (f64[n][(b, h)][None, None] for n in ("q", "k", "v"))
+            ref, rlse = orem.remainder_attention(q4, k4, v4, [[kept[b][h]]], wl.block, c,
+                                                 rows=[(0, 0, i) for i in mine])
+            ref0, _ = orem.remainder_attention(q4, k4, v4, [[kept[b][h]]], wl.block, c,
+                                               rows=[(0, 0, i) for i in mine], first_order=False)
+            kbar = oracle.pool_blocks(k4[0, 0], wl.block)
+            for i in mine:
+                a, e = i * wl.block, min((i + 1) * wl.block, wl.seq_len)
+                got = rem[b, h, a:e].float().cpu().numpy()
+                excess, mean, mean_bound = parity.remainder_errors(got, ref[0, 0, a:e],
+                                                                   ref[0, 0, a:e] - ref0[0, 0, a:e], True)
+                assert excess <= 0.0 and mean <= mean_bound, ("remainder", (b, h, i), excess, mean, mean_bound)
+                lse_bound = parity.remainder_lse_bound(q4[0, 0, a:e], kbar, c)
+                assert np.all(np.abs(rem_lse[b, h, a:e].cpu().numpy() - rlse[0, 0, a:e]) <= lse_bound)
+        say(f"[workload {wl.name} r={r}] remainder ok on {len(rows)} sampled query blocks")
+        del rem, rem_lse
         if r == 1.0:
             dout, _ = sva.dense_attention(prob, dev["q"], dev["k"], dev["v"])
             torch.cuda.synchronize()
