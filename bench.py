@@ -279,6 +279,41 @@ def measure(args, wl, with_cpu: bool):
         dense_flops = 4.0 * D * B * H * float(N) * N
         extra["dense_attention"] = {"ms": dense_ms, "tflops": dense_flops / (dense_ms * 1e-3) / 1e12,
                                     "sparse_path_speedup": dense_ms / ms_step}
+    else:
+        dout = None
+
+    # first-order remainder of the dropped blocks (same lists): the kept part
+    # in float32, block moments, weights, the per-head GEMM and the pooled-key
+    # attention with the merge, as one call
+    if nb <= 4096:
+        ws = torch.empty(sva.remainder_workspace(prob), dtype=torch.uint8, device="cuda")
+        orem = torch.empty_like(out)
+        sva.sparse_attention_remainder(prob, dev["q"], dev["k"], dev["v"], qp, kp, idx, cnt, out=orem,
+                                       workspace=ws, stream=stream)
+        a, b = ev(), ev()
+        a.record(stream)
+        for _ in range(args.steps):
+            sva.sparse_attention_remainder(prob, dev["q"], dev["k"], dev["v"], qp, kp, idx, cnt, out=orem,
+                                           workspace=ws, stream=stream)
+        b.record(stream)
+        torch.cuda.synchronize()
+        rem_ms = a.elapsed_time(b) / args.steps
+        nbp = (nb + 31) // 32 * 32
+        bhn = float(B * H * N)
+        rem_flops = {"moments": 2.0 * D * D * bhn,                       # one outer product per token
+                     "weights_gemm": 2.0 * B * H * nb * nb * D * D,      # T_i = sum_j E_ij M_j
+                     "pooled_attention": 4.0 * D * nb * bhn + 2.0 * D * D * bhn}
+        rec_rem = {"ms": round(rem_ms, 4), "sparse_attention_ms": round(att_ms, 4),
+                   "extra_ms_over_sparse": round(rem_ms - att_ms, 4),
+                   "remainder_flops": rem_flops, "padded_blocks": nbp,
+                   "workspace_bytes": int(ws.numel()),
+                   "mean_abs_change_vs_sparse": float((orem.float() - out.float()).abs().mean())}
+        if dout is not None:
+            rec_rem["mean_abs_diff_vs_dense"] = float((orem.float() - dout.float()).abs().mean())
+            rec_rem["sparse_mean_abs_diff_vs_dense"] = float((out.float() - dout.float()).abs().mean())
+        extra["remainder"] = rec_rem
+        del ws, orem
+    if dout is not None:
         del dout
 
     # the fused QKNorm + RoPE + pool producer on the same Q and K (unit gamma):
