@@ -54,6 +54,7 @@ __global__ __launch_bounds__(256) void rem_moments_kernel(RemMomentArgs a) {
   __shared__ __attribute__((aligned(1024))) unsigned char Kt[NCHK][CT];
   __shared__ __attribute__((aligned(1024))) unsigned char Vt[NCHK][CT];
   __shared__ float kmean[D];
+  __shared__ float part[2][4][D];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -80,30 +81,54 @@ __global__ __launch_bounds__(256) void rem_moments_kernel(RemMomentArgs a) {
   const uint16_t* Vb = a.v + ((size_t)bh * a.N + t0) * D;
   auto tile_off = [](int t, int c) { return (t >> 5) * CT + (t & 31) * G::RB + (swz_v<G::NCH>(t & 31, c) << 4); };
 
-  for (int p = tid; p < PIECES; p += NT) {
-    const int t = p / G::DCH, c = p - (p / G::DCH) * G::DCH;
-    uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-    if (t < n) {
-      kv = *reinterpret_cast<const uint4*>(Kb + (size_t)t * D + c * 8);
-      vv = *reinterpret_cast<const uint4*>(Vb + (size_t)t * D + c * 8);
+  // Thread (g, c) takes the 16-byte column piece c (of the NCH pieces of an
+  // LDS row; pieces past D are idle) of rows g, g + NG, ...: rows are read
+  // whole by consecutive threads, and each thread keeps the float32 sums of
+  // its eight columns.  The lanes of a wave that share c are NCH apart, so a
+  // fixed XOR-shuffle tree adds them, and the four waves' sums are added in
+  // order: the means are reproducible.
+  constexpr int NG = NT / G::NCH;            // row groups
+  const int g = tid / G::NCH, c = tid - g * G::NCH;
+  float ks[8] = {}, vs[8] = {};
+  if (c < G::DCH) {
+    for (int t = g; t < S; t += NG) {
+      uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
+      if (t < n) {
+        kv = *reinterpret_cast<const uint4*>(Kb + (size_t)t * D + c * 8);
+        vv = *reinterpret_cast<const uint4*>(Vb + (size_t)t * D + c * 8);
+      }
+      *reinterpret_cast<uint4*>(&Kt[0][0] + tile_off(t, c)) = kv;
+      *reinterpret_cast<uint4*>(&Vt[0][0] + tile_off(t, c)) = vv;
+      const bf16x8 kx = __builtin_bit_cast(bf16x8, kv), vx = __builtin_bit_cast(bf16x8, vv);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        ks[e] += (float)kx[e];
+        vs[e] += (float)vx[e];
+      }
     }
-    *reinterpret_cast<uint4*>(&Kt[0][0] + tile_off(t, c)) = kv;
-    *reinterpret_cast<uint4*>(&Vt[0][0] + tile_off(t, c)) = vv;
+  }
+#pragma unroll
+  for (int off = G::NCH; off < 64; off <<= 1)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      ks[e] += __shfl_xor(ks[e], off, 64);
+      vs[e] += __shfl_xor(vs[e], off, 64);
+    }
+  if (lane < G::DCH) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      part[0][w][lane * 8 + e] = ks[e];
+      part[1][w][lane * 8 + e] = vs[e];
+    }
   }
   __syncthreads();
-
-  // means over the valid tokens, float32; threads 0..D-1 take K, D..2D-1 V
-  if (tid < 2 * D) {
-    const bool isk = tid < D;
-    const int d = isk ? tid : tid - D;
-    const unsigned char* base = isk ? &Kt[0][0] : &Vt[0][0];
+  if (tid < 2 * D) {                         // threads 0..D-1 take K, D..2D-1 V
+    const int kv = tid < D ? 0 : 1;
+    const int d = tid - kv * D;
     float s = 0.0f;
-    for (int t = 0; t < n; ++t) {
-      const uint16_t x = *reinterpret_cast<const uint16_t*>(base + tile_off(t, d >> 3) + (d & 7) * 2);
-      s += __uint_as_float((unsigned)x << 16);
-    }
+    for (int q = 0; q < 4; ++q) s += part[kv][q][d];
     s /= (float)n;
-    if (isk) {
+    if (kv == 0) {
       kmean[d] = s;
       kbar[d] = bf16_bits(s);
     } else {
@@ -162,11 +187,21 @@ __global__ __launch_bounds__(256) void rem_moments_kernel(RemMomentArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// First-order weights.  kRemRows query blocks of one head per workgroup: the
+// First-order weights.  kRemRows query blocks of one head per workgroup (each
+// pooled key row a thread loads serves all of them): the
 // kept sets as LDS bitmaps, then two passes over the key blocks (row maxima,
 // then the weights), each thread taking key blocks tid, tid + 256, ...
 // ---------------------------------------------------------------------------
-constexpr int kRemRows = 8;
+constexpr int kRemRows = 32;
+
+// Position of key jj (0..31) of a chunk in a row of E: the eight keys one MFMA
+// lane takes for (kk, hf) -- kk*16 + hf*4 + 0..3, then kk*16 + 8 + hf*4 + 0..3,
+// the order of a softmax_chunk register group -- are the 16-byte piece
+// kk*2 + hf.
+__host__ __device__ __forceinline__ int e_position(int jj) {
+  const int kk = jj >> 4, r = jj & 15;
+  return kk * 16 + ((r >> 2) & 1) * 8 + (r >> 3) * 4 + (r & 3);
+}
 
 template <int D>
 __global__ __launch_bounds__(256) void rem_weights_kernel(RemWeightArgs a) {
@@ -248,107 +283,135 @@ __global__ __launch_bounds__(256) void rem_weights_kernel(RemWeightArgs a) {
   for (int j = tid; j < nBp; j += NT) {
     float s[kRemRows] = {};
     if (j < nB) scores(j, s);
+    uint16_t* Ec = a.E + ((size_t)bh * (nBp / 32) + (j >> 5)) * a.nBr * 32 + e_position(j & 31);
 #pragma unroll
     for (int ri = 0; ri < kRemRows; ++ri) {
       if (i0 + ri >= nB) break;
       const bool kept = j >= nB || ((bm[ri][j >> 5] >> (j & 31)) & 1u);
       const float e = kept ? 0.0f : exp2f((s[ri] - rmax[ri]) * kLog2e);
-      a.E[((size_t)bh * nBp + i0 + ri) * nBp + j] = bf16_bits(e);
+      Ec[(size_t)(i0 + ri) * 32] = bf16_bits(e);
     }
   }
 }
 
 // ---------------------------------------------------------------------------
 // T_i = sum_j E[i][j] M_j, per head: C [nB x D*D] = E [nB x nBp] . M [nBp x D*D].
-// A workgroup takes 128 columns (one LDS tile row of 256 bytes) and 128 rows
-// i (32 per wave); per 32-row chunk of M the tile is staged by direct loads
-// (double-buffered) and each wave accumulates T^T += M_tile^T E^T with the
-// PV step of the attention kernels (the E values take the place of P).
-// Workgroups of one column tile are consecutive in XCD order, so the M tile
-// they share is fetched into one L2.
+// A workgroup takes 128 columns (one LDS tile row of 256 bytes) and 256 rows
+// i (64 per wave, two 32-row halves); each transpose read of M feeds both
+// halves' MFMAs.  Per 32-key chunk, the M tile (32 x 128, V-swizzled) and the
+// E tile (256 rows x 64 bytes, contiguous in the chunk-blocked layout; the
+// 16-byte pieces of row r XOR-swizzled by (r/4)%4 so that 16 lanes reading 16
+// consecutive rows hit all 64 banks) are staged by direct loads in three LDS
+// stages, two chunks ahead.  Each chunk issues one load group (chunk 0 again
+// past the end), so the wait counts are constants.  The waves run the PV step
+// with E in place of P.  Workgroups of one column tile are consecutive in XCD
+// order, so the M tile they share comes from one L2.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void rem_gemm_kernel(RemGemmArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void rem_gemm_kernel(RemGemmArgs a) {
   using G = Geo<128>;
-  constexpr int CT = 32 * G::RB;             // 32 rows x 128 columns of bf16
-  constexpr int NUW = CT / 1024 / 4;         // direct-load pieces per wave
-  __shared__ __attribute__((aligned(1024))) unsigned char Ms[2][CT];
+  constexpr int CT = 32 * G::RB;             // M tile: 32 rows x 128 columns of bf16
+  constexpr int ET = kRemGemmRows * 64;      // E tile: 256 rows x 32 keys of bf16
+  constexpr int NUW = CT / 1024 / 4;         // M direct loads per wave per chunk
+  constexpr int NUE = ET / 1024 / 4;         // E direct loads per wave per chunk
+  constexpr int NST = 3, PD = 2;             // LDS stages, load distance (chunks)
+  __shared__ __attribute__((aligned(1024))) unsigned char Ms[NST][CT];
+  __shared__ __attribute__((aligned(1024))) unsigned char Es[NST][ET];
 
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int hf = lane >> 5, l32 = lane & 31;
-  const int DD = a.DD, nB = a.nB, nBp = a.nBp;
-  const int nct = DD / 128, nrg = (nB + 127) / 128;
+  const int DD = a.DD, nB = a.nB, nBp = a.nBp, nBr = a.nBr;
+  const int nct = DD / 128, nrg = (nB + kRemGemmRows - 1) / kRemGemmRows;
   const int id = __builtin_amdgcn_readfirstlane(xcd_remap(blockIdx.x, a.n_wg));
   const int rg = id % nrg;
   const int tt = id / nrg;
   const int ct = tt % nct;
   const int bh = tt / nct;
   const int c0 = ct * 128;
-  const int i = rg * 128 + w * 32 + l32;
-  const bool live = i < nB;
-  const uint16_t* Mh = a.mom + (size_t)bh * nBp * DD;
-  const uint16_t* Er = a.E + ((size_t)bh * nBp + (live ? i : 0)) * nBp;
+  const int nch = nBp / 32;
 
-  const __amdgpu_buffer_rsrc_t rs =
-      __builtin_amdgcn_make_buffer_rsrc((void*)Mh, (short)0, nBp * DD * 2, 0x00020000);
-  int mv[NUW];
+  const __amdgpu_buffer_rsrc_t mrs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(a.mom + (size_t)bh * nBp * DD), (short)0, nBp * DD * 2, 0x00020000);
+  const __amdgpu_buffer_rsrc_t ers = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(a.E + (size_t)bh * nch * nBr * 32), (short)0, nch * nBr * 64, 0x00020000);
+  int mv[NUW], ev[NUE];
 #pragma unroll
   for (int v = 0; v < NUW; ++v) {
     const int r = (w * NUW + v) * G::RPI + lane / G::NCH;
-    const int c = swz_v<G::NCH>(r, lane % G::NCH);
-    mv[v] = (r * DD + c0 + c * 8) * 2;
+    mv[v] = (r * DD + c0 + swz_v<G::NCH>(r, lane % G::NCH) * 8) * 2;
+  }
+#pragma unroll
+  for (int v = 0; v < NUE; ++v) {
+    const int r = (w * NUE + v) * 16 + (lane >> 2);   // row of the E tile
+    ev[v] = r * 64 + (((lane & 3) ^ ((r >> 2) & 3)) << 4);
   }
   const unsigned ms_base = __builtin_amdgcn_readfirstlane((unsigned)(size_t)(const lds_u8*)&Ms[0][0]);
-  auto load_m = [&](int st, int j0) {
+  const unsigned es_base = __builtin_amdgcn_readfirstlane((unsigned)(size_t)(const lds_u8*)&Es[0][0]);
+  auto fetch = [&](int st, int ch) {
+    const int c = ch < nch ? ch : 0;         // past the end: chunk 0 again (in bounds, unused)
 #pragma unroll
-    for (int v = 0; v < NUW; ++v) buffer_to_lds(rs, ms_base + st * CT + (w * NUW + v) * 1024, mv[v], j0 * DD * 2);
+    for (int v = 0; v < NUW; ++v) buffer_to_lds(mrs, ms_base + st * CT + (w * NUW + v) * 1024, mv[v], c * 32 * DD * 2);
+#pragma unroll
+    for (int v = 0; v < NUE; ++v)
+      buffer_to_lds(ers, es_base + st * ET + (w * NUE + v) * 1024, ev[v], (c * nBr + rg * kRemGemmRows) * 64);
   };
-  // E values of row i in the order of a softmax_chunk register group
-  auto load_e = [&](bf16x8 (&e)[2], int j0) {
+  // E operand offsets in a stage: row w*64 + h2*32 + l32, piece kk*2 + hf
+  int eoff[2][2];
+#pragma unroll
+  for (int h2 = 0; h2 < 2; ++h2)
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
-      if (live) {
-        const uint16_t* p = Er + j0 + kk * 16 + hf * 4;
-        const u32x2 lo = *reinterpret_cast<const u32x2*>(p);
-        const u32x2 hi = *reinterpret_cast<const u32x2*>(p + 8);
-        const u32x4 x = {lo[0], lo[1], hi[0], hi[1]};
-        e[kk] = __builtin_bit_cast(bf16x8, x);
-      } else {
-        e[kk] = bf16x8{};
-      }
+      const int r = w * 64 + h2 * 32 + l32;
+      eoff[h2][kk] = r * 64 + (((kk * 2 + hf) ^ ((r >> 2) & 3)) << 4);
     }
-  };
 
   int koff[G::DQ], voff[G::DT];
   operand_offsets<128>(lane, koff, voff);
-  f32x16 acc[G::DT];
+  f32x16 acc[2][G::DT];
 #pragma unroll
-  for (int dt = 0; dt < G::DT; ++dt) acc[dt] = f32x16{};
-  const int nch = nBp / 32;
-  bf16x8 ecur[2], enext[2] = {bf16x8{}, bf16x8{}};
-  load_m(0, 0);
-  load_e(ecur, 0);
-  for (int ch = 0; ch < nch; ++ch) {
-    wait_vmcnt_lds_idle<0>();                // this wave's loads of chunk ch landed
-    wg_barrier();                            // every wave's; chunk ch-1's stage is free
-    if (ch + 1 < nch) {
-      load_m((ch + 1) & 1, (ch + 1) * 32);
-      load_e(enext, (ch + 1) * 32);
+  for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+    for (int dt = 0; dt < G::DT; ++dt) acc[h2][dt] = f32x16{};
+  fetch(0, 0);
+  fetch(1, 1);
+  for (int ch0 = 0; ch0 < nch; ch0 += NST) {
+#pragma unroll
+    for (int c = 0; c < NST; ++c) {
+      const int ch = ch0 + c;
+      if (ch >= nch) break;
+      wait_vmcnt_lds_idle<NUW + NUE>();      // chunk ch landed (chunk ch+1 may be in flight)
+      wg_barrier();                          // every wave's; chunk ch-1's stage is free
+      fetch((c + PD) % NST, ch + PD);
+      bf16x8 eop[2][2];
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) eop[h2][kk] = *reinterpret_cast<const bf16x8*>(&Es[c][0] + eoff[h2][kk]);
+#pragma unroll
+      for (int dt = 0; dt < G::DT; ++dt)
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+          const bf16x8 mop = tr_operand<128>(&Ms[c][0], voff[dt], kk);
+#pragma unroll
+          for (int h2 = 0; h2 < 2; ++h2)
+            acc[h2][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(mop, eop[h2][kk], acc[h2][dt], 0, 0, 0);
+        }
     }
-    pv_chunk<128>(ecur, &Ms[ch & 1][0], voff, acc);
-    ecur[0] = enext[0];
-    ecur[1] = enext[1];
   }
   wait_vmcnt<0>();
-  if (live) {
+#pragma unroll
+  for (int h2 = 0; h2 < 2; ++h2) {
+    const int i = rg * kRemGemmRows + w * 64 + h2 * 32 + l32;
+    if (i >= nB) continue;
     uint16_t* Tr = a.T + ((size_t)bh * nBp + i) * DD + c0;
 #pragma unroll
     for (int dt = 0; dt < G::DT; ++dt)
 #pragma unroll
       for (int r4 = 0; r4 < 4; ++r4) {
         const int col = dt * 32 + r4 * 8 + hf * 4;
-        const bf16x2 x = cvt2(acc[dt][r4 * 4 + 0], acc[dt][r4 * 4 + 1]);
-        const bf16x2 y = cvt2(acc[dt][r4 * 4 + 2], acc[dt][r4 * 4 + 3]);
+        const bf16x2 x = cvt2(acc[h2][dt][r4 * 4 + 0], acc[h2][dt][r4 * 4 + 1]);
+        const bf16x2 y = cvt2(acc[h2][dt][r4 * 4 + 2], acc[h2][dt][r4 * 4 + 3]);
         const bf16x4 o = {x[0], x[1], y[0], y[1]};
         *reinterpret_cast<bf16x4*>(Tr + col) = o;
       }
@@ -356,11 +419,13 @@ __global__ __launch_bounds__(256) void rem_gemm_kernel(RemGemmArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Remainder attention and merge.  One workgroup (S/32 waves of 32 queries) per
-// query block, as the 32-query sparse kernel.  The pooled keys kbar_j of the
-// head are walked in 32-row chunks (double-buffered direct loads): S^T = Kbar
-// Q^T, logit + log2 n_j in log2 units (-inf for kept and padding blocks), P
-// rounded to bf16 with l summed from it, O^T += Vbar^T P^T.  The reference
+// Remainder attention and merge.  One workgroup of four waves (32 queries
+// each) per 128 queries: one query block at S = 128, two at S = 64 (the
+// pooled keys are the same for every query block of a head; only the masks
+// differ).  The pooled keys kbar_j of the head are walked in 32-row chunks
+// (four LDS stages): S^T = Kbar Q^T, logit + log2 n_j in log2 units (-inf for
+// kept and padding blocks), P rounded to bf16 with l summed from it,
+// O^T += Vbar^T P^T.  The reference
 // starts at max(LSE of the kept part, r_i) (log2 units) and moves up only
 // when a chunk's maximum passes it by more than 8, so it is rarely moved.  At
 // the end the first-order term exp(r_i) c T_i q is one MFMA pass with T_i rows
@@ -368,40 +433,53 @@ __global__ __launch_bounds__(256) void rem_gemm_kernel(RemGemmArgs a) {
 // LSE in float32) is added with its weight exp(LSE) before the division.
 // ---------------------------------------------------------------------------
 template <int D, int S, bool OUT_F32>
-__global__ __launch_bounds__(2 * S) __attribute__((amdgpu_waves_per_eu(2, 2)))
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void rem_attn_kernel(RemAttnArgs a) {
   using G = Geo<D>;
-  constexpr int NW = S / 32;
+  constexpr int NW = 4;                      // waves: 128 queries
+  constexpr int NQB = 128 / S;               // query blocks per workgroup
   constexpr int CT = 32 * G::RB;
   constexpr int NUW = CT / 1024 / NW;
   constexpr int kWords = kRemMaxBlocks / 32;
   static_assert(NUW >= 1, "tile split");
-  __shared__ __attribute__((aligned(1024))) unsigned char Ks[2][CT];
-  __shared__ __attribute__((aligned(1024))) unsigned char Vs[2][CT];
-  __shared__ uint32_t bm[kWords];
+  __shared__ __attribute__((aligned(1024))) unsigned char Ks[4][CT];
+  __shared__ __attribute__((aligned(1024))) unsigned char Vs[4][CT];
+  __shared__ uint32_t bms[NQB][kWords];
 
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int hf = lane >> 5, l32 = lane & 31;
   const int N = a.N, nB = a.nB, nBp = a.nBp;
-  const int row = __builtin_amdgcn_readfirstlane(xcd_remap(blockIdx.x, a.n_rows));
-  const int bh = row / nB;
-  const int i = row - bh * nB;
+  const int groups = (nB + NQB - 1) / NQB;
+  const int item = __builtin_amdgcn_readfirstlane(xcd_remap(blockIdx.x, a.n_rows));
+  const int bh = item / groups;
+  const int ib0 = (item - bh * groups) * NQB;
+  const int qb = w * 32 / S;                 // this wave's query block within the workgroup
+  const int i_raw = ib0 + qb;                // may be nB (no such block: the wave only helps load)
+  const int i = min(i_raw, nB - 1);
+  const uint32_t* bm = bms[qb];
 
-  for (int t = threadIdx.x; t < nBp / 32; t += 2 * S) bm[t] = 0u;
+  // padding blocks j in [nB, nBp) are masked like kept ones
+  for (int t = threadIdx.x; t < NQB * kWords; t += 256) {
+    const int j0 = (t % kWords) * 32;
+    (&bms[0][0])[t] = j0 + 32 <= nB ? 0u : (j0 >= nB ? ~0u : ~0u << (nB - j0));
+  }
   __syncthreads();
-  {
+#pragma unroll
+  for (int b2 = 0; b2 < NQB; ++b2) {
+    if (ib0 + b2 >= nB) break;
+    const int row = bh * nB + ib0 + b2;
     const int cnt = min(max(a.kv_count[row], 0), a.kmax);
     const int32_t* idx = a.kv_idx + (size_t)row * a.kmax;
-    for (int t = threadIdx.x; t < cnt; t += 2 * S) {
+    for (int t = threadIdx.x; t < cnt; t += 256) {
       const int j = idx[t];
-      if (j >= 0 && j < nB) atomicOr(&bm[j >> 5], 1u << (j & 31));
+      if (j >= 0 && j < nB) atomicOr(&bms[b2][j >> 5], 1u << (j & 31));
     }
   }
   __syncthreads();
 
-  const int qr = i * S + w * 32 + l32;
-  const bool present = qr < N;
+  const int qr = i_raw * S + (w * 32) % S + l32;
+  const bool present = i_raw < nB && qr < N;
   bf16x8 qop[G::DQ];
   load_q<D>(qop, a.q + (size_t)bh * N * D, qr, present, hf);
 
@@ -422,39 +500,75 @@ void rem_attn_kernel(RemAttnArgs a) {
   const float log2_s = S == 128 ? 7.0f : 6.0f;
   const float log2_last = __log2f((float)(N - (nB - 1) * S));
 
+  // Pipeline over the pooled-key chunks: four LDS stages (chunk x in stage
+  // x % 4), loads three chunks ahead, and the S products of the next chunk
+  // issued alongside this chunk's softmax, as in the 32-query kernel.  Each
+  // iteration issues one load group (chunk 0 again past the end), so the wait
+  // counts are constants.
+  constexpr int NST = 4, PD = 3;
   const int nch = nBp / 32;
-  load_chunk(ld, 0, 0);
-  for (int ch = 0; ch < nch; ++ch) {
-    wait_vmcnt_lds_idle<0>();
-    wg_barrier();
-    if (ch + 1 < nch) load_chunk(ld, (ch + 1) & 1, (ch + 1) * 32);
-    const uint32_t word = bm[ch];
-    f32x16 sacc;
-    qk_chunk<D>(sacc, &Ks[ch & 1][0], koff, qop);
+  auto fetch = [&](int st, int ch) { load_chunk(ld, st, ch < nch ? ch * 32 : 0); };
+  // logits in log2 units plus log2 n_j, -inf for kept and padding blocks;
+  // every block but the last has n_j = S, so only the last block's chunk
+  // takes the general form
+  const int last_ch = (nB - 1) / 32;
+  auto masked = [&](f32x16& x, int ch) {
+    const uint32_t word = bm[ch] >> (hf * 4);
     float mx = -INFINITY;
+    if (ch != last_ch) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int jj = (r >> 2) * 8 + hf * 4 + (r & 3);
-      const int j = ch * 32 + jj;
-      const bool off = j >= nB || ((word >> jj) & 1u);
-      sacc[r] = off ? -INFINITY : __builtin_fmaf(sacc[r], sl2, j == nB - 1 ? log2_last : log2_s);
-      mx = fmaxf(mx, sacc[r]);
-    }
-    mx = swap_halves_max(mx);
-    if (__builtin_amdgcn_ballot_w64(mx > m_ref + 8.0f) != 0) {
-      if (mx > m_ref + 8.0f) {
-        const float f = __builtin_amdgcn_exp2f(m_ref - mx);
-        l_part *= f;
+      for (int r = 0; r < 16; ++r) {
+        const int jj = (r >> 2) * 8 + (r & 3);           // key within the chunk, less hf*4
+        const float b = ((word >> jj) & 1u) ? -INFINITY : log2_s;
+        x[r] = __builtin_fmaf(x[r], sl2, b);
+        mx = fmaxf(mx, x[r]);
+      }
+    } else {
 #pragma unroll
-        for (int dt = 0; dt < G::DT; ++dt)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) oacc[dt][r] *= f;
-        m_ref = mx;
+      for (int r = 0; r < 16; ++r) {
+        const int jj = (r >> 2) * 8 + (r & 3);
+        const int j = ch * 32 + hf * 4 + jj;
+        const float b = ((word >> jj) & 1u) ? -INFINITY : (j == nB - 1 ? log2_last : log2_s);
+        x[r] = __builtin_fmaf(x[r], sl2, b);
+        mx = fmaxf(mx, x[r]);
       }
     }
-    bf16x8 pop[2];
-    softmax_chunk(sacc, pop, l_part, m_ref, 1.0f);
-    pv_chunk<D>(pop, &Vs[ch & 1][0], voff, oacc);
+    return swap_halves_max(mx);
+  };
+  fetch(0, 0);
+  fetch(1, 1);
+  fetch(2, 2);
+  wait_vmcnt<2 * NUW * (PD - 1)>();
+  wg_barrier();
+  f32x16 sacc;
+  qk_chunk<D>(sacc, &Ks[0][0], koff, qop);
+  for (int ch0 = 0; ch0 < nch; ch0 += NST) {
+#pragma unroll
+    for (int c = 0; c < NST; ++c) {
+      const int ch = ch0 + c;
+      if (ch >= nch) break;
+      wait_vmcnt_lds_idle<2 * NUW * (PD - 2)>();     // chunk ch+1 landed
+      wg_barrier();
+      fetch((c + PD) % NST, ch + PD);
+      f32x16 snext;
+      qk_chunk<D>(snext, &Ks[(c + 1) % NST][0], koff, qop);
+      const float mx = masked(sacc, ch);
+      if (__builtin_amdgcn_ballot_w64(mx > m_ref + 8.0f) != 0) {
+        if (mx > m_ref + 8.0f) {
+          const float f = __builtin_amdgcn_exp2f(m_ref - mx);
+          l_part *= f;
+#pragma unroll
+          for (int dt = 0; dt < G::DT; ++dt)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) oacc[dt][r] *= f;
+          m_ref = mx;
+        }
+      }
+      bf16x8 pop[2];
+      softmax_chunk(sacc, pop, l_part, m_ref, 1.0f);
+      pv_chunk<D>(pop, &Vs[c][0], voff, oacc);
+      sacc = snext;
+    }
   }
   wait_vmcnt<0>();
 
@@ -513,9 +627,12 @@ hipError_t launch_moments_ds(const Dims& d, const RemMomentArgs& a, hipStream_t 
 
 template <int D, int S>
 hipError_t launch_rem_attn_ds(const Dims& d, const RemAttnArgs& a, hipStream_t stream) {
-  dim3 grid(a.n_rows), block(2 * S);
-  if (d.out_f32) hipLaunchKernelGGL((rem_attn_kernel<D, S, true>), grid, block, 0, stream, a);
-  else hipLaunchKernelGGL((rem_attn_kernel<D, S, false>), grid, block, 0, stream, a);
+  constexpr int NQB = 128 / S;
+  RemAttnArgs g = a;
+  g.n_rows = d.B * d.H * ((d.nB + NQB - 1) / NQB);   // workgroups
+  dim3 grid(g.n_rows), block(256);
+  if (d.out_f32) hipLaunchKernelGGL((rem_attn_kernel<D, S, true>), grid, block, 0, stream, g);
+  else hipLaunchKernelGGL((rem_attn_kernel<D, S, false>), grid, block, 0, stream, g);
   return hipGetLastError();
 }
 
@@ -529,6 +646,7 @@ hipError_t launch_weights_d(const Dims& d, const RemWeightArgs& a, hipStream_t s
 }  // namespace
 
 int rem_padded_blocks(int nB) { return (nB + 31) / 32 * 32; }
+int rem_weight_rows(int nB) { return (nB + kRemGemmRows - 1) / kRemGemmRows * kRemGemmRows; }
 
 hipError_t launch_block_moments(const Dims& d, const RemMomentArgs& a, hipStream_t stream) {
   switch (d.D * 1000 + d.S) {
@@ -552,7 +670,9 @@ hipError_t launch_remainder(const Dims& d, const RemWeightArgs& wa, const RemGem
     default: return hipErrorInvalidValue;
   }
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(rem_gemm_kernel, dim3(ga.n_wg), dim3(256), 0, stream, ga);
+  RemGemmArgs g = ga;
+  g.n_wg = d.B * d.H * (g.DD / 128) * ((d.nB + kRemGemmRows - 1) / kRemGemmRows);
+  hipLaunchKernelGGL(rem_gemm_kernel, dim3(g.n_wg), dim3(256), 0, stream, g);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   switch (d.D * 1000 + d.S) {
     case 64128: return launch_rem_attn_ds<64, 128>(d, aa, stream);

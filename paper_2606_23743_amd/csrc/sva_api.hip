@@ -117,7 +117,7 @@ RemLayout rem_layout(const Dims& d) {
   L.kbar = off; off += up(bh * nbp * D * 2);
   L.vbar = off; off += up(bh * nbp * D * 2);
   L.mom = off;  off += up(bh * nbp * D * D * 2);
-  L.E = off;    off += up(bh * nbp * nbp * 2);
+  L.E = off;    off += up(bh * nbp * (size_t)sva::rem_weight_rows(d.nB) * 2);
   L.r = off;    off += up(bh * nbp * 4);
   L.T = off;    off += up(bh * nbp * D * D * 2);
   L.total = off;
@@ -132,7 +132,8 @@ int check_remainder(const sva_problem* prob, Dims* d) {
   const int64_t bh = (int64_t)d->B * d->H;
   // grids: one workgroup per (b, h, padded block), and per (b, h, column tile, row group)
   if (bh * nbp > INT32_MAX) return SVA_ERR_SHAPE;
-  if (bh * ((int64_t)d->D * d->D / 128) * ((d->nB + 127) / 128) > INT32_MAX) return SVA_ERR_SHAPE;
+  if (bh * ((int64_t)d->D * d->D / 128) * ((d->nB + sva::kRemGemmRows - 1) / sva::kRemGemmRows) > INT32_MAX)
+    return SVA_ERR_SHAPE;
   return SVA_OK;
 }
 
@@ -453,6 +454,7 @@ int sva_sparse_attention_remainder(const sva_problem* prob, const void* q, const
   wa.r = reinterpret_cast<float*>(ws + L.r);
   wa.nB = d.nB;
   wa.nBp = nbp;
+  wa.nBr = sva::rem_weight_rows(d.nB);
   wa.kmax = kmax;
   wa.scale = (float)d.scale;
 
@@ -462,8 +464,9 @@ int sva_sparse_attention_remainder(const sva_problem* prob, const void* q, const
   ga.T = reinterpret_cast<uint16_t*>(ws + L.T);
   ga.nB = d.nB;
   ga.nBp = nbp;
+  ga.nBr = wa.nBr;
   ga.DD = d.D * d.D;
-  ga.n_wg = d.B * d.H * (ga.DD / 128) * ((d.nB + 127) / 128);
+  ga.n_wg = 0;                      // set by the launcher
 
   sva::RemAttnArgs aa{};
   aa.q = static_cast<const uint16_t*>(q);
@@ -481,7 +484,7 @@ int sva_sparse_attention_remainder(const sva_problem* prob, const void* q, const
   aa.nB = d.nB;
   aa.nBp = nbp;
   aa.kmax = kmax;
-  aa.n_rows = d.B * d.H * d.nB;
+  aa.n_rows = 0;                    // set by the launcher
   aa.scale = (float)d.scale;
   aa.scale_log2 = (float)(d.scale * 1.4426950408889634);
   return hip_status(sva::launch_remainder(d, wa, ga, aa, s));

@@ -79,10 +79,15 @@ hipError_t launch_attention_fp8(const Dims& d, bool sparse, const Fp8AttnArgs& a
 // First-order remainder of the dropped key blocks; remainder.hip.  Block
 // arrays are padded to nBp = rem_padded_blocks(nB) rows (a multiple of 32;
 // padding rows zero).  Layouts per (b, h): kbar, vbar [nBp, D] bf16; moments
-// [nBp, D, D] bf16 with M[e][d] = sum_t V[t][e] (K[t][d] - kbar[d]); E [nBp,
-// nBp] bf16; r [nBp] float32; T [nBp, D, D] bf16.
+// [nBp, D, D] bf16 with M[e][d] = sum_t V[t][e] (K[t][d] - kbar[d]); E bf16
+// [nBp/32 chunks][nBr rows][32] (nBr = rem_weight_rows(nB); the 32 keys of a
+// chunk permuted so that each MFMA lane's eight values are one 16-byte piece);
+// r [nBp] float32; T [nBp, D, D] bf16.
 constexpr int kRemMaxBlocks = 4096;
+constexpr int kRemGemmRows = 256;   // rows i per workgroup of the T GEMM
 int rem_padded_blocks(int nB);
+// Rows of each 32-key chunk of E: nB rounded up to kRemGemmRows.
+int rem_weight_rows(int nB);
 struct RemMomentArgs {
   const uint16_t* k;
   const uint16_t* v;
@@ -98,14 +103,14 @@ struct RemWeightArgs {
   const int32_t* kv_count;
   uint16_t* E;
   float* r;
-  int nB, nBp, kmax;
+  int nB, nBp, nBr, kmax;
   float scale;        // c
 };
 struct RemGemmArgs {
   const uint16_t* E;
   const uint16_t* mom;
   uint16_t* T;
-  int nB, nBp, DD, n_wg;
+  int nB, nBp, nBr, DD, n_wg;   // n_wg: set by the launcher
 };
 struct RemAttnArgs {
   const uint16_t* q;
@@ -119,7 +124,7 @@ struct RemAttnArgs {
   const float* lse_a; // its LSE [B, H, N]
   void* out;
   float* lse;
-  int N, nB, nBp, kmax, n_rows;
+  int N, nB, nBp, kmax, n_rows;   // n_rows: workgroups, set by the launcher
   float scale;        // c
   float scale_log2;   // c * log2(e)
 };

@@ -139,10 +139,12 @@ def test_compute_entry_points_reject_before_launch(lib):
 
 def _remainder_bytes(B, H, N, D, S):
     up = lambda x: (x + 255) // 256 * 256
-    nbp = (-(-N // S) + 31) // 32 * 32
+    nb = -(-N // S)
+    nbp = (nb + 31) // 32 * 32
+    nbr = (nb + 255) // 256 * 256            # rows of each 32-key chunk of the weights
     bh = B * H
     return (up(bh * N * D * 4) + up(bh * N * 4) + 2 * up(bh * nbp * D * 2) + 2 * up(bh * nbp * D * D * 2)
-            + up(bh * nbp * nbp * 2) + up(bh * nbp * 4))
+            + up(bh * nbp * nbr * 2) + up(bh * nbp * 4))
 
 
 def test_remainder_workspace_and_rejects_before_launch(lib):
