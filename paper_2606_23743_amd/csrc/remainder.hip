@@ -427,10 +427,11 @@ void rem_gemm_kernel(RemGemmArgs a) {
 // kept and padding blocks), P rounded to bf16 with l summed from it,
 // O^T += Vbar^T P^T.  The reference
 // starts at max(LSE of the kept part, r_i) (log2 units) and moves up only
-// when a chunk's maximum passes it by more than 8, so it is rarely moved.  At
-// the end the first-order term exp(r_i) c T_i q is one MFMA pass with T_i rows
-// from global memory and Q^T from registers, and the kept-block result (O and
-// LSE in float32) is added with its weight exp(LSE) before the division.
+// when a chunk's maximum passes it by more than 8, so it is rarely moved.  The
+// first-order term exp(r_i) c T_i q (one MFMA pass, T_i rows from global
+// memory, Q^T from registers) and the kept-block result (O and LSE in
+// float32, weight exp(LSE)) are the starting numerator and row sum, so their
+// loads overlap the first chunks' and the end is one division.
 // ---------------------------------------------------------------------------
 template <int D, int S, bool OUT_F32>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
@@ -538,6 +539,40 @@ void rem_attn_kernel(RemAttnArgs a) {
   fetch(0, 0);
   fetch(1, 1);
   fetch(2, 2);
+
+  // The kept part and the first-order term enter as the starting numerator
+  // and row sum at the starting reference; the rescaling below moves them
+  // with the pooled keys' sums.  Numerator: exp2(LSE - m) O_kept +
+  // c exp2(r - m) T_i q (T_i rows e from global, one MFMA pass per 32-row
+  // tile); row sum: exp2(LSE - m), on one half of the lane pair.
+  {
+    const float l_a = __builtin_amdgcn_exp2f(lse_a * kLog2e - m_ref);   // 0 without a kept part
+    const float f1 = a.scale * __builtin_amdgcn_exp2f(r2 - m_ref);
+    const uint16_t* Ti = a.T + ((size_t)bh * nBp + i) * D * D;
+    const size_t obase = ((size_t)bh * N + (present ? qr : 0)) * D;
+#pragma unroll
+    for (int dt = 0; dt < G::DT; ++dt) {
+      const int e = dt * 32 + l32;
+      f32x16 tacc = f32x16{};
+#pragma unroll
+      for (int s = 0; s < G::DQ; ++s) {
+        const bf16x8 top = e < D ? *reinterpret_cast<const bf16x8*>(Ti + (size_t)e * D + s * 16 + hf * 8) : bf16x8{};
+        tacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(top, qop[s], tacc, 0, 0, 0);
+      }
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int d = dt * 32 + r4 * 8 + hf * 4;
+        float4 oa = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        if (present && d < D) oa = *reinterpret_cast<const float4*>(a.o_a + obase + d);
+        oacc[dt][r4 * 4 + 0] = __builtin_fmaf(f1, tacc[r4 * 4 + 0], l_a * oa.x);
+        oacc[dt][r4 * 4 + 1] = __builtin_fmaf(f1, tacc[r4 * 4 + 1], l_a * oa.y);
+        oacc[dt][r4 * 4 + 2] = __builtin_fmaf(f1, tacc[r4 * 4 + 2], l_a * oa.z);
+        oacc[dt][r4 * 4 + 3] = __builtin_fmaf(f1, tacc[r4 * 4 + 3], l_a * oa.w);
+      }
+    }
+    l_part = hf == 0 ? l_a : 0.0f;
+  }
+
   wait_vmcnt<2 * NUW * (PD - 1)>();
   wg_barrier();
   f32x16 sacc;
@@ -572,27 +607,8 @@ void rem_attn_kernel(RemAttnArgs a) {
   }
   wait_vmcnt<0>();
 
-  // first-order term: oacc += c exp2(r2 - m_ref) (T_i q), T_i rows e from global
-  const uint16_t* Ti = a.T + ((size_t)bh * nBp + i) * D * D;
-  const float f1 = a.scale * __builtin_amdgcn_exp2f(r2 - m_ref);
-#pragma unroll
-  for (int dt = 0; dt < G::DT; ++dt) {
-    const int e = dt * 32 + l32;
-    f32x16 tacc = f32x16{};
-#pragma unroll
-    for (int s = 0; s < G::DQ; ++s) {
-      const bf16x8 top = e < D ? *reinterpret_cast<const bf16x8*>(Ti + (size_t)e * D + s * 16 + hf * 8) : bf16x8{};
-      tacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(top, qop[s], tacc, 0, 0, 0);
-    }
-#pragma unroll
-    for (int r = 0; r < 16; ++r) oacc[dt][r] = __builtin_fmaf(f1, tacc[r], oacc[dt][r]);
-  }
-
-  // merge with the kept-block result and normalise
   const float l_tot = swap_halves_sum(l_part);
-  const float l_a = __builtin_amdgcn_exp2f(lse_a * kLog2e - m_ref);
-  const float den = l_tot + l_a;
-  const float inv = 1.0f / den;
+  const float inv = 1.0f / l_tot;
   if (!present) return;
   const size_t obase = ((size_t)bh * N + qr) * D;
 #pragma unroll
@@ -601,11 +617,8 @@ void rem_attn_kernel(RemAttnArgs a) {
     for (int r4 = 0; r4 < 4; ++r4) {
       const int d = dt * 32 + r4 * 8 + hf * 4;
       if (d < D) {
-        const float4 oa = *reinterpret_cast<const float4*>(a.o_a + obase + d);
-        const float o0 = __builtin_fmaf(l_a, oa.x, oacc[dt][r4 * 4 + 0]) * inv;
-        const float o1 = __builtin_fmaf(l_a, oa.y, oacc[dt][r4 * 4 + 1]) * inv;
-        const float o2 = __builtin_fmaf(l_a, oa.z, oacc[dt][r4 * 4 + 2]) * inv;
-        const float o3 = __builtin_fmaf(l_a, oa.w, oacc[dt][r4 * 4 + 3]) * inv;
+        const float o0 = oacc[dt][r4 * 4 + 0] * inv, o1 = oacc[dt][r4 * 4 + 1] * inv;
+        const float o2 = oacc[dt][r4 * 4 + 2] * inv, o3 = oacc[dt][r4 * 4 + 3] * inv;
         if constexpr (OUT_F32) {
           *reinterpret_cast<float4*>(static_cast<float*>(a.out) + obase + d) = make_float4(o0, o1, o2, o3);
         } else {
@@ -615,7 +628,7 @@ void rem_attn_kernel(RemAttnArgs a) {
         }
       }
     }
-  if (a.lse && hf == 0) a.lse[(size_t)bh * N + qr] = (m_ref + __log2f(den)) * kLn2;
+  if (a.lse && hf == 0) a.lse[(size_t)bh * N + qr] = (m_ref + __log2f(l_tot)) * kLn2;
 }
 
 template <int D, int S>
