@@ -51,8 +51,11 @@ __global__ __launch_bounds__(256) void rem_moments_kernel(RemMomentArgs a) {
   constexpr int PIECES = S * G::DCH;         // 16-byte pieces of one tensor's block
   constexpr int TILES = G::DT * G::DT;
   constexpr int TPW = (TILES + 3) / 4;       // output tiles per wave
-  __shared__ __attribute__((aligned(1024))) unsigned char Kt[NCHK][CT];
-  __shared__ __attribute__((aligned(1024))) unsigned char Vt[NCHK][CT];
+  // K and V tiles in one array: after the products it holds M for the store
+  __shared__ __attribute__((aligned(1024))) unsigned char KVt[2][NCHK][CT];
+  static_assert(2 * NCHK * CT >= D * D * 2, "M staging");
+  unsigned char (*Kt)[CT] = KVt[0];
+  unsigned char (*Vt)[CT] = KVt[1];
   __shared__ float kmean[D];
   __shared__ float part[2][4][D];
 
@@ -171,6 +174,10 @@ __global__ __launch_bounds__(256) void rem_moments_kernel(RemMomentArgs a) {
                                                            tr_operand<D>(&Kt[ch][0], db, kk), acc[x], 0, 0, 0);
     }
   }
+  // M through LDS (row e, D bf16 per row) so that the global stores are
+  // whole 16-byte pieces of consecutive rows
+  __syncthreads();                           // every wave is done with the tiles
+  uint16_t* Ms = reinterpret_cast<uint16_t*>(&KVt[0][0][0]);
 #pragma unroll
   for (int x = 0; x < TPW; ++x) {
     const int tile = w + 4 * x;
@@ -180,10 +187,13 @@ __global__ __launch_bounds__(256) void rem_moments_kernel(RemMomentArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int e = et * 32 + (r >> 2) * 8 + hf * 4 + (r & 3);
-        if (e < D && d < D) mom[(size_t)e * D + d] = bf16_bits(acc[x][r]);
+        if (e < D && d < D) Ms[e * D + d] = bf16_bits(acc[x][r]);
       }
     }
   }
+  __syncthreads();
+  for (int p = tid; p < D * D / 8; p += NT)
+    reinterpret_cast<uint4*>(mom)[p] = reinterpret_cast<const uint4*>(Ms)[p];
 }
 
 // ---------------------------------------------------------------------------
