@@ -1,12 +1,14 @@
 """GPU parity at the size limits of the boundary: 2048 key blocks per row (the
 most the selection kernel holds in registers) in both selection modes, with
-attention on sampled query blocks in bf16 and fp8, and fp8 dense attention at
-2047 blocks (the longest kept-block list the fp8 kernel holds in LDS)."""
+attention on sampled query blocks in bf16 and fp8, fp8 dense attention at
+2047 blocks (the longest kept-block list the fp8 kernel holds in LDS), and
+4096 blocks for the block-pair kernel and the first-order remainder."""
 import numpy as np
 import pytest
 
 import oracle
 import oracle.fp8_attention as of8
+import oracle.remainder as orem
 import paper_2606_23743_amd as sva
 from paper_2606_23743_amd import inputs, workloads
 
@@ -113,6 +115,43 @@ def test_block_pairs_at_4096_blocks():
         assert mx <= parity.MAX_ABS and mean <= parity.MEAN_ABS, (i, mx, mean)
         assert np.all(np.abs(lse.cpu().numpy()[0, 0, sl] - rlse[0, 0, sl]) <= parity.LSE_TOL), i
     say(f"[limits nb4096 pairs] rows {rows} within the parity bounds")
+
+
+def test_remainder_at_4096_blocks():
+    """The first-order remainder at its largest block count, nB = 4096 (128
+    bitmap words per row, no padding rows, 4096-row weight chunks), on the
+    oracle's lists, sampled rows (first and last included) against the
+    oracle with the remainder's bounds."""
+    wl = SC("nb4096_remainder", 1, 1, 128, (4, 256, 256), 64, "topk", keep_ratio=0.05, seed=215)
+    bits = inputs.generate(wl)
+    dev = device_inputs(bits)
+    prob = sva.problem_for(wl)
+    nb = sva.num_blocks(prob)
+    assert nb == 4096
+    f64 = {n: oracle.bf16_bits_to_f64(bits[n]) for n in ("q", "k", "v")}
+    scores = oracle.block_scores(oracle.pool_blocks(f64["q"], wl.block), oracle.pool_blocks(f64["k"], wl.block),
+                                 scale_of(wl))
+    kept, _ = oracle_select(wl, scores)
+    oidx, ocnt = _kept_arrays(kept, nb)
+    qp, kp = sva.pool_blocks(prob, dev["q"], dev["k"])
+    out, lse = sva.sparse_attention_remainder(prob, dev["q"], dev["k"], dev["v"], qp, kp, oidx, ocnt, want_lse=True)
+    torch.cuda.synchronize()
+    rows = [0, 1, 2047, 4094, 4095]
+    c = scale_of(wl)
+    ref, rlse = orem.remainder_attention(f64["q"], f64["k"], f64["v"], kept, wl.block, c,
+                                         rows=[(0, 0, i) for i in rows])
+    ref0, _ = orem.remainder_attention(f64["q"], f64["k"], f64["v"], kept, wl.block, c,
+                                       rows=[(0, 0, i) for i in rows], first_order=False)
+    o = out.float().cpu().numpy()
+    kbar = oracle.pool_blocks(f64["k"][0, 0], wl.block)
+    for i in rows:
+        sl = slice(i * wl.block, (i + 1) * wl.block)
+        excess, mean, mean_bound = parity.remainder_errors(o[0, 0, sl], ref[0, 0, sl], ref[0, 0, sl] - ref0[0, 0, sl],
+                                                           True)
+        assert excess <= 0.0 and mean <= mean_bound, (i, excess, mean, mean_bound)
+        bound = parity.remainder_lse_bound(f64["q"][0, 0, sl], kbar, c)
+        assert np.all(np.abs(lse.cpu().numpy()[0, 0, sl] - rlse[0, 0, sl]) <= bound), i
+    say(f"[limits nb4096 remainder] rows {rows} within the remainder bounds")
 
 
 def test_fp8_dense_at_2047_blocks():
