@@ -13,14 +13,15 @@
 //                       operands by transpose reads of LDS tiles
 //   rem_weights_kernel  per query block i: r_i = max_j c qbar_i.kbar_j and
 //                       E[i][j] = exp(c qbar_i.kbar_j - r_i) for the dropped j,
-//                       0 for kept and padding columns (bf16)
+//                       0 for kept and padding columns (bf16, chunk-blocked)
 //   rem_gemm_kernel     T_i = sum_j E[i][j] M_j: per head one GEMM of E
 //                       [nB x nB] with the flattened moments [nB x D*D] (MFMA,
-//                       M tiles staged in LDS by direct loads, E from global)
-//   rem_attn_kernel     per query block: an online softmax over the nB pooled
-//                       keys kbar_j with weight n_j (kept and padding blocks
-//                       masked), values vbar_j; then exp(r_i) c T_i q, and the
-//                       merge with the kept-block result (float32 O and LSE)
+//                       M and E tiles staged in LDS by direct loads)
+//   rem_attn_kernel     per 128 queries: the kept-block result (float32 O and
+//                       LSE) and exp(r_i) c T_i q as the starting numerator,
+//                       then an online softmax over the nB pooled keys kbar_j
+//                       with weight n_j (kept and padding blocks masked),
+//                       values vbar_j
 #include "attn_wave32.h"
 
 namespace sva {
@@ -519,27 +520,35 @@ void rem_attn_kernel(RemAttnArgs a) {
   constexpr int NST = 4, PD = 3;
   const int nch = nBp / 32;
   auto fetch = [&](int st, int ch) { load_chunk(ld, st, ch < nch ? ch * 32 : 0); };
-  // logits in log2 units plus log2 n_j, -inf for kept and padding blocks;
-  // every block but the last has n_j = S, so only the last block's chunk
-  // takes the general form
+  // x = logit in log2 units + log2 n_j - m_ref (-inf for kept and padding
+  // blocks), so the exponential takes x as it is.  The chunk's mask word is
+  // the same for the whole wave (one query block per wave): the condition of
+  // register r -- bit jj of the word for lanes 0..31, bit jj + 4 for lanes
+  // 32..63 -- is a scalar lane mask, and each logit costs a select, an FMA
+  // and a max.  Every block but the last has n_j = S; the last block's chunk
+  // takes the general form.
   const int last_ch = (nB - 1) / 32;
   auto masked = [&](f32x16& x, int ch) {
-    const uint32_t word = bm[ch] >> (hf * 4);
+    const uint32_t word = __builtin_amdgcn_readfirstlane(bm[ch]);
     float mx = -INFINITY;
     if (ch != last_ch) {
+      const float bias = log2_s - m_ref;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int jj = (r >> 2) * 8 + (r & 3);           // key within the chunk, less hf*4
-        const float b = ((word >> jj) & 1u) ? -INFINITY : log2_s;
-        x[r] = __builtin_fmaf(x[r], sl2, b);
+        const uint64_t lanes = (((word >> jj) & 1u) ? 0x00000000FFFFFFFFull : 0ull) |
+                               (((word >> (jj + 4)) & 1u) ? 0xFFFFFFFF00000000ull : 0ull);
+        const float y = __builtin_fmaf(x[r], sl2, bias);
+        x[r] = __builtin_amdgcn_inverse_ballot_w64(lanes) ? -INFINITY : y;
         mx = fmaxf(mx, x[r]);
       }
     } else {
+      const uint32_t mine = word >> (hf * 4);
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int jj = (r >> 2) * 8 + (r & 3);
         const int j = ch * 32 + hf * 4 + jj;
-        const float b = ((word >> jj) & 1u) ? -INFINITY : (j == nB - 1 ? log2_last : log2_s);
+        const float b = ((mine >> jj) & 1u) ? -INFINITY : (j == nB - 1 ? log2_last : log2_s) - m_ref;
         x[r] = __builtin_fmaf(x[r], sl2, b);
         mx = fmaxf(mx, x[r]);
       }
@@ -597,20 +606,22 @@ void rem_attn_kernel(RemAttnArgs a) {
       fetch((c + PD) % NST, ch + PD);
       f32x16 snext;
       qk_chunk<D>(snext, &Ks[(c + 1) % NST][0], koff, qop);
-      const float mx = masked(sacc, ch);
-      if (__builtin_amdgcn_ballot_w64(mx > m_ref + 8.0f) != 0) {
-        if (mx > m_ref + 8.0f) {
-          const float f = __builtin_amdgcn_exp2f(m_ref - mx);
+      const float mx = masked(sacc, ch);             // relative to m_ref
+      if (__builtin_amdgcn_ballot_w64(mx > 8.0f) != 0) {
+        if (mx > 8.0f) {
+          const float f = __builtin_amdgcn_exp2f(-mx);
           l_part *= f;
 #pragma unroll
           for (int dt = 0; dt < G::DT; ++dt)
 #pragma unroll
             for (int r = 0; r < 16; ++r) oacc[dt][r] *= f;
-          m_ref = mx;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) sacc[r] -= mx;
+          m_ref += mx;
         }
       }
       bf16x8 pop[2];
-      softmax_chunk(sacc, pop, l_part, m_ref, 1.0f);
+      softmax_chunk(sacc, pop, l_part, 0.0f, 1.0f);
       pv_chunk<D>(pop, &Vs[c][0], voff, oacc);
       sacc = snext;
     }
