@@ -180,7 +180,12 @@ void attn_q32_kernel(AttnArgs a) {
         bf16x8 pop[2];
         qk(snext, &Ks[(c + 1) % NST][0]);
         softmax(sacc, pop);
+        // The PV products issue at raised wave priority, ahead of the other
+        // wave's softmax on the SIMD: measured 1.5-2.5% faster at the 64B-class
+        // layer (raising it for the S products or the softmax was slower).
+        __builtin_amdgcn_s_setprio(1);
         pv(pop, &Vs[c][0]);
+        __builtin_amdgcn_s_setprio(0);
         const int nvalid = __builtin_amdgcn_readfirstlane(N - nkey0);
         if (nvalid < CK) {
           asm volatile("");        // keep this a real (rarely taken) branch, not select code
