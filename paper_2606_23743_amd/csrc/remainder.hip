@@ -203,7 +203,7 @@ __global__ __launch_bounds__(256) void rem_moments_kernel(RemMomentArgs a) {
 // kept sets as LDS bitmaps, then two passes over the key blocks (row maxima,
 // then the weights), each thread taking key blocks tid, tid + 256, ...
 // ---------------------------------------------------------------------------
-constexpr int kRemRows = 32;
+constexpr int kRemRows = 16;
 
 // Position of key jj (0..31) of a chunk in a row of E: the eight keys one MFMA
 // lane takes for (kk, hf) -- kk*16 + hf*4 + 0..3, then kk*16 + 8 + hf*4 + 0..3,
