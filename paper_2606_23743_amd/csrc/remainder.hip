@@ -199,9 +199,9 @@ __global__ __launch_bounds__(256) void rem_moments_kernel(RemMomentArgs a) {
 
 // ---------------------------------------------------------------------------
 // First-order weights.  kRemRows query blocks of one head per workgroup (each
-// pooled key row a thread loads serves all of them): the
-// kept sets as LDS bitmaps, then two passes over the key blocks (row maxima,
-// then the weights), each thread taking key blocks tid, tid + 256, ...
+// pooled key row a thread loads serves all of them): the kept sets as LDS
+// bitmaps, then two passes over the key blocks (row maxima, then the
+// weights), each thread taking key blocks tid, tid + 256, ...
 // ---------------------------------------------------------------------------
 constexpr int kRemRows = 16;
 
@@ -436,13 +436,13 @@ void rem_gemm_kernel(RemGemmArgs a) {
 // differ).  The pooled keys kbar_j of the head are walked in 32-row chunks
 // (four LDS stages): S^T = Kbar Q^T, logit + log2 n_j in log2 units (-inf for
 // kept and padding blocks), P rounded to bf16 with l summed from it,
-// O^T += Vbar^T P^T.  The reference
-// starts at max(LSE of the kept part, r_i) (log2 units) and moves up only
-// when a chunk's maximum passes it by more than 8, so it is rarely moved.  The
-// first-order term exp(r_i) c T_i q (one MFMA pass, T_i rows from global
-// memory, Q^T from registers) and the kept-block result (O and LSE in
-// float32, weight exp(LSE)) are the starting numerator and row sum, so their
-// loads overlap the first chunks' and the end is one division.
+// O^T += Vbar^T P^T.  The reference starts at max(LSE of the kept part, r_i)
+// (log2 units) and moves up only when a chunk's maximum passes it by more
+// than 8, so it is rarely moved.  The first-order term exp(r_i) c T_i q (one
+// MFMA pass, T_i rows from global memory, Q^T from registers) and the
+// kept-block result (O and LSE in float32, weight exp(LSE)) are the starting
+// numerator and row sum, so their loads overlap the first chunks' and the
+// end is one division.
 // ---------------------------------------------------------------------------
 template <int D, int S, bool OUT_F32>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
