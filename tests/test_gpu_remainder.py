@@ -174,3 +174,32 @@ def test_workspace_is_reusable_and_sized_by_the_call():
         assert torch.equal(o, fresh), wl.name
         outs.append(o)
     assert outs[1].shape[2] == wl2.seq_len
+
+
+def test_custom_softmax_scale():
+    """A softmax scale other than 1/sqrt(D) reaches every place the remainder
+    uses it: the first-order weights, the pooled-key logits and the c M q
+    factor."""
+    wl = SC("rem_scale", 1, 2, 64, (3, 10, 13), 64, "topk", keep_ratio=0.2, seed=310)
+    c = 0.21
+    bits = inputs.generate(wl)
+    dev = device_inputs(bits)
+    prob = sva.problem_for(wl, out_dtype="f32", softmax_scale=c)
+    nb = sva.num_blocks(prob)
+    kept = _oracle_lists(wl, bits)
+    idx, cnt = _arrays(kept, nb)
+    qp, kp = sva.pool_blocks(prob, dev["q"], dev["k"])
+    out, lse = sva.sparse_attention_remainder(prob, dev["q"], dev["k"], dev["v"], qp, kp, idx, cnt, want_lse=True)
+    torch.cuda.synchronize()
+    got, glse = out.cpu().numpy(), lse.cpu().numpy()
+    for h in range(wl.heads):
+        f = {n: oracle.bf16_bits_to_f64(bits[n][0, h])[None, None] for n in ("q", "k", "v")}
+        ref, rlse = orem.remainder_attention(f["q"], f["k"], f["v"], [[kept[0][h]]], wl.block, c)
+        ref0, _ = orem.remainder_attention(f["q"], f["k"], f["v"], [[kept[0][h]]], wl.block, c, first_order=False)
+        excess, mean, mean_bound = parity.remainder_errors(got[0, h], ref[0, 0], ref[0, 0] - ref0[0, 0], False)
+        assert excess <= 0.0 and mean <= mean_bound, (h, excess, mean, mean_bound)
+        bound = parity.remainder_lse_bound(f["q"][0, 0], oracle.pool_blocks(f["k"][0, 0], wl.block), c)
+        assert np.all(np.abs(glse[0, h] - rlse[0, 0]) <= bound), h
+        # and the scale matters: the result at 1/sqrt(D) is far from this one
+        other, _ = orem.remainder_attention(f["q"], f["k"], f["v"], [[kept[0][h]]], wl.block, scale_of(wl))
+        assert np.abs(other[0, 0] - ref[0, 0]).max() > 10 * parity.MAX_ABS
