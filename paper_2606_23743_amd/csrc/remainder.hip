@@ -438,11 +438,10 @@ void rem_gemm_kernel(RemGemmArgs a) {
 // kept and padding blocks), P rounded to bf16 with l summed from it,
 // O^T += Vbar^T P^T.  The reference starts at max(LSE of the kept part, r_i)
 // (log2 units) and moves up only when a chunk's maximum passes it by more
-// than 8, so it is rarely moved.  The first-order term exp(r_i) c T_i q (one
-// MFMA pass, T_i rows from global memory, Q^T from registers) and the
-// kept-block result (O and LSE in float32, weight exp(LSE)) are the starting
-// numerator and row sum, so their loads overlap the first chunks' and the
-// end is one division.
+// than 8, so it is rarely moved.  The first-order term exp(r_i) c T_i q (the
+// rows of T_i staged as the first chunks of the pipeline, S step against
+// Q^T) and the kept-block result (O and LSE in float32, weight exp(LSE)) are
+// the starting numerator and row sum, so the end is one division.
 // ---------------------------------------------------------------------------
 template <int D, int S, bool OUT_F32>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
@@ -512,14 +511,37 @@ void rem_attn_kernel(RemAttnArgs a) {
   const float log2_s = S == 128 ? 7.0f : 6.0f;
   const float log2_last = __log2f((float)(N - (nB - 1) * S));
 
-  // Pipeline over the pooled-key chunks: four LDS stages (chunk x in stage
-  // x % 4), loads three chunks ahead, and the S products of the next chunk
-  // issued alongside this chunk's softmax, as in the 32-query kernel.  Each
-  // iteration issues one load group (chunk 0 again past the end), so the wait
-  // counts are constants.
+  // Pipeline over one sequence of 32-row chunks: first the G::DT row tiles of
+  // T_i of each query block of the workgroup (the S step with T's rows as
+  // keys gives T_i q in the numerator's layout; a wave computes only on its
+  // own block's tiles), then the nch pooled-key chunks.  Four LDS stages
+  // (chunk g in stage g % 4), loads three chunks ahead by direct loads, and
+  // in the pooled part the S products of the next chunk issued alongside
+  // this chunk's softmax, as in the 32-query kernel.  Each chunk issues one
+  // load group (a T tile with a dummy V tile; chunk 0 again past the end), so
+  // the wait counts are constants.
   constexpr int NST = 4, PD = 3;
+  constexpr int NTC = NQB * G::DT;           // T tiles ahead of the pooled chunks
   const int nch = nBp / 32;
-  auto fetch = [&](int st, int ch) { load_chunk(ld, st, ch < nch ? ch * 32 : 0); };
+  ChunkLoader<D, NUW, CT> tl[NQB];           // T_i of each block: D rows of D, like a K tile
+#pragma unroll
+  for (int b2 = 0; b2 < NQB; ++b2) {
+    const uint16_t* Tb = a.T + ((size_t)bh * nBp + min(ib0 + b2, nB - 1)) * D * D;
+    loader_init(tl[b2], Tb, Tb, D, &Ks[0][0], &Vs[0][0], w, lane);
+  }
+  auto fetch_pooled = [&](int st, int g) {
+    const int ch = g - NTC;
+    load_chunk(ld, st, ch < nch ? ch * 32 : 0);
+  };
+  // chunk g with g a compile-time constant (the T part, fully unrolled)
+  auto fetch_const = [&](int st, int g) {
+    if (g < NTC) {
+      load_tile<true>(tl[g / G::DT], st, (g % G::DT) * 32);
+      load_tile<false>(ld, st, 0);
+    } else {
+      fetch_pooled(st, g);
+    }
+  };
   // x = logit in log2 units + log2 n_j - m_ref (-inf for kept and padding
   // blocks), so the exponential takes x as it is.  The chunk's mask word is
   // the same for the whole wave (one query block per wave): the condition of
@@ -555,47 +577,54 @@ void rem_attn_kernel(RemAttnArgs a) {
     }
     return swap_halves_max(mx);
   };
-  fetch(0, 0);
-  fetch(1, 1);
-  fetch(2, 2);
-
   // The kept part and the first-order term enter as the starting numerator
   // and row sum at the starting reference; the rescaling below moves them
-  // with the pooled keys' sums.  Numerator: exp2(LSE - m) O_kept +
-  // c exp2(r - m) T_i q (T_i rows e from global, one MFMA pass per 32-row
-  // tile); row sum: exp2(LSE - m), on one half of the lane pair.
+  // with the pooled keys' sums.  Numerator: exp2(LSE - m) O_kept (its loads
+  // issued first) + c exp2(r - m) T_i q (the T tiles); row sum:
+  // exp2(LSE - m), on one half of the lane pair.
+  const float l_a = __builtin_amdgcn_exp2f(lse_a * kLog2e - m_ref);   // 0 without a kept part
+  const float f1 = a.scale * __builtin_amdgcn_exp2f(r2 - m_ref);
+  float4 oa[G::DT][4];
   {
-    const float l_a = __builtin_amdgcn_exp2f(lse_a * kLog2e - m_ref);   // 0 without a kept part
-    const float f1 = a.scale * __builtin_amdgcn_exp2f(r2 - m_ref);
-    const uint16_t* Ti = a.T + ((size_t)bh * nBp + i) * D * D;
     const size_t obase = ((size_t)bh * N + (present ? qr : 0)) * D;
 #pragma unroll
-    for (int dt = 0; dt < G::DT; ++dt) {
-      const int e = dt * 32 + l32;
-      f32x16 tacc = f32x16{};
-#pragma unroll
-      for (int s = 0; s < G::DQ; ++s) {
-        const bf16x8 top = e < D ? *reinterpret_cast<const bf16x8*>(Ti + (size_t)e * D + s * 16 + hf * 8) : bf16x8{};
-        tacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(top, qop[s], tacc, 0, 0, 0);
-      }
+    for (int dt = 0; dt < G::DT; ++dt)
 #pragma unroll
       for (int r4 = 0; r4 < 4; ++r4) {
         const int d = dt * 32 + r4 * 8 + hf * 4;
-        float4 oa = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-        if (present && d < D) oa = *reinterpret_cast<const float4*>(a.o_a + obase + d);
-        oacc[dt][r4 * 4 + 0] = __builtin_fmaf(f1, tacc[r4 * 4 + 0], l_a * oa.x);
-        oacc[dt][r4 * 4 + 1] = __builtin_fmaf(f1, tacc[r4 * 4 + 1], l_a * oa.y);
-        oacc[dt][r4 * 4 + 2] = __builtin_fmaf(f1, tacc[r4 * 4 + 2], l_a * oa.z);
-        oacc[dt][r4 * 4 + 3] = __builtin_fmaf(f1, tacc[r4 * 4 + 3], l_a * oa.w);
+        oa[dt][r4] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        if (present && d < D) oa[dt][r4] = *reinterpret_cast<const float4*>(a.o_a + obase + d);
       }
+  }
+#pragma unroll
+  for (int g = 0; g < PD; ++g) fetch_const(g, g);
+#pragma unroll
+  for (int dt = 0; dt < G::DT; ++dt)
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4) {
+      oacc[dt][r4 * 4 + 0] = l_a * oa[dt][r4].x;
+      oacc[dt][r4 * 4 + 1] = l_a * oa[dt][r4].y;
+      oacc[dt][r4 * 4 + 2] = l_a * oa[dt][r4].z;
+      oacc[dt][r4 * 4 + 3] = l_a * oa[dt][r4].w;
     }
-    l_part = hf == 0 ? l_a : 0.0f;
+  l_part = hf == 0 ? l_a : 0.0f;
+#pragma unroll
+  for (int g = 0; g < NTC; ++g) {            // chunk g: T tile g % DT of block g / DT
+    wait_vmcnt_lds_idle<2 * NUW * (PD - 1)>();       // chunk g landed
+    wg_barrier();                                   // every wave's; the stage of chunk g-1 is free
+    fetch_const((g + PD) % NST, g + PD);
+    if (g / G::DT == qb) {
+      f32x16 tacc;
+      qk_chunk<D>(tacc, &Ks[g % NST][0], koff, qop);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) oacc[g % G::DT][r] = __builtin_fmaf(f1, tacc[r], oacc[g % G::DT][r]);
+    }
   }
 
-  wait_vmcnt<2 * NUW * (PD - 1)>();
+  wait_vmcnt_lds_idle<2 * NUW * (PD - 1)>();         // pooled chunk 0 landed
   wg_barrier();
   f32x16 sacc;
-  qk_chunk<D>(sacc, &Ks[0][0], koff, qop);
+  qk_chunk<D>(sacc, &Ks[NTC % NST][0], koff, qop);
   for (int ch0 = 0; ch0 < nch; ch0 += NST) {
 #pragma unroll
     for (int c = 0; c < NST; ++c) {
@@ -603,9 +632,9 @@ void rem_attn_kernel(RemAttnArgs a) {
       if (ch >= nch) break;
       wait_vmcnt_lds_idle<2 * NUW * (PD - 2)>();     // chunk ch+1 landed
       wg_barrier();
-      fetch((c + PD) % NST, ch + PD);
+      fetch_pooled((NTC + c + PD) % NST, NTC + ch + PD);
       f32x16 snext;
-      qk_chunk<D>(snext, &Ks[(c + 1) % NST][0], koff, qop);
+      qk_chunk<D>(snext, &Ks[(NTC + c + 1) % NST][0], koff, qop);
       const float mx = masked(sacc, ch);             // relative to m_ref
       if (__builtin_amdgcn_ballot_w64(mx > 8.0f) != 0) {
         if (mx > 8.0f) {
@@ -622,7 +651,7 @@ void rem_attn_kernel(RemAttnArgs a) {
       }
       bf16x8 pop[2];
       softmax_chunk(sacc, pop, l_part, 0.0f, 1.0f);
-      pv_chunk<D>(pop, &Vs[c][0], voff, oacc);
+      pv_chunk<D>(pop, &Vs[(NTC + c) % NST][0], voff, oacc);
       sacc = snext;
     }
   }
