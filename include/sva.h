@@ -216,8 +216,9 @@ int sva_remainder_workspace(const sva_problem* prob, size_t* bytes);
  *              valid tokens (float32 sum, rounded once)
  *   vbar     : bf16 [B, H, nB, D] device, written: the same for V
  *   moments  : bf16 [B, H, nB, D, D] device, written: M_j[e][d] (d fastest),
- *              from K - kbar rounded to bf16 (kbar in float32), products
- *              accumulated in float32, rounded once
+ *              computed as sum_t V[t][e] K[t][d] - (sum_t V[t][e]) (sum_t
+ *              K[t][d]) / n_j from the exact bf16 products with float32 sums,
+ *              rounded once
  * All pointers 16-byte aligned. */
 int sva_block_moments(const sva_problem* prob, const void* k, const void* v, void* kbar,
                       void* vbar, void* moments, void* stream);

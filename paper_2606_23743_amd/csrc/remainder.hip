@@ -37,11 +37,16 @@ __device__ __forceinline__ uint16_t bf16_bits(float x) { return __builtin_bit_ca
 // ---------------------------------------------------------------------------
 // Block means and moments.  One workgroup (4 waves) per (b, h, key block j);
 // rows j >= nB (padding up to `rows`) are written as zeros.  The block's K and
-// V are staged as 32-row V-swizzled tiles; K is replaced in place by K - kbar
-// (rows past the block's end stay zero).  M = V^T (K - kbar): the A operand is
-// the transpose read of the V tile at column tile et, the B operand the same
-// read of the centred K tile at column tile dt, so M[e][d] lands with d along
-// the lanes.  Wave w takes the (et, dt) tiles with (et*DT + dt) % 4 == w.
+// V rows are staged by direct loads as 32-row V-swizzled tiles (rows past the
+// block's end zeroed), then, on MFMA with both operands from the LDS
+// transpose read:
+//   P = V^T K             tile (et, dt): A = the V tile at et, B = the K tile at dt
+//   sv = V^T 1, sk = 1^T K   the same reads against an all-ones operand: sv
+//                            lands in P's row layout, sk in its column layout
+//   M = P - sv sk^T / n,  kbar = sk / n,  vbar = sv / n
+// so the means and the moment come from one pass over exact bf16 products with
+// float32 sums.  Wave w takes the (et, dt) tiles with (et*DT + dt) % 4 == w;
+// at DT = 4 its column tile dt = w is fixed.
 // ---------------------------------------------------------------------------
 template <int D, int S>
 __global__ __launch_bounds__(256) void rem_moments_kernel(RemMomentArgs a) {
@@ -49,16 +54,15 @@ __global__ __launch_bounds__(256) void rem_moments_kernel(RemMomentArgs a) {
   constexpr int NT = 256;
   constexpr int NCHK = S / 32;               // 32-row tiles per block
   constexpr int CT = 32 * G::RB;
-  constexpr int PIECES = S * G::DCH;         // 16-byte pieces of one tensor's block
+  constexpr int NUW = CT / 1024 / 4;         // direct-load pieces per wave per tile
   constexpr int TILES = G::DT * G::DT;
   constexpr int TPW = (TILES + 3) / 4;       // output tiles per wave
+  static_assert(NUW >= 1, "tile split");
   // K and V tiles in one array: after the products it holds M for the store
   __shared__ __attribute__((aligned(1024))) unsigned char KVt[2][NCHK][CT];
   static_assert(2 * NCHK * CT >= D * D * 2, "M staging");
   unsigned char (*Kt)[CT] = KVt[0];
   unsigned char (*Vt)[CT] = KVt[1];
-  __shared__ float kmean[D];
-  __shared__ float part[2][4][D];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -83,98 +87,82 @@ __global__ __launch_bounds__(256) void rem_moments_kernel(RemMomentArgs a) {
   const int n = min(S, a.N - t0);
   const uint16_t* Kb = a.k + ((size_t)bh * a.N + t0) * D;
   const uint16_t* Vb = a.v + ((size_t)bh * a.N + t0) * D;
-  auto tile_off = [](int t, int c) { return (t >> 5) * CT + (t & 31) * G::RB + (swz_v<G::NCH>(t & 31, c) << 4); };
 
-  // Thread (g, c) takes the 16-byte column piece c (of the NCH pieces of an
-  // LDS row; pieces past D are idle) of rows g, g + NG, ...: rows are read
-  // whole by consecutive threads, and each thread keeps the float32 sums of
-  // its eight columns.  The lanes of a wave that share c are NCH apart, so a
-  // fixed XOR-shuffle tree adds them, and the four waves' sums are added in
-  // order: the means are reproducible.
-  constexpr int NG = NT / G::NCH;            // row groups
-  const int g = tid / G::NCH, c = tid - g * G::NCH;
-  float ks[8] = {}, vs[8] = {};
-  if (c < G::DCH) {
-    for (int t = g; t < S; t += NG) {
-      uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-      if (t < n) {
-        kv = *reinterpret_cast<const uint4*>(Kb + (size_t)t * D + c * 8);
-        vv = *reinterpret_cast<const uint4*>(Vb + (size_t)t * D + c * 8);
-      }
-      *reinterpret_cast<uint4*>(&Kt[0][0] + tile_off(t, c)) = kv;
-      *reinterpret_cast<uint4*>(&Vt[0][0] + tile_off(t, c)) = vv;
-      const bf16x8 kx = __builtin_bit_cast(bf16x8, kv), vx = __builtin_bit_cast(bf16x8, vv);
+  // Both tensors with the V swizzle (the loader's second tensor path): rows
+  // of a partial block past its end read an earlier row, zeroed below.
+  ChunkLoader<D, NUW, CT> lk, lv;
+  loader_init(lk, Kb, Kb, n, &Kt[0][0], &Kt[0][0], w, lane);
+  loader_init(lv, Vb, Vb, n, &Vt[0][0], &Vt[0][0], w, lane);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        ks[e] += (float)kx[e];
-        vs[e] += (float)vx[e];
-      }
-    }
+  for (int ch = 0; ch < NCHK; ++ch) {
+    load_tile<false>(lk, ch, ch * 32);
+    load_tile<false>(lv, ch, ch * 32);
   }
-#pragma unroll
-  for (int off = G::NCH; off < 64; off <<= 1)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      ks[e] += __shfl_xor(ks[e], off, 64);
-      vs[e] += __shfl_xor(vs[e], off, 64);
-    }
-  if (lane < G::DCH) {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      part[0][w][lane * 8 + e] = ks[e];
-      part[1][w][lane * 8 + e] = vs[e];
-    }
-  }
+  wait_vmcnt<0>();
   __syncthreads();
-  if (tid < 2 * D) {                         // threads 0..D-1 take K, D..2D-1 V
-    const int kv = tid < D ? 0 : 1;
-    const int d = tid - kv * D;
-    float s = 0.0f;
-    for (int q = 0; q < 4; ++q) s += part[kv][q][d];
-    s /= (float)n;
-    if (kv == 0) {
-      kmean[d] = s;
-      kbar[d] = bf16_bits(s);
-    } else {
-      vbar[d] = bf16_bits(s);
+  if (n < S) {
+    for (int p = tid; p < (S - n) * G::NCH; p += NT) {
+      const int t = n + p / G::NCH, c = p % G::NCH;
+      const int off = (t >> 5) * CT + (t & 31) * G::RB + c * 16;
+      *reinterpret_cast<uint4*>(&Kt[0][0] + off) = make_uint4(0, 0, 0, 0);
+      *reinterpret_cast<uint4*>(&Vt[0][0] + off) = make_uint4(0, 0, 0, 0);
     }
+    __syncthreads();
   }
-  __syncthreads();
 
-  // K - kbar in place, rounded to bf16 (rows past the block's end stay zero)
-  for (int p = tid; p < PIECES; p += NT) {
-    const int t = p / G::DCH, c = p - (p / G::DCH) * G::DCH;
-    if (t >= n) continue;
-    uint4* slot = reinterpret_cast<uint4*>(&Kt[0][0] + tile_off(t, c));
-    const bf16x8 x = __builtin_bit_cast(bf16x8, *slot);
-    u32x4 y;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float a0 = (float)x[2 * e] - kmean[c * 8 + 2 * e];
-      const float a1 = (float)x[2 * e + 1] - kmean[c * 8 + 2 * e + 1];
-      y[e] = __builtin_bit_cast(unsigned, cvt2(a0, a1));
-    }
-    *slot = __builtin_bit_cast(uint4, y);
-  }
-  __syncthreads();
-
-  f32x16 acc[TPW];
+  const u32x4 one_bits = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};   // bf16 1.0 x 8
+  const bf16x8 ones = __builtin_bit_cast(bf16x8, one_bits);
+  static_assert(4 % G::DT == 0, "a wave's column tile is fixed");
+  const int dtw = w % G::DT;                 // this wave's column tile
+  const int db = tr_offset<D>(lane, dtw);
+  f32x16 acc[TPW], sk = f32x16{};
 #pragma unroll
   for (int x = 0; x < TPW; ++x) acc[x] = f32x16{};
+#pragma unroll
+  for (int ch = 0; ch < NCHK; ++ch)
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const bf16x8 kb = tr_operand<D>(&Kt[ch][0], db, kk);
+      sk = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ones, kb, sk, 0, 0, 0);
+#pragma unroll
+      for (int x = 0; x < TPW; ++x) {
+        const int tile = w + 4 * x;
+        if (tile < TILES) {
+          const int et = tile / G::DT;
+          acc[x] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand<D>(&Vt[ch][0], tr_offset<D>(lane, et), kk), kb,
+                                                           acc[x], 0, 0, 0);
+        }
+      }
+    }
+  const float inv_n = 1.0f / (float)n;
+  // means: the K sums of columns dtw*32 .. (written by the wave with et = 0),
+  // and per tile the V sums of its rows (written by the tile with dt = 0);
+  // the moment is P - sv sk^T / n
 #pragma unroll
   for (int x = 0; x < TPW; ++x) {
     const int tile = w + 4 * x;
     if (tile < TILES) {
-      const int et = tile / G::DT, dt = tile - (tile / G::DT) * G::DT;
-      const int ea = tr_offset<D>(lane, et), db = tr_offset<D>(lane, dt);
+      const int et = tile / G::DT;
+      const int ea = tr_offset<D>(lane, et);
+      f32x16 sv = f32x16{};
 #pragma unroll
       for (int ch = 0; ch < NCHK; ++ch)
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk)
-          acc[x] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand<D>(&Vt[ch][0], ea, kk),
-                                                           tr_operand<D>(&Kt[ch][0], db, kk), acc[x], 0, 0, 0);
+          sv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand<D>(&Vt[ch][0], ea, kk), ones, sv, 0, 0, 0);
+      if (dtw == 0 && l32 == 0) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int e = et * 32 + (r >> 2) * 8 + hf * 4 + (r & 3);
+          if (e < D) vbar[e] = bf16_bits(sv[r] * inv_n);
+        }
+      }
+      if (et == 0 && hf == 0 && dtw * 32 + l32 < D) kbar[dtw * 32 + l32] = bf16_bits(sk[0] * inv_n);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[x][r] = __builtin_fmaf(-sv[r] * inv_n, sk[r], acc[x][r]);
     }
   }
+
   // M through LDS (row e, D bf16 per row) so that the global stores are
   // whole 16-byte pieces of consecutive rows
   __syncthreads();                           // every wave is done with the tiles
@@ -183,8 +171,8 @@ __global__ __launch_bounds__(256) void rem_moments_kernel(RemMomentArgs a) {
   for (int x = 0; x < TPW; ++x) {
     const int tile = w + 4 * x;
     if (tile < TILES) {
-      const int et = tile / G::DT, dt = tile - (tile / G::DT) * G::DT;
-      const int d = dt * 32 + l32;
+      const int et = tile / G::DT;
+      const int d = dtw * 32 + l32;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int e = et * 32 + (r >> 2) * 8 + hf * 4 + (r & 3);

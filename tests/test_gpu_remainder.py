@@ -86,7 +86,8 @@ def test_block_moments(wl):
             # means: float32 sums rounded once to bf16
             assert np.all(np.abs(gk[b, h] - okb) <= 2.0 ** -8 * np.abs(okb) + 1e-6)
             assert np.all(np.abs(gv[b, h] - ovb) <= 2.0 ** -8 * np.abs(ovb) + 1e-6)
-            # moments: K - kbar rounded to bf16 per term, float32 sums, one bf16 rounding
+            # moments: float32 sums of exact products less the outer product of the
+            # sums (bounded as if K - kbar were rounded to bf16), one bf16 rounding
             bound = np.empty_like(om)
             for j, (a, e) in enumerate(oracle.block_bounds(wl.seq_len, wl.block)):
                 dk = np.abs(k[a:e] - okb[j])
