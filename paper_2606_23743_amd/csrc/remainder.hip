@@ -186,12 +186,17 @@ __global__ __launch_bounds__(256) void rem_moments_kernel(RemMomentArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// First-order weights.  kRemRows query blocks of one head per workgroup (each
-// pooled key row a thread loads serves all of them): the kept sets as LDS
-// bitmaps, then two passes over the key blocks (row maxima, then the
-// weights), each thread taking key blocks tid, tid + 256, ...
+// First-order weights.  A workgroup of four waves takes 128 query blocks of
+// one head, a lane one query block i (32 per wave).  The scores c qbar_i.kbar_j
+// are a small dense product per head, done on MFMA as S^T = Kbar Qbar^T over
+// 32-key chunks; each float32 mean is split into bf16 high and low parts and
+// the three products hi.hi + hi.lo + lo.hi are summed in float32 (relative
+// error about 2^-16, against the 2^-9 of E's bf16 storage).  Pass one takes
+// the row maxima r_i (a lane's registers and the lane pair), pass two writes
+// E = exp(s - r_i) chunk-blocked, one 16-byte piece per lane and key half;
+// then the kept entries of each row's list are set to zero.
 // ---------------------------------------------------------------------------
-constexpr int kRemRows = 16;
+constexpr int kRemRows = 128;              // query blocks per workgroup
 
 // Position of key jj (0..31) of a chunk in a row of E: the eight keys one MFMA
 // lane takes for (kk, hf) -- kk*16 + hf*4 + 0..3, then kk*16 + 8 + hf*4 + 0..3,
@@ -203,92 +208,134 @@ __host__ __device__ __forceinline__ int e_position(int jj) {
 }
 
 template <int D>
-__global__ __launch_bounds__(256) void rem_weights_kernel(RemWeightArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void rem_weights_kernel(RemWeightArgs a) {
+  using G = Geo<D>;
   constexpr int NT = 256;
-  constexpr int kWords = kRemMaxBlocks / 32;
-  __shared__ float qs[kRemRows][D];
-  __shared__ uint32_t bm[kRemRows][kWords];
-  __shared__ float red[kRemRows][4];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int nB = a.nB, nBp = a.nBp;
+  constexpr int CT = 32 * G::RB;
+  __shared__ __attribute__((aligned(1024))) unsigned char Kh[CT], Kl[CT];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int hf = lane >> 5, l32 = lane & 31;
+  const int nB = a.nB, nBp = a.nBp, nBr = a.nBr, nch = nBp / 32;
   const int groups = (nB + kRemRows - 1) / kRemRows;
   const int bh = blockIdx.x / groups;
   const int i0 = (blockIdx.x - bh * groups) * kRemRows;
-  for (int t = tid; t < kRemRows * D; t += NT) {
-    const int ri = t / D, d = t - (t / D) * D;
-    qs[ri][d] = i0 + ri < nB ? a.q_pool[((size_t)bh * nB + i0 + ri) * D + d] : 0.0f;
+  const int i = i0 + w * 32 + l32;           // this lane's query block
+  const bool live = i < nB;
+  const float c = a.scale;
+  const float* kp = a.k_pool + (size_t)bh * nB * D;
+
+  // Qbar^T operand of row i, high and low bf16 parts: d = s*16 + hf*8 + 0..7
+  auto split8 = [](const float* x, bf16x8& hi, bf16x8& lo) {
+    u32x4 h, l;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const bf16x2 ph = cvt2(x[2 * e], x[2 * e + 1]);
+      const bf16x2 pl = cvt2(x[2 * e] - (float)ph[0], x[2 * e + 1] - (float)ph[1]);
+      h[e] = __builtin_bit_cast(unsigned, ph);
+      l[e] = __builtin_bit_cast(unsigned, pl);
+    }
+    hi = __builtin_bit_cast(bf16x8, h);
+    lo = __builtin_bit_cast(bf16x8, l);
+  };
+  bf16x8 qh[G::DQ], ql[G::DQ];
+  {
+    const float* qr = a.q_pool + ((size_t)bh * nB + (live ? i : 0)) * D;
+#pragma unroll
+    for (int s = 0; s < G::DQ; ++s) {
+      float x[8];
+      const float4 x0 = *reinterpret_cast<const float4*>(qr + s * 16 + hf * 8);
+      const float4 x1 = *reinterpret_cast<const float4*>(qr + s * 16 + hf * 8 + 4);
+      x[0] = x0.x; x[1] = x0.y; x[2] = x0.z; x[3] = x0.w;
+      x[4] = x1.x; x[5] = x1.y; x[6] = x1.z; x[7] = x1.w;
+      if (!live) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[e] = 0.0f;
+      }
+      split8(x, qh[s], ql[s]);
+    }
   }
-  for (int t = tid; t < kRemRows * kWords; t += NT) (&bm[0][0])[t] = 0u;
+  int koff[G::DQ], voff[G::DT];
+  operand_offsets<D>(lane, koff, voff);
+
+  // scores of chunk ch (natural-log units; -inf past nB), lane = row i
+  auto chunk_scores = [&](int ch, f32x16& sc) {
+    __syncthreads();                         // the previous chunk's tiles are read
+    for (int p = tid; p < 32 * G::DCH; p += NT) {
+      const int r = p / G::DCH, cp = p - (p / G::DCH) * G::DCH;
+      const int j = ch * 32 + r;
+      float x[8];
+      if (j < nB) {
+        const float4 x0 = *reinterpret_cast<const float4*>(kp + (size_t)j * D + cp * 8);
+        const float4 x1 = *reinterpret_cast<const float4*>(kp + (size_t)j * D + cp * 8 + 4);
+        x[0] = x0.x; x[1] = x0.y; x[2] = x0.z; x[3] = x0.w;
+        x[4] = x1.x; x[5] = x1.y; x[6] = x1.z; x[7] = x1.w;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[e] = 0.0f;
+      }
+      bf16x8 hi, lo;
+      split8(x, hi, lo);
+      const int off = r * G::RB + (swz_k<G::NCH>(r, cp) << 4);
+      *reinterpret_cast<bf16x8*>(Kh + off) = hi;
+      *reinterpret_cast<bf16x8*>(Kl + off) = lo;
+    }
+    __syncthreads();
+    f32x16 acc = f32x16{};
+#pragma unroll
+    for (int s = 0; s < G::DQ; ++s) {
+      const bf16x8 kh = *reinterpret_cast<const bf16x8*>(Kh + koff[s]);
+      const bf16x8 kl = *reinterpret_cast<const bf16x8*>(Kl + koff[s]);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kh, qh[s], acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kh, ql[s], acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kl, qh[s], acc, 0, 0, 0);
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int j = ch * 32 + (r >> 2) * 8 + hf * 4 + (r & 3);
+      sc[r] = j < nB ? acc[r] * c : -INFINITY;
+    }
+  };
+
+  float mx = -INFINITY;
+  for (int ch = 0; ch < nch; ++ch) {
+    f32x16 sc;
+    chunk_scores(ch, sc);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[r]);
+  }
+  const float rmax = swap_halves_max(mx);
+  if (live && hf == 0) a.r[(size_t)bh * nBp + i] = rmax;
+
+  for (int ch = 0; ch < nch; ++ch) {
+    f32x16 sc;
+    chunk_scores(ch, sc);
+    if (live) {
+      uint16_t* Ec = a.E + (((size_t)bh * nch + ch) * nBr + i) * 32;
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        u32x4 pk;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float e0 = exp2f((sc[kk * 8 + 2 * e] - rmax) * kLog2e);
+          const float e1 = exp2f((sc[kk * 8 + 2 * e + 1] - rmax) * kLog2e);
+          pk[e] = __builtin_bit_cast(unsigned, cvt2(e0, e1));
+        }
+        *reinterpret_cast<u32x4*>(Ec + kk * 16 + hf * 8) = pk;
+      }
+    }
+  }
+
+  // the blocks a row keeps carry no first-order weight
   __syncthreads();
-  for (int ri = 0; ri < kRemRows && i0 + ri < nB; ++ri) {
-    const int row = bh * nB + i0 + ri;
+  for (int rr = 0; rr < kRemRows && i0 + rr < nB; ++rr) {
+    const int row = bh * nB + i0 + rr;
     const int cnt = min(max(a.kv_count[row], 0), a.kmax);
     const int32_t* idx = a.kv_idx + (size_t)row * a.kmax;
     for (int t = tid; t < cnt; t += NT) {
       const int j = idx[t];
-      if (j >= 0 && j < nB) atomicOr(&bm[ri][j >> 5], 1u << (j & 31));
-    }
-  }
-  __syncthreads();
-
-  const float c = a.scale;
-  const float* kp = a.k_pool + (size_t)bh * nB * D;
-  auto scores = [&](int j, float (&s)[kRemRows]) {
-#pragma unroll
-    for (int ri = 0; ri < kRemRows; ++ri) s[ri] = 0.0f;
-    const float4* kr = reinterpret_cast<const float4*>(kp + (size_t)j * D);
-    for (int d4 = 0; d4 < D / 4; ++d4) {
-      const float4 kv = kr[d4];
-#pragma unroll
-      for (int ri = 0; ri < kRemRows; ++ri) {
-        s[ri] = fmaf(qs[ri][4 * d4 + 0], kv.x, s[ri]);
-        s[ri] = fmaf(qs[ri][4 * d4 + 1], kv.y, s[ri]);
-        s[ri] = fmaf(qs[ri][4 * d4 + 2], kv.z, s[ri]);
-        s[ri] = fmaf(qs[ri][4 * d4 + 3], kv.w, s[ri]);
-      }
-    }
-#pragma unroll
-    for (int ri = 0; ri < kRemRows; ++ri) s[ri] *= c;
-  };
-
-  float mx[kRemRows];
-#pragma unroll
-  for (int ri = 0; ri < kRemRows; ++ri) mx[ri] = -INFINITY;
-  for (int j = tid; j < nB; j += NT) {
-    float s[kRemRows];
-    scores(j, s);
-#pragma unroll
-    for (int ri = 0; ri < kRemRows; ++ri) mx[ri] = fmaxf(mx[ri], s[ri]);
-  }
-#pragma unroll
-  for (int ri = 0; ri < kRemRows; ++ri) {
-    float m = mx[ri];
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
-    if (lane == 0) red[ri][w] = m;
-  }
-  __syncthreads();
-  float rmax[kRemRows];
-#pragma unroll
-  for (int ri = 0; ri < kRemRows; ++ri) rmax[ri] = fmaxf(fmaxf(red[ri][0], red[ri][1]), fmaxf(red[ri][2], red[ri][3]));
-  if (tid < kRemRows && i0 + tid < nB) {
-    float rv = rmax[0];
-#pragma unroll
-    for (int ri = 1; ri < kRemRows; ++ri)
-      if (ri == tid) rv = rmax[ri];
-    a.r[(size_t)bh * nBp + i0 + tid] = rv;
-  }
-
-  for (int j = tid; j < nBp; j += NT) {
-    float s[kRemRows] = {};
-    if (j < nB) scores(j, s);
-    uint16_t* Ec = a.E + ((size_t)bh * (nBp / 32) + (j >> 5)) * a.nBr * 32 + e_position(j & 31);
-#pragma unroll
-    for (int ri = 0; ri < kRemRows; ++ri) {
-      if (i0 + ri >= nB) break;
-      const bool kept = j >= nB || ((bm[ri][j >> 5] >> (j & 31)) & 1u);
-      const float e = kept ? 0.0f : exp2f((s[ri] - rmax[ri]) * kLog2e);
-      Ec[(size_t)(i0 + ri) * 32] = bf16_bits(e);
+      if (j >= 0 && j < nB) a.E[(((size_t)bh * nch + (j >> 5)) * nBr + i0 + rr) * 32 + e_position(j & 31)] = 0;
     }
   }
 }
