@@ -353,10 +353,12 @@ hipError_t launch_attention(const Dims& d, bool sparse, const uint16_t* q, const
   a.kmax = kmax;
   a.n_rows = dd.B * dd.H * dd.nB;
   a.scale_log2 = (float)(dd.scale * 1.4426950408889634);
+  const int64_t fb = ((int64_t)dd.frame_tokens + dd.S / 2) / dd.S;
+  a.frame_blocks = fb < 1 ? 1 : (fb > dd.nB ? dd.nB : (int)fb);
   // fixed-reference-max kernel (block pairs for sparse 64-token blocks), then
   // the rescaling kernel for any block it marked
   hipError_t e = (sparse && pair_attention_fits(dd, kmax)) ? launch_attention_pair(dd, a, stream)
-                                                     : launch_attention_q32(dd, sparse, a, stream);
+                                                     : launch_attention_q16(dd, sparse, a, stream);
   if (e != hipSuccess) return e;
   return launch_attention_rescaling(dd, sparse, a, stream);
 }

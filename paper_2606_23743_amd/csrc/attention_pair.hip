@@ -17,9 +17,10 @@
 // another order) is marked (NaN first output element of both blocks) and the
 // per-iteration rescaling kernel that runs next recomputes it with the general
 // list semantics.  Per chunk, the arithmetic of a wave is that of the
-// 32-query kernel (Sᵀ = K·Qᵀ, fixed reference maximum from the wave's first
-// chunk, P rounded to bf16 with l summed from it, Oᵀ += Vᵀ·Pᵀ).
-#include "attn_wave32.h"
+// 32-query kernel (attn_w16.h: Sᵀ = K·Qᵀ on 16x16x32 products, fixed reference
+// maximum from the wave's first chunk, P rounded to bf16 with l summed from
+// it, Oᵀ += Vᵀ·Pᵀ), so keep-all lists give dense attention bit for bit.
+#include "attn_w16.h"
 
 namespace sva {
 namespace {
@@ -32,6 +33,7 @@ template <int D, bool OUT_F32>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_pair_kernel(AttnArgs a, int n_pairs) {
   using G = Geo<D>;
+  using G16 = Geo16<D>;
   constexpr int S = 64;                      // tokens per (query and key) block
   constexpr int NW = 4;                      // waves per workgroup
   constexpr int CK = 32;                     // keys per staged chunk
@@ -50,8 +52,6 @@ void attn_pair_kernel(AttnArgs a, int n_pairs) {
 
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int hf = lane >> 5;
-  const int l32 = lane & 31;
   const int N = a.N, nB = a.nB;
   const float sl2 = a.scale_log2;
 
@@ -133,29 +133,36 @@ void attn_pair_kernel(AttnArgs a, int n_pairs) {
   auto active = [&](int u) -> bool { return ((u >> qsel) & 1) != 0; };
   auto key0_of = [&](int u, int c2) -> int { return (u >> 2) * S + c2 * CK; };
 
-  // ---- Q^T operand: query qb*S + (w&1)*32 + l32 ----
-  const int qr = qb * S + (w & 1) * 32 + l32;
-  bf16x8 qop[G::DQ];
-  load_q<D>(qop, Qh, qr, qb < nB && qr < N, hf);
+  // ---- Q^T operands: queries qb*S + (w&1)*32 + 0..31 ----
+  const int qbase = qb * S + (w & 1) * 32;
+  bf16x8 qop[2][G16::KS];
+  load_q16<D>(qop, Qh, qbase, qb < nB ? N : 0, lane);
 
   // direct global -> LDS loads of this wave's pieces of a chunk
-  ChunkLoader<D, NUW, CT> ld;
+  ChunkLoader<D, NUW, CT, true> ld;
   loader_init(ld, Kh, Vh, N, &Ks[0][0], &Vs[0][0], w, lane);
   auto fetch = [&](int st, int key0) { load_chunk(ld, st, key0); };
 
-  int koff[G::DQ], voff[G::DT];
-  operand_offsets<D>(lane, koff, voff);
+  int koff[G16::KS], voff[G16::DT];
+  operand_offsets16<D>(lane, koff, voff);
 
-  float m_ref = 0.0f;
-  float l_part = 0.0f;
+  float m_ref[2] = {0.0f, 0.0f};
+  float l_part[2] = {0.0f, 0.0f};
   bool ref_set = false;                      // wave-uniform: the reference is taken
-  f32x16 oacc[G::DT];
+  f32x4 oacc[G16::DT][2];
 #pragma unroll
-  for (int dt = 0; dt < G::DT; ++dt) oacc[dt] = f32x16{};
+  for (int dt = 0; dt < G16::DT; ++dt) oacc[dt][0] = oacc[dt][1] = f32x4{};
 
-  auto qk = [&](f32x16& sacc, const unsigned char* kt) { qk_chunk<D>(sacc, kt, koff, qop); };
-  auto softmax = [&](const f32x16& sacc, bf16x8 (&pop)[2]) { softmax_chunk(sacc, pop, l_part, m_ref, sl2); };
-  auto pv = [&](const bf16x8 (&pop)[2], const unsigned char* vt) { pv_chunk<D>(pop, vt, voff, oacc); };
+  auto qk = [&](f32x4 (&s)[2][2], const unsigned char* kt) { qk16<D>(s, kt, koff, qop); };
+  auto softmax = [&](const f32x4 (&s)[2][2], bf16x8 (&pop)[2]) { softmax16(s, pop, l_part, m_ref, sl2); };
+  auto pv = [&](const bf16x8 (&pop)[2], const unsigned char* vt) { pv16<D>(pop, vt, voff, oacc); };
+  auto take = [](f32x4 (&dst)[2][2], const f32x4 (&src)[2][2]) {
+#pragma unroll
+    for (int x = 0; x < 2; ++x) {
+      dst[x][0] = src[x][0];
+      dst[x][1] = src[x][1];
+    }
+  };
 
   // ---- pipeline over the union, two entries (four chunks) per iteration ----
   // Chunk c of an iteration: entry u0 (c = 0, 1) or u1 (c = 2, 3), half c % 2,
@@ -164,7 +171,9 @@ void attn_pair_kernel(AttnArgs a, int n_pairs) {
   // u3's first).  Each chunk issues one load group (past the end: block 0, in
   // bounds), so the wait count is a constant, as in the 32-query kernel.
   int u0 = ent(0), u1 = ent(1), u2 = ent(2), u3 = ent(3);
-  f32x16 sacc = f32x16{};
+  f32x4 sacc[2][2];
+#pragma unroll
+  for (int x = 0; x < 2; ++x) sacc[x][0] = sacc[x][1] = f32x4{};
   if (U > 0) {
     fetch(0, key0_of(u0, 0));
     fetch(1, key0_of(u0, 1));
@@ -174,8 +183,8 @@ void attn_pair_kernel(AttnArgs a, int n_pairs) {
     if (active(u0)) {
       qk(sacc, &Ks[0][0]);
       const int valid = __builtin_amdgcn_readfirstlane(N - key0_of(u0, 0));
-      if (valid < CK) mask_tail(sacc, valid, hf);
-      m_ref = chunk_reference(sacc, sl2);    // chunk 0 of a block holds a valid key
+      if (valid < CK) mask_tail16(sacc, valid, lane);
+      chunk_reference16(sacc, sl2, m_ref);   // chunk 0 of a block holds a valid key
       ref_set = true;
     }
   }
@@ -191,10 +200,12 @@ void attn_pair_kernel(AttnArgs a, int n_pairs) {
       const int uc = c < 2 ? u0 : u1;                 // this chunk's entry
       const int un = c == 0 ? u0 : (c < 3 ? u1 : u2); // the next chunk's entry
       const int nkey0 = key0_of(un, (c + 1) & 1);
-      f32x16 snext = f32x16{};
+      f32x4 snext[2][2];
+#pragma unroll
+      for (int x = 0; x < 2; ++x) snext[x][0] = snext[x][1] = f32x4{};
       bf16x8 pop[2];
       if (active(uc) && !ref_set) {                    // the wave's first chunk
-        m_ref = chunk_reference(sacc, sl2);
+        chunk_reference16(sacc, sl2, m_ref);
         ref_set = true;
       }
       if (active(un) && active(uc)) {
@@ -213,10 +224,10 @@ void attn_pair_kernel(AttnArgs a, int n_pairs) {
       const int nvalid = __builtin_amdgcn_readfirstlane(N - nkey0);
       if (nvalid < CK && active(un)) {
         asm volatile("");
-        mask_tail(snext, nvalid, hf);
+        mask_tail16(snext, nvalid, lane);
       }
-      sacc = snext;
-      if (c & 1) rescale_if_large<D>(l_part, m_ref, oacc);                 // after each 64-key block
+      take(sacc, snext);
+      if (c & 1) rescale_if_large16<D>(l_part, m_ref, oacc);               // after each 64-key block
     }
     u0 = u2;
     u1 = u3;
@@ -226,8 +237,10 @@ void attn_pair_kernel(AttnArgs a, int n_pairs) {
   wait_vmcnt<0>();           // no load may still target this workgroup's LDS
 
   // ---- epilogue: overflow check, then O = O^T / l and LSE ----
-  const float l_tot = swap_halves_sum(l_part);
-  const bool over = overflowed<D>(l_tot, oacc);
+  float l_tot[2];
+  l_tot[0] = quad_sum(l_part[0]);
+  l_tot[1] = quad_sum(l_part[1]);
+  const bool over = overflowed16<D>(l_tot, oacc);
   if (__builtin_amdgcn_ballot_w64(over) != 0 && lane == 0) atomicOr(&wg_bad, 1);
   __syncthreads();
   if (wg_bad) {
@@ -235,9 +248,8 @@ void attn_pair_kernel(AttnArgs a, int n_pairs) {
       mark_block<OUT_F32>(a.out, head + (size_t)(2 * p + threadIdx.x) * S * D);
     return;
   }
-  const bool has = ref_set && l_tot > 0.0f;
-  if (qb < nB && qr < N)
-    store_query<D, OUT_F32>(a.out, a.lse, head + (size_t)qr * D, (size_t)bh * N + qr, oacc, l_tot, m_ref, has, hf);
+  const bool has[2] = {ref_set && l_tot[0] > 0.0f, ref_set && l_tot[1] > 0.0f};
+  if (qb < nB) store_query16<D, OUT_F32>(a.out, a.lse, head, (size_t)bh * N, qbase, N, oacc, l_tot, m_ref, has, lane);
 }
 
 template <int D>

@@ -18,6 +18,7 @@ struct AttnArgs {
   float* lse;
   int N, nB, kmax, n_rows;
   float scale_log2;   // c * log2(e)
+  int frame_blocks;   // query blocks per frame of the latent grid, rounded (>= 1)
 };
 
 }  // namespace sva

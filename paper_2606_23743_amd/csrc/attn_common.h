@@ -11,6 +11,7 @@ typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
 typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
 typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(2))) float f32x2;
 typedef __attribute__((ext_vector_type(4))) short i16x4;
 typedef __attribute__((ext_vector_type(2))) unsigned u32x2;
@@ -44,6 +45,15 @@ __device__ __forceinline__ int swz_k(int r, int c) {
 template <int NCH>
 __device__ __forceinline__ int swz_v(int r, int c) {
   return NCH == 16 ? c ^ (4 * (r & 3)) : c ^ (4 * ((r >> 1) & 1));
+}
+
+// V tiles of the 16x16 kernels (attn_w16.h): a 32-lane transpose-read group
+// takes pieces 2dt and 2dt+1 of 8 consecutive rows.  Piece c of row r at
+// c ^ 2(r & 7) (256-byte rows) or c ^ 2((r >> 1) & 3) (128-byte rows, two per
+// 256-byte bank window) puts those 16 reads on disjoint banks.
+template <int NCH>
+__device__ __forceinline__ int swz_v16(int r, int c) {
+  return NCH == 16 ? c ^ (2 * (r & 7)) : c ^ (2 * ((r >> 1) & 3));
 }
 
 __device__ __forceinline__ bf16x2 cvt2(float a, float b) {

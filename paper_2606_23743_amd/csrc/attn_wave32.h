@@ -2,8 +2,8 @@
 // query per lane pair): the direct global -> LDS chunk loads, the per-lane LDS
 // offsets of the operand reads, S^T = K Q^T and O^T += V^T P^T on
 // mfma_f32_32x32x16_bf16, the fixed-reference softmax and the output store.
-// The 128-token kernel (attention_q32.hip) and the block-pair kernel
-// (attention_pair.hip) run the same per-chunk arithmetic through these.
+// The chunk loader also serves the 16x16 attention kernels (attn_w16.h); the
+// 32x32 arithmetic serves the remainder kernels (remainder.hip).
 #pragma once
 
 #include "attn_common.h"
@@ -20,8 +20,9 @@ typedef __attribute__((address_space(3))) unsigned char lds_u8;
 // chunk's key offset is the scalar offset.  Every address lies inside the
 // head's rows: full chunks by construction, the sequence's last partial chunk
 // by clamping rows past the end to its first row, and a chunk wholly past the
-// end by reading chunk 0 instead.
-template <int D, int NUW, int CT>
+// end by reading chunk 0 instead.  V16 selects the V tile swizzle of the 16x16
+// kernels (swz_v16) in place of the one of the transpose reads below.
+template <int D, int NUW, int CT, bool V16 = false>
 struct ChunkLoader {
   __amdgpu_buffer_rsrc_t krs, vrs;
   int kgv[NUW], vgv[NUW];
@@ -29,8 +30,8 @@ struct ChunkLoader {
   int w, lane, N;
 };
 
-template <int D, int NUW, int CT>
-__device__ __forceinline__ void loader_init(ChunkLoader<D, NUW, CT>& f, const uint16_t* Kh, const uint16_t* Vh,
+template <int D, int NUW, int CT, bool V16>
+__device__ __forceinline__ void loader_init(ChunkLoader<D, NUW, CT, V16>& f, const uint16_t* Kh, const uint16_t* Vh,
                                             int N, const unsigned char* ks, const unsigned char* vs, int w,
                                             int lane) {
   using G = Geo<D>;
@@ -40,7 +41,7 @@ __device__ __forceinline__ void loader_init(ChunkLoader<D, NUW, CT>& f, const ui
   for (int v = 0; v < NUW; ++v) {
     const int r = (w * NUW + v) * G::RPI + lane / G::NCH;
     const int p = lane % G::NCH;
-    int ck = swz_k<G::NCH>(r, p), cv = swz_v<G::NCH>(r, p);
+    int ck = swz_k<G::NCH>(r, p), cv = V16 ? swz_v16<G::NCH>(r, p) : swz_v<G::NCH>(r, p);
     if (ck >= G::DCH) ck = 0;                        // padding pieces: any in-row address
     if (cv >= G::DCH) cv = 0;
     f.kgv[v] = (r * D + ck * 8) * 2;
@@ -59,8 +60,8 @@ __device__ __forceinline__ void buffer_to_lds(const __amdgpu_buffer_rsrc_t& rs, 
 }
 
 // one tensor's pieces (TK: K, else V) of the chunk starting at key0 into stage st
-template <bool TK, int D, int NUW, int CT>
-__device__ __forceinline__ void load_tile(const ChunkLoader<D, NUW, CT>& f, int st, int key0) {
+template <bool TK, int D, int NUW, int CT, bool V16>
+__device__ __forceinline__ void load_tile(const ChunkLoader<D, NUW, CT, V16>& f, int st, int key0) {
   using G = Geo<D>;
   const __amdgpu_buffer_rsrc_t& rs = TK ? f.krs : f.vrs;
   const unsigned base = (TK ? f.ks_base : f.vs_base) + st * CT;
@@ -81,15 +82,15 @@ __device__ __forceinline__ void load_tile(const ChunkLoader<D, NUW, CT>& f, int 
       const int u = f.w * NUW + v;
       const int r = u * G::RPI + ln / G::NCH;
       const int rs_ = r < valid ? r : 0;
-      int c = TK ? swz_k<G::NCH>(r, p) : swz_v<G::NCH>(r, p);
+      int c = TK ? swz_k<G::NCH>(r, p) : (V16 ? swz_v16<G::NCH>(r, p) : swz_v<G::NCH>(r, p));
       if (c >= G::DCH) c = 0;
       buffer_to_lds(rs, base + u * 1024, (rs_ * D + c * 8) * 2, key0 * D * 2);
     }
   }
 }
 
-template <int D, int NUW, int CT>
-__device__ __forceinline__ void load_chunk(const ChunkLoader<D, NUW, CT>& f, int st, int key0) {
+template <int D, int NUW, int CT, bool V16>
+__device__ __forceinline__ void load_chunk(const ChunkLoader<D, NUW, CT, V16>& f, int st, int key0) {
   load_tile<true>(f, st, key0);
   load_tile<false>(f, st, key0);
 }

@@ -29,9 +29,9 @@ struct SelectRule {
 // The rescaling (per-iteration online softmax) kernel; attention.hip.
 hipError_t launch_attention_rescaling(const Dims& d, bool sparse, const AttnArgs& a, hipStream_t stream);
 
-// 32-queries-per-wave, two-waves-per-SIMD attention with a fixed reference max;
-// attention_q32.hip.
-hipError_t launch_attention_q32(const Dims& d, bool sparse, const AttnArgs& a, hipStream_t stream);
+// 32-queries-per-wave, two-waves-per-SIMD attention with a fixed reference max
+// on 16x16x32 products; attention_q16.hip.
+hipError_t launch_attention_q16(const Dims& d, bool sparse, const AttnArgs& a, hipStream_t stream);
 
 // Sparse attention for 64-token blocks, two neighbouring query blocks per
 // workgroup walking the union of their lists; attention_pair.hip.  Used when

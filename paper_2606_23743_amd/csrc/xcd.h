@@ -36,4 +36,35 @@ __host__ __device__ __forceinline__ int xcd_remap_segments(int id, int n, int c)
   return k * seg + xcd * c + (slot - k * c);
 }
 
+// Row order inside a head for sparse lists: frame tiles.  With F query blocks
+// per frame (rounded), logical rows are cut into super-rows of FPT frames
+// (F * FPT rows) and each super-row is walked tile by tile, a tile being BPT
+// consecutive blocks of each of the FPT frames (the last tile of a super-row
+// is the F % BPT blocks left over).  So a run of BPT * FPT consecutive logical
+// rows is a (frames) x (blocks) patch of the video whose blocks keep mostly
+// the same key blocks.  The last partial super-row is tiled with the whole
+// frames it holds; rows past those keep their own index.  A bijection on
+// [0, nB) for every F, FPT, BPT >= 1.
+__host__ __device__ __forceinline__ int frame_tile_in(int r, int F, int fpt, int bpt) {
+  const int tsz = fpt * bpt, fullc = F / bpt;
+  if (r < fullc * tsz) {
+    const int tc = r / tsz, u = r - tc * tsz, f = u / bpt, d = u - f * bpt;
+    return f * F + tc * bpt + d;
+  }
+  const int rem = F - fullc * bpt, u = r - fullc * tsz, f = u / rem, d = u - f * rem;
+  return f * F + fullc * bpt + d;
+}
+
+__host__ __device__ __forceinline__ int frame_tile_order(int l, int nB, int F, int fpt, int bpt) {
+  const int span = F * fpt;
+  const int whole = (nB / span) * span;
+  if (l < whole) {
+    const int sr = l / span;
+    return sr * span + frame_tile_in(l - sr * span, F, fpt, bpt);
+  }
+  const int ft = (nB - whole) / F;   // whole frames in the tail
+  if (ft > 0 && l < whole + ft * F) return whole + frame_tile_in(l - whole, F, ft, bpt);
+  return l;
+}
+
 }  // namespace sva
