@@ -193,16 +193,23 @@ int sva_dense_attention(const sva_problem* prob, const void* q, const void* k,
  * instead of dropped; the paper gives no formula, so this is the reading
  * implemented).  For query q of query block i and a key block j that row i
  * does not keep (n_j valid tokens, block means qbar_i, kbar_j, vbar_j), every
- * exp(c q.k_t) of the block is expanded to first order about the means:
+ * exp(c q.k_t) of the block is expanded to first order about the block's mean
+ * key, exp(c q.kbar_j) (1 + c q.(k_t - kbar_j)), with the weight of the
+ * first-order term then taken at the block-mean query (the block-mean form):
  *   exp(c q.k_t) ~ exp(c q.kbar_j) + exp(c qbar_i.kbar_j) c q.(k_t - kbar_j)
  * so the block adds n_j exp(c q.kbar_j) to the row sum and
  * n_j exp(c q.kbar_j) vbar_j + exp(c qbar_i.kbar_j) c M_j q to the numerator,
- * with the block moment M_j[e][d] = sum_t V[t][e] (K[t][d] - kbar_j[d]).  A
- * block is dropped for row i when no in-range entry of the row's list names
- * it.  The result is exact where every key of a dropped block equals the
- * block mean, equals dense attention when every block is kept, and otherwise
- * differs from dense attention by second-order terms in the deviations of
- * queries and keys from their block means.  Requires nB <= SVA_REMAINDER_MAX_BLOCKS. ---- */
+ * with the block moment M_j[e][d] = sum_t V[t][e] (K[t][d] - kbar_j[d]).  The
+ * block-mean weight makes the first-order terms of a query block one D x D
+ * matrix; with the query's own weight (the plain expansion) each query would
+ * contract every dropped block's moment, about three times the kept-block
+ * FLOPs at 15% density.  A block is dropped for row i when no in-range entry
+ * of the row's list names it.  The result is exact where every key of a
+ * dropped block equals the block mean and equals dense attention when every
+ * block is kept.  Otherwise it differs from the plain expansion by
+ * (exp(c qbar_i.kbar_j) - exp(c q.kbar_j)) c M_j q per dropped block, first
+ * order in the key deviations where a block's queries differ by order one.
+ * Requires nB <= SVA_REMAINDER_MAX_BLOCKS. ---- */
 #define SVA_REMAINDER_MAX_BLOCKS 4096
 
 /* Device workspace that sva_sparse_attention_remainder needs, in bytes

@@ -54,12 +54,16 @@ Parity status per function:
                                       inputs equal plain attention)
   remainder.block_moments     pinned (brute force over tokens, independent identity)
   remainder.remainder_attention
-                              pinned to its reading (exact on constant-key blocks,
-                                      dense when all kept, constant values,
-                                      second-order error convergence)
+                              pinned (term-by-term sum over dropped tokens,
+                                      exact on constant-key blocks, dense when
+                                      all kept, constant values, convergence
+                                      orders: second in the key deviations for
+                                      the plain expansion, first for the
+                                      block-mean form where queries vary)
   The paper's own routing rule and its formula for the first-order remainder of
   non-kept blocks: parity unpinned (neither is written out in the paper's text;
-  remainder.py implements a first-order expansion about the block means).
+  remainder.py implements the plain first-order expansion about the block-mean
+  keys, and the block-mean-query form the kernels compute).
 """
 from .blocks import bf16_bits_to_f64, num_blocks, block_bounds, pool_blocks
 from .select import (block_scores, topk_count, select_topk, first_frame_blocks,

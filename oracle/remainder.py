@@ -3,25 +3,21 @@
 
 Section 4.2.2 (and the summary of piecewise sparse attention in Section 2)
 describes the non-critical blocks as compensated by a first-order Taylor
-approximation rather than dropped; the paper states no formula.  Reading taken
-here: the exponential of a dropped block's logits is expanded to first order
-about the block means.
+approximation rather than dropped; the paper states no formula.  The
+definition taken here is the plain first-order expansion of each dropped key's
+exponential about its block's mean key.
 
-For query token n of query block i (query q = Q[n], block-mean query qbar_i)
-and a key block j that row i does not keep (valid tokens t, n_j of them, means
-kbar_j and vbar_j, deviations dk_t = K[t] - kbar_j):
+For query token n (query q = Q[n]) of query block i and a key block j that row
+i does not keep (valid tokens t, n_j of them, means kbar_j and vbar_j,
+deviations dk_t = K[t] - kbar_j):
 
     exp(c q.K[t]) = exp(c q.kbar_j) * exp(c q.dk_t)
-                 ~ exp(c q.kbar_j) + exp(c qbar_i.kbar_j) * c q.dk_t
+                 ~ exp(c q.kbar_j) * (1 + c q.dk_t)          (first order in dk_t)
 
-The first factor is kept exactly; the second is taken to first order in the
-key deviation, and in that first-order term the weight is taken at the
-block-mean query (replacing q by qbar_i there changes the result by a product
-of a query deviation and a key deviation: second order).  Summed over the
-block, with sum_t dk_t = 0:
+Summed over the block, with sum_t dk_t = 0:
 
     weight_j = n_j exp(c q.kbar_j)
-    value_j  = n_j exp(c q.kbar_j) vbar_j + exp(c qbar_i.kbar_j) c M_j q
+    value_j  = exp(c q.kbar_j) (n_j vbar_j + c M_j q)
     M_j[e, d] = sum_t V[t, e] dk_t[d]                 (the block's moment)
 
 and the output adds these to the exact sums over the kept keys m:
@@ -30,16 +26,31 @@ and the output adds these to the exact sums over the kept keys m:
              / (sum_m exp(c q.K[m]) + sum_j weight_j)
     LSE[n] = ln(denominator)
 
+Its error against dense attention is second order in the key deviations alone,
+whatever the queries are.
+
+weight="block_mean" gives the cheaper second approximation the GPU kernels
+compute: in the first-order term only, exp(c q.kbar_j) is replaced by
+exp(c qbar_i.kbar_j) with qbar_i the block-mean query, so that the term becomes
+one matrix per query block, T_i = sum_j exp(c qbar_i.kbar_j) M_j, applied to
+every query of the block.  That replacement is exact when the block's queries
+equal their mean and otherwise changes each first-order term by the relative
+amount exp(c (qbar_i - q).kbar_j) - 1, which is of order one when the queries
+of a block differ by order one: the error of this form against dense attention
+is then first order in the key deviations (a product of a query and a key
+deviation), not second.  The zero-order weight and value keep the query's own
+logit in both forms, so the two forms share the denominator.
+
 A block is dropped for row i when no in-range entry of the row's list names
 it; the kept part attends the list as given (an entry listed twice counts
-twice), as the sparse attention does.  The result is exact when every dropped
-block's keys equal their mean, equals dense attention when every block is
-kept, and otherwise differs from dense attention by second-order terms in the
-query and key deviations from their block means.
+twice), as the sparse attention does.  Both forms are exact when every dropped
+block's keys equal their mean and equal dense attention when every block is
+kept.
 
-Parity: pinned to the mathematics of this reading (exactness cases, second-
-order convergence, moment identities); the paper's own formula is not in its
-text, so parity against the paper is unpinned.
+Parity: pinned to the mathematics of the expansion (a term-by-term sum over
+tokens, exactness cases, second-order convergence in the key deviations, and
+the first order of the block-mean form where queries vary); the paper's own
+formula is not in its text, so parity against the paper is unpinned.
 """
 from __future__ import annotations
 
@@ -88,7 +99,20 @@ def dropped_blocks(kept_row, n_blocks: int):
     return [j for j in range(n_blocks) if j not in named]
 
 
-def remainder_attention(q, k, v, kept, block: int, scale: float, rows=None, first_order: bool = True):
+def first_order_log_weights(qr: np.ndarray, qbar_i: np.ndarray, kbar_drop: np.ndarray, scale: float,
+                            weight: str) -> np.ndarray:
+    """Natural-log weights of the first-order terms, [n, J]: c q_n.kbar_j for
+    the plain expansion (weight="query"), c qbar_i.kbar_j for every query of
+    the block in the block-mean form (weight="block_mean")."""
+    if weight == "query":
+        return scale * (qr @ kbar_drop.T)
+    if weight == "block_mean":
+        return np.broadcast_to(scale * (qbar_i @ kbar_drop.T), (qr.shape[0], kbar_drop.shape[0]))
+    raise ValueError(f"weight must be 'query' or 'block_mean', not {weight!r}")
+
+
+def remainder_attention(q, k, v, kept, block: int, scale: float, rows=None, first_order: bool = True,
+                        weight: str = "query"):
     """Attention over the kept blocks plus the first-order remainder of the
     dropped ones (the definition in the module docstring).
 
@@ -97,6 +121,8 @@ def remainder_attention(q, k, v, kept, block: int, scale: float, rows=None, firs
     rows        : optional iterable of (b, h, i); other query blocks stay NaN
     first_order : False leaves out the c M_j q terms (zero order only), which
                   gives the size of the first-order part as a difference
+    weight      : "query" (the plain expansion) or "block_mean" (the block-mean
+                  query in the first-order weight, as the GPU kernels compute)
     returns (out float64 [B, H, N, D], lse float64 [B, H, N])
     """
     q = np.asarray(q, dtype=np.float64)
@@ -122,8 +148,7 @@ def remainder_attention(q, k, v, kept, block: int, scale: float, rows=None, firs
         # exponents (natural log) of every term, then one common reference
         a_log = scale * (qr @ k[b, h, key_tok].T)              # kept keys     [n, m]
         z_log = scale * (qr @ kbar[b, h, drop].T) + log_token_count(count[drop])   # zero order [n, J]
-        f_log = scale * (qbar[b, h, i] @ kbar[b, h, drop].T)   # first order   [J]
-        f_log = np.broadcast_to(f_log, z_log.shape)
+        f_log = first_order_log_weights(qr, qbar[b, h, i], kbar[b, h, drop], scale, weight)   # [n, J]
         ref = np.max(np.concatenate([a_log, z_log, f_log], axis=1), axis=1, keepdims=True)
         wa = np.exp(a_log - ref)
         wz = np.exp(z_log - ref)

@@ -4,7 +4,9 @@
 //
 // For query q of query block i and a dropped key block j (n_j valid tokens,
 // means kbar_j and vbar_j, moment M_j[e][d] = sum_t v_t[e] (k_t - kbar_j)[d]),
-// the block's exponentials are expanded to first order about the block means:
+// the block's exponentials are expanded to first order about the block's mean
+// key, with the weight of the first-order term taken at the block-mean query
+// (so that the term is one matrix per query block):
 //   row sum    += n_j exp(c q.kbar_j)
 //   numerator  += n_j exp(c q.kbar_j) vbar_j + exp(c qbar_i.kbar_j) c M_j q
 // on top of the exact sums over the kept keys.  Four kernels:

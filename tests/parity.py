@@ -116,6 +116,12 @@ def attention_errors(gpu_out: np.ndarray, ref: np.ndarray, valid: np.ndarray):
 REM_F_REL = 2.0 ** -7
 REM_OUT_REL = 2.0 ** -8
 
+# The form of the first-order remainder the kernels compute (oracle/remainder.py):
+# the block-mean query in the first-order weight.  Against the plain expansion
+# (weight="query") the kernels are held to the same bounds plus the exact gap
+# between the two forms, which the oracle computes.
+KERNEL_REMAINDER_FORM = "block_mean"
+
 
 def remainder_errors(got, ref, first, bf16_out: bool):
     """(worst excess over the elementwise bound, mean error, mean bound):
@@ -128,6 +134,18 @@ def remainder_errors(got, ref, first, bf16_out: bool):
     bound = MAX_ABS + REM_F_REL * f + (REM_OUT_REL * np.abs(ref) if bf16_out else 0.0)
     mean_bound = MEAN_ABS + np.mean(0.5 * REM_F_REL * f) + (0.5 * REM_OUT_REL * np.mean(np.abs(ref)) if bf16_out else 0.0)
     return float(np.max(err - bound)), float(np.mean(err)), float(mean_bound)
+
+
+def remainder_errors_vs_plain(got, ref_plain, ref_kernel_form, first, bf16_out: bool):
+    """remainder_errors against the plain expansion, each element's bound
+    widened by |ref_kernel_form - ref_plain| (the first-order weight taken at
+    the block-mean query instead of the query's own)."""
+    gap = np.abs(np.asarray(ref_kernel_form, dtype=np.float64) - np.asarray(ref_plain, dtype=np.float64))
+    got = np.asarray(got, dtype=np.float64)
+    err = np.abs(got - np.asarray(ref_plain, dtype=np.float64))
+    f = np.abs(np.asarray(first, dtype=np.float64))
+    bound = MAX_ABS + REM_F_REL * f + gap + (REM_OUT_REL * np.abs(ref_plain) if bf16_out else 0.0)
+    return float(np.max(err - bound)), float(np.mean(gap)), float(np.max(gap))
 
 
 def remainder_lse_bound(q, kbar, scale):

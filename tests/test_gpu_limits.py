@@ -139,9 +139,10 @@ def test_remainder_at_4096_blocks():
     rows = [0, 1, 2047, 4094, 4095]
     c = scale_of(wl)
     ref, rlse = orem.remainder_attention(f64["q"], f64["k"], f64["v"], kept, wl.block, c,
-                                         rows=[(0, 0, i) for i in rows])
+                                         rows=[(0, 0, i) for i in rows], weight=parity.KERNEL_REMAINDER_FORM)
     ref0, _ = orem.remainder_attention(f64["q"], f64["k"], f64["v"], kept, wl.block, c,
-                                       rows=[(0, 0, i) for i in rows], first_order=False)
+                                       rows=[(0, 0, i) for i in rows], first_order=False,
+                                       weight=parity.KERNEL_REMAINDER_FORM)
     o = out.float().cpu().numpy()
     kbar = oracle.pool_blocks(f64["k"][0, 0], wl.block)
     for i in rows:

@@ -120,12 +120,25 @@ def test_remainder_attention(wl, out_dtype):
     for b in range(wl.batch):
         for h in range(wl.heads):
             f = {n: oracle.bf16_bits_to_f64(bits[n][b, h])[None, None] for n in ("q", "k", "v")}
-            ref, rlse = orem.remainder_attention(f["q"], f["k"], f["v"], [[kept[b][h]]], wl.block, c)
+            ref, rlse = orem.remainder_attention(f["q"], f["k"], f["v"], [[kept[b][h]]], wl.block, c,
+                                                 weight=parity.KERNEL_REMAINDER_FORM)
             ref0, _ = orem.remainder_attention(f["q"], f["k"], f["v"], [[kept[b][h]]], wl.block, c,
-                                               first_order=False)
+                                               first_order=False, weight=parity.KERNEL_REMAINDER_FORM)
             excess, mean, mean_bound = parity.remainder_errors(got[b, h], ref[0, 0], ref[0, 0] - ref0[0, 0],
                                                                out_dtype == "bf16")
             assert excess <= 0.0 and mean <= mean_bound, ((b, h), excess, mean, mean_bound)
+            # against the plain expansion (the query's own first-order weight):
+            # the same bounds widened by the exact gap between the two forms
+            plain, plse = orem.remainder_attention(f["q"], f["k"], f["v"], [[kept[b][h]]], wl.block, c,
+                                                   weight="query")
+            excess_p, gap_mean, gap_max = parity.remainder_errors_vs_plain(got[b, h], plain[0, 0], ref[0, 0],
+                                                                           ref[0, 0] - ref0[0, 0],
+                                                                           out_dtype == "bf16")
+            assert excess_p <= 0.0, ((b, h), excess_p)
+            assert np.abs(plse - rlse).max() < 1e-9          # the two forms share the denominator
+            if b == 0 and h == 0:
+                say(f"[remainder {wl.name} {out_dtype}] block-mean vs plain expansion: mean |gap| "
+                    f"{gap_mean:.2e}, max {gap_max:.2e}")
             lse_bound = parity.remainder_lse_bound(f["q"][0, 0], oracle.pool_blocks(f["k"][0, 0], wl.block), c)
             assert np.all(np.abs(glse[b, h] - rlse[0, 0]) <= lse_bound), (b, h)
             worst = max(worst, float(np.max(np.abs(got[b, h] - ref[0, 0]))))
@@ -195,12 +208,15 @@ def test_custom_softmax_scale():
     got, glse = out.cpu().numpy(), lse.cpu().numpy()
     for h in range(wl.heads):
         f = {n: oracle.bf16_bits_to_f64(bits[n][0, h])[None, None] for n in ("q", "k", "v")}
-        ref, rlse = orem.remainder_attention(f["q"], f["k"], f["v"], [[kept[0][h]]], wl.block, c)
-        ref0, _ = orem.remainder_attention(f["q"], f["k"], f["v"], [[kept[0][h]]], wl.block, c, first_order=False)
+        ref, rlse = orem.remainder_attention(f["q"], f["k"], f["v"], [[kept[0][h]]], wl.block, c,
+                                             weight=parity.KERNEL_REMAINDER_FORM)
+        ref0, _ = orem.remainder_attention(f["q"], f["k"], f["v"], [[kept[0][h]]], wl.block, c, first_order=False,
+                                           weight=parity.KERNEL_REMAINDER_FORM)
         excess, mean, mean_bound = parity.remainder_errors(got[0, h], ref[0, 0], ref[0, 0] - ref0[0, 0], False)
         assert excess <= 0.0 and mean <= mean_bound, (h, excess, mean, mean_bound)
         bound = parity.remainder_lse_bound(f["q"][0, 0], oracle.pool_blocks(f["k"][0, 0], wl.block), c)
         assert np.all(np.abs(glse[0, h] - rlse[0, 0]) <= bound), h
         # and the scale matters: the result at 1/sqrt(D) is far from this one
-        other, _ = orem.remainder_attention(f["q"], f["k"], f["v"], [[kept[0][h]]], wl.block, scale_of(wl))
+        other, _ = orem.remainder_attention(f["q"], f["k"], f["v"], [[kept[0][h]]], wl.block, scale_of(wl),
+                                            weight=parity.KERNEL_REMAINDER_FORM)
         assert np.abs(other[0, 0] - ref[0, 0]).max() > 10 * parity.MAX_ABS

@@ -117,9 +117,11 @@ def _run(wl, ratios):
             mine = [i for (bb, hh, i) in rows if (bb, hh) == (b, h)]
             q4, k4, v4 = (f64[n][(b, h)][None, None] for n in ("q", "k", "v"))
             ref, rlse = orem.remainder_attention(q4, k4, v4, [[kept[b][h]]], wl.block, c,
-                                                 rows=[(0, 0, i) for i in mine])
+                                                 rows=[(0, 0, i) for i in mine],
+                                                 weight=parity.KERNEL_REMAINDER_FORM)
             ref0, _ = orem.remainder_attention(q4, k4, v4, [[kept[b][h]]], wl.block, c,
-                                               rows=[(0, 0, i) for i in mine], first_order=False)
+                                               rows=[(0, 0, i) for i in mine], first_order=False,
+                                               weight=parity.KERNEL_REMAINDER_FORM)
             kbar = oracle.pool_blocks(k4[0, 0], wl.block)
             for i in mine:
                 a, e = i * wl.block, min((i + 1) * wl.block, wl.seq_len)

@@ -358,17 +358,35 @@ def _moments_not_centred(k, v, block):
 
 _ORIG_BLOCK_MOMENTS = orem.block_moments
 
+def _weight_at_block_mean(qr, qbar_i, kbar_drop, scale, weight):
+    return _ORIG_FIRST_ORDER_LOG_WEIGHTS(qr, qbar_i, kbar_drop, scale, "block_mean")
+
+
+def _weight_at_query_always(qr, qbar_i, kbar_drop, scale, weight):
+    return _ORIG_FIRST_ORDER_LOG_WEIGHTS(qr, qbar_i, kbar_drop, scale, "query")
+
+
+_ORIG_FIRST_ORDER_LOG_WEIGHTS = orem.first_order_log_weights
+
 REM_MUTANTS = [
     ("moment applied transposed", "moment_times_query", _moment_times_query_transposed,
-     [lambda: TR.test_error_is_second_order(True), lambda: TR.test_error_is_second_order(False)]),
+     [lambda: TR.test_error_is_second_order(True, "query"), lambda: TR.test_error_is_second_order(False, "query"),
+      lambda: TR.test_first_order_term_by_term()]),
     ("first-order term dropped", "moment_times_query", _no_first_order,
-     [lambda: TR.test_error_is_second_order(True), lambda: TR.test_error_is_second_order(False)]),
+     [lambda: TR.test_error_is_second_order(True, "query"), lambda: TR.test_error_is_second_order(False, "query"),
+      lambda: TR.test_error_is_second_order(True, "block_mean"), lambda: TR.test_first_order_term_by_term()]),
     ("first-order term with the wrong sign", "moment_times_query", _moment_sign_flipped,
-     [lambda: TR.test_error_is_second_order(True)]),
+     [lambda: TR.test_error_is_second_order(True, "query"), lambda: TR.test_first_order_term_by_term()]),
     ("dropped block counted as one token", "log_token_count", _block_counts_ignored,
-     [lambda: TR.test_constant_key_blocks_equal_dense(37, 8), lambda: TR.test_constant_key_blocks_equal_dense(9, 4)]),
+     [lambda: TR.test_constant_key_blocks_equal_dense(37, 8, "query"),
+      lambda: TR.test_constant_key_blocks_equal_dense(9, 4, "block_mean"), lambda: TR.test_first_order_term_by_term()]),
     ("moments about zero, not the block mean", "block_moments", _moments_not_centred,
-     [lambda: TR.test_moments_bruteforce_and_identity(), lambda: TR.test_constant_key_blocks_equal_dense(40, 8)]),
+     [lambda: TR.test_moments_bruteforce_and_identity(), lambda: TR.test_constant_key_blocks_equal_dense(40, 8, "query")]),
+    ("first-order weight at the block-mean query", "first_order_log_weights", _weight_at_block_mean,
+     [lambda: TR.test_plain_expansion_is_second_order_in_the_key_deviation(),
+      lambda: TR.test_first_order_term_by_term()]),
+    ("block-mean form computed with the query's own weight", "first_order_log_weights", _weight_at_query_always,
+     [lambda: TR.test_block_mean_form_is_first_order_in_the_key_deviation()]),
 ]
 
 

@@ -2,7 +2,9 @@
 [0, n): a lost item leaves output rows unwritten, a repeated one writes a row
 twice.  The kernels only reach the segment order on more than 8 x 128 rows,
 beyond what the small GPU cases launch, so both maps are checked here on the
-host for every n up to 3000 and the workload sizes."""
+host for every n up to 3000 and the workload sizes; so is the frame-tile
+order of query blocks inside a head, for every block count up to 1300 and
+frame sizes from 1 to 60 blocks, with one small order written out."""
 import os
 import shutil
 import subprocess
@@ -41,6 +43,24 @@ int main() {
     const int s = id / 8, x = id % 8;
     bad += sva::xcd_remap_segments(id, n, c) != (s / c) * 8 * c + x * c + s % c;
   }
+  // frame tiles: a bijection on [0, nB) for every frame size and tile shape
+  const int fs[] = {1, 2, 3, 7, 13, 28, 29, 55, 60};
+  const int tiles[][2] = {{8, 4}, {1, 1}, {2, 3}, {8, 8}, {5, 7}};
+  for (int nb = 1; nb <= 1300; ++nb)
+    for (int f : fs)
+      for (auto& tl : tiles) {
+        std::vector<char> seen(nb, 0);
+        for (int l = 0; l < nb; ++l) {
+          const int r = sva::frame_tile_order(l, nb, f, tl[0], tl[1]);
+          if (r < 0 || r >= nb || seen[r]) { ++bad; break; }
+          seen[r] = 1;
+        }
+      }
+  // 10 blocks, 3 per frame, tiles of 2 blocks x 2 frames: super-row {0..5} in
+  // the order 0 1 3 4 (two blocks of frames 0 and 1) then 2 5 (the leftover
+  // column); the tail holds one whole frame (6 7 8) and block 9
+  const int want[10] = {0, 1, 3, 4, 2, 5, 6, 7, 8, 9};
+  for (int l = 0; l < 10; ++l) bad += sva::frame_tile_order(l, 10, 3, 2, 2) != want[l];
   std::printf("bad=%d\n", bad);
   return bad != 0;
 }
