@@ -181,6 +181,35 @@ def _stream(stream) -> Optional[int]:
     return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
 
 
+def _side_stream(stream):
+    """The stream a call was given, as a torch stream object, when it is not
+    the current stream (None otherwise)."""
+    torch = _torch()
+    if stream is None:
+        return None
+    cur = torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return None if stream.cuda_stream == cur else stream
+    h = int(stream.cuda_stream if hasattr(stream, "cuda_stream") else stream)
+    return None if h == cur else torch.cuda.ExternalStream(h)
+
+
+def _record(stream, *tensors):
+    """Mark every tensor a call reads or writes as in use on the call's stream
+    when that is not the current stream: the caching allocator then keeps the
+    memory of a tensor freed meanwhile (a workspace or output allocated here
+    on the current stream, or an input the caller drops) from being handed to
+    another allocation until the work enqueued on that stream has finished."""
+    s = _side_stream(stream)
+    if s is None:
+        return
+    for x in tensors:
+        if isinstance(x, dict):
+            _record(stream, *x.values())
+        elif x is not None:
+            x.record_stream(s)
+
+
 def _need(t, dtype, shape, name):
     torch = _torch()
     if not isinstance(t, torch.Tensor):
@@ -214,6 +243,7 @@ def pool_blocks(prob: Problem, q, k, q_pool=None, k_pool=None, stream=None) -> T
     _need(k_pool, torch.float32, pshape, "k_pool")
     _check(load().sva_pool_blocks(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(q_pool), _ptr(k_pool),
                                   _stream(stream)), "sva_pool_blocks")
+    _record(stream, q, k, q_pool, k_pool)
     return q_pool, k_pool
 
 
@@ -247,6 +277,7 @@ def qknorm_rope_pool(prob: Problem, q_in, k_in, gamma_q, gamma_k, eps: float = 1
                                        _ptr(gamma_q), _ptr(gamma_k), _ptr(q_out), _ptr(k_out),
                                        _ptr(q_pool), _ptr(k_pool), _stream(stream)),
            "sva_qknorm_rope_pool")
+    _record(stream, q_in, k_in, gamma_q, gamma_k, q_out, k_out, q_pool, k_pool)
     return q_out, k_out, q_pool, k_pool
 
 
@@ -273,6 +304,7 @@ def select_blocks(prob: Problem, sel: SelectParams, q_pool, k_pool, kmax: Option
     _check(load().sva_select_blocks(ctypes.byref(prob), ctypes.byref(sel), _ptr(q_pool), _ptr(k_pool),
                                     int(kmax), _ptr(kv_idx), _ptr(kv_count), _ptr(mask), _stream(stream)),
            "sva_select_blocks")
+    _record(stream, q_pool, k_pool, kv_idx, kv_count, mask)
     return kv_idx, kv_count, mask
 
 
@@ -303,6 +335,7 @@ def sparse_attention(prob: Problem, q, k, v, kv_idx, kv_count, out=None, want_ls
     _check(load().sva_sparse_attention(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(kv_idx),
                                        _ptr(kv_count), int(kmax), _ptr(out), _ptr(lse), _stream(stream)),
            "sva_sparse_attention")
+    _record(stream, q, k, v, kv_idx, kv_count, out, lse)
     return out, lse
 
 
@@ -332,6 +365,7 @@ def block_moments(prob: Problem, k, v, kbar=None, vbar=None, moments=None, strea
     _need(moments, torch.bfloat16, (B, H, nb, D, D), "moments")
     _check(load().sva_block_moments(ctypes.byref(prob), _ptr(k), _ptr(v), _ptr(kbar), _ptr(vbar), _ptr(moments),
                                     _stream(stream)), "sva_block_moments")
+    _record(stream, k, v, kbar, vbar, moments)
     return kbar, vbar, moments
 
 
@@ -364,6 +398,7 @@ def sparse_attention_remainder(prob: Problem, q, k, v, q_pool, k_pool, kv_idx, k
         ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(q_pool), _ptr(k_pool), _ptr(kv_idx), _ptr(kv_count),
         int(kmax), _ptr(workspace), int(workspace.numel()), _ptr(out), _ptr(lse), _stream(stream)),
         "sva_sparse_attention_remainder")
+    _record(stream, q, k, v, q_pool, k_pool, kv_idx, kv_count, workspace, out, lse)
     return out, lse
 
 
@@ -380,6 +415,7 @@ def dense_attention(prob: Problem, q, k, v, out=None, want_lse: bool = False, ls
         _need(lse, torch.float32, shp[:3], "lse")
     _check(load().sva_dense_attention(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(out),
                                       _ptr(lse), _stream(stream)), "sva_dense_attention")
+    _record(stream, q, k, v, out, lse)
     return out, lse
 
 
@@ -437,6 +473,7 @@ def quantize_fp8(prob: Problem, q, k, v, out: Optional[dict] = None, stream=None
     st = _fp8_struct(out)
     _check(load().sva_quantize_fp8(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), ctypes.byref(st),
                                    _stream(stream)), "sva_quantize_fp8")
+    _record(stream, q, k, v, out)
     return out
 
 
@@ -463,6 +500,7 @@ def sparse_attention_fp8(prob: Problem, quant: dict, kv_idx, kv_count, out=None,
     _check(load().sva_sparse_attention_fp8(ctypes.byref(prob), ctypes.byref(st), _ptr(kv_idx),
                                            _ptr(kv_count), int(kmax), _ptr(out), _ptr(lse),
                                            _stream(stream)), "sva_sparse_attention_fp8")
+    _record(stream, quant, kv_idx, kv_count, out, lse)
     return out, lse
 
 
@@ -484,6 +522,7 @@ def dense_attention_fp8(prob: Problem, quant: dict, out=None, want_lse: bool = F
     st = _fp8_struct(quant)
     _check(load().sva_dense_attention_fp8(ctypes.byref(prob), ctypes.byref(st), _ptr(out), _ptr(lse),
                                           _stream(stream)), "sva_dense_attention_fp8")
+    _record(stream, quant, out, lse)
     return out, lse
 
 
@@ -540,6 +579,7 @@ def token_select(x, keep_ratio: float, scores=None, kept_idx=None, kept_pos=None
                                    _ptr(kept_idx), _ptr(kept_pos), _ptr(workspace),
                                    workspace.numel() * workspace.element_size(), _stream(stream)),
            "sva_token_select")
+    _record(stream, x, scores, kept_idx, kept_pos, workspace)
     return scores, kept_idx, kept_pos
 
 
@@ -555,6 +595,7 @@ def token_gather(x, kept_idx, x_kept=None, stream=None):
     _need(x_kept, torch.bfloat16, (B, k, C), "x_kept")
     _check(load().sva_token_gather(ctypes.byref(tokens(B, N, C)), k, _ptr(x), _ptr(kept_idx),
                                    _ptr(x_kept), _stream(stream)), "sva_token_gather")
+    _record(stream, x, kept_idx, x_kept)
     return x_kept
 
 
@@ -572,4 +613,5 @@ def token_scatter(y_kept, kept_pos, base, out=None, stream=None):
     _need(out, torch.bfloat16, (B, N, C), "out")
     _check(load().sva_token_scatter(ctypes.byref(tokens(B, N, C)), k, _ptr(y_kept), _ptr(kept_pos),
                                     _ptr(base), _ptr(out), _stream(stream)), "sva_token_scatter")
+    _record(stream, y_kept, kept_pos, base, out)
     return out
