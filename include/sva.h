@@ -291,6 +291,22 @@ int sva_token_select(const sva_tokens* t, double keep_ratio, const void* x, doub
                      int32_t* kept_idx, int32_t* kept_pos, void* workspace, size_t workspace_bytes,
                      void* stream);
 
+/* sva_token_select for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same kernels and results, with the workspace in a static
+ * device array of SVA_TOKEN_SELECT_NOALLOC_MAX_BATCH * 33024 bytes (528 KB)
+ * that each GPU the library runs on holds until the process ends.  Arguments
+ * as for sva_token_select, without the workspace; the caller still passes the
+ * outputs.  The call allocates nothing (no hipMalloc, hipFree or allocating
+ * library routine); its first call on a device looks the array's address up
+ * once.  Every call on one GPU shares that GPU's array: calls that overlap on
+ * one GPU (unordered streams, several host threads) race, so order them on
+ * one stream.  SVA_ERR_SHAPE for more than SVA_TOKEN_SELECT_NOALLOC_MAX_BATCH
+ * batch entries, SVA_ERR_HIP when the address lookup fails. */
+#define SVA_TOKEN_SELECT_NOALLOC_MAX_BATCH 16
+int sva_token_select_noalloc(const sva_tokens* t, double keep_ratio, const void* x, double* scores,
+                             int32_t* kept_idx, int32_t* kept_pos, void* stream);
+
 /* x_kept[b, j, :] = x[b, kept_idx[b, j], :] for j < k (an index outside
  * [0, N) gives a row of zeros).
  *   x: bf16 [B, N, C]; kept_idx: int32 [B, k]; x_kept: bf16 [B, k, C], written. */

@@ -9,7 +9,7 @@ from . import workloads
 from ._lib import (SvaError, Problem, SelectParams, RopeParams, load, problem, problem_for,
                    select_topk, select_mass, select_for, num_blocks, max_keep, pool_blocks,
                    qknorm_rope_pool, select_blocks, sparse_attention, dense_attention,
-                   status_string, LIB_PATH, Tokens, tokens, token_keep_count, token_select,
+                   status_string, LIB_PATH, Tokens, tokens, token_keep_count, token_select, token_select_noalloc,
                    token_gather, token_scatter, token_select_workspace, Fp8Tensors, fp8_padded_len, fp8_code_dim,
                    quantize_fp8, sparse_attention_fp8, dense_attention_fp8, remainder_workspace,
                    block_moments, sparse_attention_remainder)
@@ -18,7 +18,7 @@ __all__ = [
     "workloads", "SvaError", "Problem", "SelectParams", "RopeParams", "load", "problem",
     "problem_for", "select_topk", "select_mass", "select_for", "num_blocks", "max_keep",
     "pool_blocks", "qknorm_rope_pool", "select_blocks", "sparse_attention", "dense_attention",
-    "status_string", "LIB_PATH", "Tokens", "tokens", "token_keep_count", "token_select",
+    "status_string", "LIB_PATH", "Tokens", "tokens", "token_keep_count", "token_select", "token_select_noalloc",
     "token_gather", "token_scatter", "token_select_workspace", "Fp8Tensors", "fp8_padded_len", "fp8_code_dim",
     "quantize_fp8", "sparse_attention_fp8", "dense_attention_fp8", "remainder_workspace",
     "block_moments", "sparse_attention_remainder",

@@ -84,6 +84,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "sva_token_select_workspace": [ctypes.POINTER(Tokens), ctypes.POINTER(ctypes.c_size_t)],
         "sva_token_select": [ctypes.POINTER(Tokens), ctypes.c_double, vp, vp, vp, vp, vp,
                              ctypes.c_size_t, vp],
+        "sva_token_select_noalloc": [ctypes.POINTER(Tokens), ctypes.c_double, vp, vp, vp, vp, vp],
         "sva_token_gather": [ctypes.POINTER(Tokens), ctypes.c_int32, vp, vp, vp, vp],
         "sva_token_scatter": [ctypes.POINTER(Tokens), ctypes.c_int32, vp, vp, vp, vp, vp],
         "sva_fp8_padded_len": [P, i32p],
@@ -580,6 +581,34 @@ def token_select(x, keep_ratio: float, scores=None, kept_idx=None, kept_pos=None
                                    workspace.numel() * workspace.element_size(), _stream(stream)),
            "sva_token_select")
     _record(stream, x, scores, kept_idx, kept_pos, workspace)
+    return scores, kept_idx, kept_pos
+
+
+def token_select_noalloc(x, keep_ratio: float, scores=None, kept_idx=None, kept_pos=None, stream=None) -> Tuple:
+    """sva_token_select_noalloc: token_select with the library's static
+    workspace (at most 16 batch entries; calls on one GPU must not overlap).
+    Outputs are allocated here when not given; the library call itself
+    allocates nothing."""
+    torch = _torch()
+    if x.dim() != 3:
+        raise ValueError("x must be [B, N, C]")
+    B, N, C = x.shape
+    t = tokens(B, N, C)
+    k = token_keep_count(t, keep_ratio)
+    _need(x, torch.bfloat16, (B, N, C), "x")
+    if scores is None:
+        scores = torch.empty((B, N), dtype=torch.float64, device=x.device)
+    if kept_idx is None:
+        kept_idx = torch.empty((B, k), dtype=torch.int32, device=x.device)
+    if kept_pos is None:
+        kept_pos = torch.empty((B, N), dtype=torch.int32, device=x.device)
+    _need(scores, torch.float64, (B, N), "scores")
+    _need(kept_idx, torch.int32, (B, k), "kept_idx")
+    _need(kept_pos, torch.int32, (B, N), "kept_pos")
+    _check(load().sva_token_select_noalloc(ctypes.byref(t), float(keep_ratio), _ptr(x), _ptr(scores),
+                                           _ptr(kept_idx), _ptr(kept_pos), _stream(stream)),
+           "sva_token_select_noalloc")
+    _record(stream, x, scores, kept_idx, kept_pos)
     return scores, kept_idx, kept_pos
 
 

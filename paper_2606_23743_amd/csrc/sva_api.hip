@@ -302,6 +302,24 @@ int sva_token_select(const sva_tokens* t, double keep_ratio, const void* x, doub
                                              kept_pos, workspace, static_cast<hipStream_t>(stream)));
 }
 
+int sva_token_select_noalloc(const sva_tokens* t, double keep_ratio, const void* x, double* scores,
+                             int32_t* kept_idx, int32_t* kept_pos, void* stream) {
+  static_assert(SVA_TOKEN_SELECT_NOALLOC_MAX_BATCH == sva::kTokenSelectStaticBatch, "static batch");
+  int32_t k;
+  const int st = sva_token_keep_count(t, keep_ratio, &k);
+  if (st != SVA_OK) return st;
+  if (!x || !scores || !kept_idx || !kept_pos) return SVA_ERR_INVALID_ARG;
+  if (t->batch > SVA_TOKEN_SELECT_NOALLOC_MAX_BATCH) return SVA_ERR_SHAPE;
+  if (!aligned(x, 16) || !aligned(scores, 8) || !aligned(kept_idx, 4) || !aligned(kept_pos, 4))
+    return SVA_ERR_ALIGNMENT;
+  void* ws = nullptr;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (sva::token_select_scratch(s, &ws) != hipSuccess) return SVA_ERR_HIP;
+  return hip_status(sva::launch_token_select(t->batch, t->tokens, t->channels, k,
+                                             static_cast<const uint16_t*>(x), scores, kept_idx,
+                                             kept_pos, ws, s));
+}
+
 int sva_token_gather(const sva_tokens* t, int32_t k, const void* x, const int32_t* kept_idx,
                      void* x_kept, void* stream) {
   const int st = check_tokens(t);

@@ -154,6 +154,11 @@ hipError_t launch_qknorm_rope_pool(const Dims& d, const RopeArgs& a, hipStream_t
 // feat_norm token pruning; token_prune.hip.
 // Device workspace of the token selection: one slice of this many bytes per batch entry.
 constexpr size_t kTokenSelectWsStride = 33024;
+// Batch entries the allocation-free selection's static workspace holds.
+constexpr int kTokenSelectStaticBatch = 16;
+// Device address of that workspace on the device of `stream` (looked up once
+// per device); token_prune.hip.
+hipError_t token_select_scratch(hipStream_t stream, void** ptr);
 hipError_t launch_token_select(int B, int N, int C, int k, const uint16_t* x, double* scores,
                                int32_t* kept_idx, int32_t* kept_pos, void* workspace,
                                hipStream_t stream);

@@ -12,6 +12,8 @@
 //   gather x_kept[b, j] = x[b, kept_idx[b, j]]; scatter out[b, n] = y_kept[b,
 //          kept_pos[b, n]] for kept tokens and base[b, n] for the others.  One
 //          wave per row, 16-byte loads and stores.
+#include <mutex>
+
 #include "sva_internal.h"
 
 namespace sva {
@@ -387,6 +389,39 @@ hipError_t launch_token_select(int B, int N, int C, int k, const uint16_t* x, do
   hipLaunchKernelGGL(token_write_kernel, dim3(nseg, B), dim3(kSegThreads), 0, stream, scores, ws,
                      kept_idx, kept_pos, N, seg_len, k);
   return hipGetLastError();
+}
+
+// Workspace of the allocation-free token selection (sva_token_select_noalloc):
+// kTokenSelectStaticBatch slices.  Each GPU the library runs on holds its own
+// copy until the process ends; host code never passes the array's name to a
+// kernel (in host code it is a stand-in, not a device address), only the
+// per-device address hipGetSymbolAddress returns.
+static __device__ __align__(256) unsigned char scratch[kTokenSelectStaticBatch * kTokenSelectWsStride];
+
+hipError_t token_select_scratch(hipStream_t stream, void** ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = stream ? hipStreamGetDevice(stream, &dev) : hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    // once per device, with that device current
+    int cur = 0;
+    if ((e = hipGetDevice(&cur)) != hipSuccess) return e;
+    if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    const hipError_t back = cur != dev ? hipSetDevice(cur) : hipSuccess;
+    if (e != hipSuccess) return e;
+    if (back != hipSuccess) return back;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_token_gather(int B, int N, int C, int k, const uint16_t* x, const int32_t* kept_idx,

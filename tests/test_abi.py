@@ -221,6 +221,14 @@ def test_token_entry_points_reject_before_launch(lib):
     assert sel(ctypes.byref(t), 0.5, A, A + 4, A, A, B, W, None) == _lib.SVA_ERR_ALIGNMENT
     assert sel(ctypes.byref(t), 0.5, A, A, A, A, B + 4, W, None) == _lib.SVA_ERR_ALIGNMENT
     assert sel(ctypes.byref(t), 2.0, A, A, A, A, B, W, None) == _lib.SVA_ERR_INVALID_ARG
+    # the allocation-free form: the same checks, and more than 16 batch
+    # entries (its static workspace) rejected, all before any device call
+    nsel = lib.sva_token_select_noalloc
+    assert nsel(ctypes.byref(t), 0.5, None, A, A, A, None) == _lib.SVA_ERR_INVALID_ARG
+    assert nsel(ctypes.byref(t), 0.5, A, A, A, None, None) == _lib.SVA_ERR_INVALID_ARG
+    assert nsel(ctypes.byref(t), 0.5, A + 8, A, A, A, None) == _lib.SVA_ERR_ALIGNMENT
+    assert nsel(ctypes.byref(t), 2.0, A, A, A, A, None) == _lib.SVA_ERR_INVALID_ARG
+    assert nsel(ctypes.byref(sva.tokens(17, 100, 64)), 0.5, A, A, A, A, None) == _lib.SVA_ERR_SHAPE
     g = lib.sva_token_gather
     assert g(ctypes.byref(t), 0, A, A, B, None) == _lib.SVA_ERR_SHAPE
     assert g(ctypes.byref(t), 101, A, A, B, None) == _lib.SVA_ERR_SHAPE
