@@ -13,9 +13,12 @@ roofline     the sparse-attention kernel alone: kept FLOPs per launch / mean
              against the bf16 dense MFMA peak; traffic = HBM bytes per launch
              from the committed rocprofv3 counter record while the kernel
              sources still match it (else null)
-cpu_baseline the float64 oracle on a bounded sample of the same workload (one
-             head's pooling and selection plus as many query blocks as fit the
-             time budget), in the same unit
+cpu_baseline the float64 oracle on the host cores, timed before the GPU is
+             touched: one forked worker per core (at most 16), one BLAS
+             thread each, each on its own head (pooling and selection of every
+             query block, then as many query blocks' attention as fit the time
+             budget); kept FLOPs / wall seconds, in the same unit, with a
+             labelled extrapolation to the whole layer
 """
 from __future__ import annotations
 
@@ -78,54 +81,89 @@ def kept_flops(idx: np.ndarray, cnt: np.ndarray, N: int, S: int, D: int):
     return flops, 4.0 * D * S * S * pairs, pairs
 
 
-def cpu_baseline(wl, bits, budget_s: float):
-    """Time the oracle on a bounded sample: head (0, 0) pooling + selection,
-    then block-sparse attention on query blocks until the budget is spent."""
-    import oracle
-    from threadpoolctl import threadpool_info
+_CPU_BITS = None     # the workload's inputs, inherited by the forked baseline workers
 
+
+def _cpu_head(task):
+    """One baseline worker: head (b, h) of the workload with one BLAS thread:
+    float64 pooling, scores and selection over all query blocks, then
+    block-sparse attention on query blocks in a seeded random order until the
+    time budget is spent."""
+    import oracle
+    from threadpoolctl import threadpool_limits
+
+    wl, b, h, budget_s = task
+    with threadpool_limits(1):
+        t0 = time.perf_counter()
+        f = {n: oracle.bf16_bits_to_f64(_CPU_BITS[n][b, h]) for n in ("q", "k", "v")}
+        c = 1.0 / np.sqrt(wl.head_dim)
+        s = oracle.block_scores(oracle.pool_blocks(f["q"], wl.block), oracle.pool_blocks(f["k"], wl.block), c)
+        nb = s.shape[-1]
+        if wl.mode == "mass":
+            forced = (oracle.first_frame_blocks(wl.grid_h, wl.grid_w, wl.block, nb)
+                      if wl.force_first_frame else [])
+            kept = oracle.select_cummass(s, wl.mass_threshold,
+                                         oracle.mass_cap(nb, wl.max_keep_ratio, len(forced)), forced)
+        else:
+            kept = oracle.select_topk(s, oracle.topk_count(nb, wl.keep_ratio, wl.topk))
+        t_select = time.perf_counter() - t0
+        q4, k4, v4 = (f[n][None, None] for n in ("q", "k", "v"))
+        ntok = [min(wl.block, wl.seq_len - i * wl.block) for i in range(nb)]
+        flops, done = 0.0, 0
+        t1 = time.perf_counter()
+        for i in np.random.default_rng(1000 * b + h).permutation(nb):
+            oracle.block_sparse_attention(q4, k4, v4, [[kept]], wl.block, c, rows=[(0, 0, int(i))])
+            flops += 4.0 * wl.head_dim * ntok[i] * sum(ntok[j] for j in kept[i])
+            done += 1
+            if time.perf_counter() - t1 > budget_s:
+                break
+        return {"flops": flops, "select_s": t_select, "attn_s": time.perf_counter() - t1, "blocks": done,
+                "n_blocks": nb}
+
+
+def cpu_baseline(wl, bits, budget_s: float):
+    """Time the oracle on the host cores: one forked worker per core (the
+    process's CPU affinity, at most 16), one BLAS thread each, each worker on
+    its own head; value = kept FLOPs of the attended query blocks / wall time.
+    Runs before the GPU is first touched, so the forked workers inherit no
+    device state."""
+    import multiprocessing as mp
+
+    global _CPU_BITS
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        avail = os.cpu_count() or 1
+    heads = [(b, h) for b in range(wl.batch) for h in range(wl.heads)]
+    workers = max(1, min(avail, 16, len(heads)))
+    step = len(heads) / workers
+    tasks = [(wl, *heads[int(w * step)], budget_s) for w in range(workers)]
+    _CPU_BITS = bits
     t0 = time.perf_counter()
-    f = {n: oracle.bf16_bits_to_f64(bits[n][0, 0]) for n in ("q", "k", "v")}
-    c = 1.0 / np.sqrt(wl.head_dim)
-    qp = oracle.pool_blocks(f["q"], wl.block)
-    kp = oracle.pool_blocks(f["k"], wl.block)
-    s = oracle.block_scores(qp, kp, c)
-    nb = s.shape[-1]
-    # BLAS registers its thread pool once numpy has called into it (the matmul above)
-    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    if wl.mode == "mass":
-        forced = oracle.first_frame_blocks(wl.grid_h, wl.grid_w, wl.block, nb) if wl.force_first_frame else []
-        kept = oracle.select_cummass(s, wl.mass_threshold, oracle.mass_cap(nb, wl.max_keep_ratio, len(forced)),
-                                     forced)
-    else:
-        kept = oracle.select_topk(s, oracle.topk_count(nb, wl.keep_ratio, wl.topk))
-    t_select = time.perf_counter() - t0
-    q4, k4, v4 = (f[n][None, None] for n in ("q", "k", "v"))
-    rng = np.random.default_rng(0)
-    order = rng.permutation(nb)
-    flops = 0.0
-    done = 0
-    t1 = time.perf_counter()
-    ntok = [min(wl.block, wl.seq_len - i * wl.block) for i in range(nb)]
-    for i in order:
-        oracle.block_sparse_attention(q4, k4, v4, [[kept]], wl.block, c, rows=[(0, 0, int(i))])
-        flops += 4.0 * wl.head_dim * ntok[i] * sum(ntok[j] for j in kept[i])
-        done += 1
-        if time.perf_counter() - t1 > budget_s:
-            break
-    t_attn = time.perf_counter() - t1
-    total = t_select + t_attn
+    with mp.get_context("fork").Pool(workers) as pool:
+        res = pool.map(_cpu_head, tasks)
+    wall = time.perf_counter() - t0
+    _CPU_BITS = None
+    flops = sum(r["flops"] for r in res)
+    blocks = sum(r["blocks"] for r in res)
+    attn_s = sum(r["attn_s"] for r in res)
+    select_s = sum(r["select_s"] for r in res)
+    nb = res[0]["n_blocks"]
     return {
-        "value": flops / total / 1e12,
+        "value": flops / wall / 1e12,
         "unit": "TFLOP/s",
-        "cores": int(threads),
+        "cores": workers,
+        "blas_threads_per_worker": 1,
+        "host_cores_available": avail,
         "kind": "oracle",
-        "sample": (f"head (b=0,h=0) of {wl.name}: float64 pooling + scores + selection over all "
-                   f"{nb} query blocks ({t_select:.2f} s), then block-sparse attention on {done} "
-                   f"random query blocks ({t_attn:.2f} s); value = kept FLOPs of those blocks / "
-                   f"total seconds"),
-        "attention_only_tflops": flops / t_attn / 1e12,
-        "seconds": total,
+        "sample": (f"{workers} heads of {wl.name} in parallel, one forked worker per core with one BLAS "
+                   f"thread: float64 pooling + scores + selection over all {nb} query blocks of each head, "
+                   f"then block-sparse attention on {blocks} query blocks in all ({budget_s:.0f} s budget per "
+                   f"worker); value = kept FLOPs of those blocks / wall seconds"),
+        "wall_seconds": round(wall, 3),
+        "attention_core_seconds": round(attn_s, 3),
+        "selection_core_seconds_per_head": round(select_s / workers, 3),
+        "attention_blocks": blocks,
         "cpu_model": _cpu_model(),
     }
 
@@ -197,6 +235,13 @@ def measure(args, wl, with_cpu: bool):
 
     print(f"[bench] generating {wl.name}", file=sys.stderr, flush=True)
     bits = inputs.generate(wl)
+    cpu = None
+    if with_cpu:
+        # before the first device call: the forked workers inherit no GPU state
+        print(f"[bench] cpu baseline (~{args.cpu_seconds:.0f} s per worker)", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(wl, bits, args.cpu_seconds)
+        print(f"[bench] cpu baseline {cpu['value']:.4f} TFLOP/s on {cpu['cores']} cores", file=sys.stderr,
+              flush=True)
     dev = {n: inputs.to_device(bits[n]) for n in ("q", "k", "v")}
     prob = sva.problem_for(wl)
     sel = sva.select_for(wl)
@@ -403,10 +448,11 @@ def measure(args, wl, with_cpu: bool):
                              for n in tp_ms}}
     del x, scores, kept_idx, kept_pos, ws, xk, xo
 
-    cpu = None
-    if with_cpu:
-        print(f"[bench] cpu baseline (~{args.cpu_seconds:.0f} s)", file=sys.stderr, flush=True)
-        cpu = cpu_baseline(wl, bits, args.cpu_seconds)
+    if cpu is not None:
+        # the whole layer on the same cores at the measured rate (kept FLOPs of
+        # every row plus each head's selection), an extrapolation
+        cpu["full_layer_seconds_extrapolated"] = round(
+            flops / (cpu["value"] * 1e12) + cpu["selection_core_seconds_per_head"] * B * H / cpu["cores"], 1)
 
     sel_desc = (f"cumulative mass tau={wl.mass_threshold} cap={kmax}" if wl.mode == "mass"
                 else f"top-k k={kmax} (r={wl.keep_ratio})" if not wl.topk else f"top-k k={wl.topk}")

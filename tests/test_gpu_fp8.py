@@ -27,6 +27,7 @@ import oracle.fp8_attention as of8
 import paper_2606_23743_amd as sva
 from paper_2606_23743_amd import inputs, workloads
 
+from . import fp8_bounds as fb
 from .gpu_cases import device_inputs, oracle_pool_all, oracle_select, say, scale_of
 
 pytestmark = pytest.mark.gpu
@@ -125,6 +126,58 @@ def _check_attention(got, got_lse, quant_ref, kept_row_lists, S, scale, rows, ou
     return np.sqrt(err2 / cnt), np.sqrt(pred2 / cnt)
 
 
+def _check_against_unquantised(got, bits, b, h, quant_ref, kept_row_lists, S, rows, out_bf16=True, queries=None):
+    """The GPU's 8-bit attention (got: [N, D] of head (b, h)) against softmax
+    attention of the unquantised bf16 inputs in float64.  Per element the
+    error may reach the P-rounding worst case of _check_attention (taken on
+    the dequantised values) plus SIGMAS standard deviations of the storage
+    error model (tests/fp8_bounds.py: Q, K, V stored as e4m3 at their group
+    scales) plus the bf16 output's rounding; the RMS over all checked
+    elements must stay under twice the combined model.  queries: offsets
+    inside each block to check (all when None).  Returns (mean |err|, max
+    |err|, rms, model rms)."""
+    x = {n: oracle.bf16_bits_to_f64(bits[n][b, h]) for n in ("q", "k", "v")}
+    N, D = x["q"].shape
+    c = 1.0 / np.sqrt(D)
+    lam = of8.softmax_scale_log2(D)
+    qf = of8.fold_scale(x["q"], lam)
+    ks = (x["k"].astype(np.float32) - quant_ref["k_mean"][0, 0].astype(np.float32)).astype(np.float64)
+    qh, kh, vh = (quant_ref[n][0, 0] for n in ("q_hat", "k_hat", "v_hat"))
+    q_exp, k_exp, v_exp = (quant_ref[n][0, 0] for n in ("q_exp", "k_exp", "v_exp"))
+    tok_block = np.arange(N) // S
+    abs_sum, n_el, err_max, err2, pred2 = 0.0, 0, 0.0, 0.0, 0.0
+    for i in rows:
+        qa, qb = i * S, min(N, (i + 1) * S)
+        blocks = kept_row_lists[i]
+        if not blocks:
+            continue
+        keys = np.concatenate([np.arange(j * S, min(N, (j + 1) * S)) for j in blocks])
+        qs = np.arange(qa, qb) if queries is None else np.array([qa + o for o in queries if qa + o < qb])
+        step = max(1, min(8, 12_000_000 // (len(keys) * D)))
+        for s0 in range(0, len(qs), step):
+            qi = qs[s0:s0 + step]
+            p, o, _ = fb.exact_attention(x["q"][qi], x["k"][keys], x["v"][keys], c)
+            eq, ek, ev = fb.storage_errors(qf[qi], q_exp[tok_block[qi]], ks[keys], k_exp[tok_block[keys]],
+                                           x["v"][keys], v_exp[:D])
+            _, var_q = fb.quantisation_effect(qf[qi], eq, ks[keys], ek, x["v"][keys], ev, p, o)
+            # P rounding and the fp8 products' summation, on the dequantised values
+            ph, oh, _ = fb.exact_attention(qh[qi], kh[keys], vh[keys], of8.LN2)
+            e = np.maximum(2.0 ** -4 * ph, np.minimum(ph, 2.0 ** -16)) + 4e-3 * ph
+            dev = np.abs(vh[keys][None, :, :] - oh[:, None, :])
+            bound_p = (e[:, :, None] * dev).sum(axis=1)
+            var_p = ((e * e / 3.0)[:, :, None] * dev * dev).sum(axis=1)
+            var = var_q + var_p + ((2.0 ** -8 * oh) ** 2 / 3.0 if out_bf16 else 0.0)
+            d = got[qi] - o
+            bound = bound_p + fb.SIGMAS * np.sqrt(var_q) + 2.0 ** -8 * np.abs(oh) + 1e-6
+            assert np.all(np.abs(d) <= bound), (i, float((np.abs(d) - bound).max()))
+            abs_sum += float(np.abs(d).sum())
+            n_el += d.size
+            err_max = max(err_max, float(np.abs(d).max()))
+            err2 += float((d * d).sum())
+            pred2 += float(var.sum())
+    return abs_sum / n_el, err_max, np.sqrt(err2 / n_el), np.sqrt(pred2 / n_el)
+
+
 CASES = [
     # (name, B, H, D, grid, S, keep)
     ("d128_s128_ragged", 1, 2, 128, (3, 5, 16), 128, 0.5),
@@ -173,6 +226,12 @@ def test_fp8_quantise_and_attend(name, B, H, D, grid, S, keep):
             assert drms <= 2.0 * dpred + 5e-4, (b, h, drms, dpred)
             say(f"[fp8 {name}] b{b} h{h}: sparse rms {rms:.2e} (model {pred:.2e}), dense rms {drms:.2e} "
                 f"(model {dpred:.2e})")
+            # against attention of the unquantised inputs
+            mean_u, max_u, rms_u, pred_u = _check_against_unquantised(o[b, h], bits, b, h, ref, kept[b][h], S,
+                                                                      rows)
+            assert rms_u <= 2.0 * pred_u, (b, h, rms_u, pred_u)
+            say(f"[fp8 {name}] b{b} h{h} vs unquantised: mean |err| {mean_u:.2e}, max {max_u:.2e}, "
+                f"rms {rms_u:.2e} (model {pred_u:.2e})")
 
 
 @pytest.mark.parametrize("S,D,step", [(128, 128, 3.0), (128, 128, 40.0), (64, 128, 3.0), (64, 112, 40.0),
@@ -322,4 +381,62 @@ def test_fp8_full_size_sampled():
         say(f"[fp8 {wl.name}] head {h}: rms {rms:.2e} (model {pred:.2e})")
         assert rms <= 2.0 * pred + 5e-4
     del dev, quant, out, lse
+    torch.cuda.empty_cache()
+
+
+def test_fp8_full_size_against_unquantised():
+    """The 64B-class layer on the GPU's own kept lists: 8-bit attention
+    against softmax attention of the unquantised inputs on sampled query
+    blocks (the first two and the last of three heads, three random ones, and
+    the block holding the largest difference between the 8-bit and the bf16
+    kernel over the whole layer), 32 queries of each (the block's first and
+    last 16, and the token of the largest difference).  Per element within
+    the derived bounds; the mean error is reported beside the 2e-3 bar the
+    bf16 path meets."""
+    wl = workloads.LARGE_64B
+    say(f"[fp8 vs unquantised {wl.name}] generating")
+    bits = inputs.generate(wl)
+    dev = device_inputs(bits)
+    prob = sva.problem_for(wl)
+    S, H, N = wl.block, wl.heads, wl.seq_len
+    nb = oracle.num_blocks(N, S)
+    qp, kp = sva.pool_blocks(prob, dev["q"], dev["k"])
+    idx, cnt, _ = sva.select_blocks(prob, sva.select_for(wl), qp, kp)
+    quant = sva.quantize_fp8(prob, dev["q"], dev["k"], dev["v"])
+    o8, _ = sva.sparse_attention_fp8(prob, quant, idx, cnt)
+    o16, _ = sva.sparse_attention(prob, dev["q"], dev["k"], dev["v"], idx, cnt)
+    torch.cuda.synchronize()
+    diff = (o8.float() - o16.float()).abs()
+    flat = int(torch.argmax(diff).item())
+    hw, nw = (flat // (N * wl.head_dim)) % H, (flat // wl.head_dim) % N
+    say(f"[fp8 vs unquantised {wl.name}] largest |fp8 - bf16| {diff.max().item():.3f} at head {hw} token {nw}; "
+        f"mean {diff.mean().item():.2e}")
+    del diff, o16, quant, qp, kp
+    idx_h, cnt_h = _np(idx), _np(cnt)
+    rng = np.random.default_rng(11)
+    picks = {0: [0, 1, nb - 1], H // 2: [0, 1, nb - 1], H - 1: [0, 1, nb - 1]}
+    for h in (0, H // 2, H - 1):
+        picks[h] += rng.choice(np.arange(2, nb - 1), 1).tolist()
+    picks.setdefault(hw, [])
+    picks[hw].append(nw // S)
+    o = _np(o8.float()).astype(np.float64)
+    total, n_rows, worst = 0.0, 0, 0.0
+    for h, rows in sorted(picks.items()):
+        ref = _dequantised(bits, S, 0, h)
+        kept_rows = {i: idx_h[0, h, i, :cnt_h[0, h, i]].tolist() for i in rows}
+        lists = [kept_rows.get(i, []) for i in range(nb)]
+        offs = list(range(16)) + list(range(S - 16, S))
+        if h == hw and nw % S not in offs:
+            offs.append(nw % S)                      # the token of the largest difference
+        mean_u, max_u, rms_u, pred_u = _check_against_unquantised(o[0, h], bits, 0, h, ref, lists, S,
+                                                                  sorted(set(rows)), queries=offs)
+        assert rms_u <= 2.0 * pred_u, (h, rms_u, pred_u)
+        say(f"[fp8 vs unquantised {wl.name}] head {h} blocks {sorted(set(rows))}: mean |err| {mean_u:.2e}, "
+            f"max {max_u:.2e}, rms {rms_u:.2e} (model {pred_u:.2e})")
+        total += mean_u
+        n_rows += 1
+        worst = max(worst, max_u)
+    say(f"[fp8 vs unquantised {wl.name}] mean |err| over the sampled heads {total / n_rows:.2e} "
+        f"(the bf16 path's bar: 2e-3), max {worst:.2e}")
+    del dev, o8
     torch.cuda.empty_cache()
