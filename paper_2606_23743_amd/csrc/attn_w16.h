@@ -1,6 +1,6 @@
 // Per-chunk arithmetic of the bf16 attention kernels on mfma_f32_16x16x32_bf16
-// (attention_q16.hip, attention_pair.hip): 32 queries per wave as two tiles of
-// 16, one staged 32-key chunk at a time.
+// (attention_q16.hip, attention_pair.hip): QT tiles of 16 queries per wave
+// (two: 32 queries), one staged 32-key chunk at a time.
 //
 // Lane l = 16g + i (group g = 0..3, column i = 0..15).  For query tile qt the
 // lane holds query qt*16 + i:
@@ -51,12 +51,12 @@ __device__ __forceinline__ void operand_offsets16(int lane, int (&koff)[Geo16<D>
 
 // Q^T operands of queries qbase + qt*16 + i at d = 32s + 8g .. +8; zero for an
 // absent query or d >= D
-template <int D>
-__device__ __forceinline__ void load_q16(bf16x8 (&qop)[2][Geo16<D>::KS], const uint16_t* Qh, int qbase, int N,
+template <int D, int QT>
+__device__ __forceinline__ void load_q16(bf16x8 (&qop)[QT][Geo16<D>::KS], const uint16_t* Qh, int qbase, int N,
                                          int lane) {
   const int g = lane >> 4, i = lane & 15;
 #pragma unroll
-  for (int qt = 0; qt < 2; ++qt) {
+  for (int qt = 0; qt < QT; ++qt) {
     const int q = qbase + qt * 16 + i;
 #pragma unroll
     for (int s = 0; s < Geo16<D>::KS; ++s) {
@@ -67,33 +67,36 @@ __device__ __forceinline__ void load_q16(bf16x8 (&qop)[2][Geo16<D>::KS], const u
   }
 }
 
-template <int D>
-__device__ __forceinline__ void qk16(f32x4 (&sacc)[2][2], const unsigned char* kt, const int (&koff)[Geo16<D>::KS],
-                                     const bf16x8 (&qop)[2][Geo16<D>::KS]) {
+template <int D, int QT>
+__device__ __forceinline__ void qk16(f32x4 (&sacc)[2][QT], const unsigned char* kt, const int (&koff)[Geo16<D>::KS],
+                                     const bf16x8 (&qop)[QT][Geo16<D>::KS]) {
   using G = Geo<D>;
 #pragma unroll
-  for (int k2 = 0; k2 < 2; ++k2) sacc[k2][0] = sacc[k2][1] = f32x4{};
+  for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) sacc[k2][qt] = f32x4{};
 #pragma unroll
   for (int s = 0; s < Geo16<D>::KS; ++s)
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2) {
       const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kt + koff[s] + k2 * 16 * G::RB);
 #pragma unroll
-      for (int qt = 0; qt < 2; ++qt)
+      for (int qt = 0; qt < QT; ++qt)
         sacc[k2][qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qop[qt][s], sacc[k2][qt], 0, 0, 0);
     }
 }
 
 // keys of the chunk at or past `valid` (the sequence's last partial chunk) to -inf
-__device__ __forceinline__ void mask_tail16(f32x4 (&sacc)[2][2], int valid, int lane) {
+template <int QT>
+__device__ __forceinline__ void mask_tail16(f32x4 (&sacc)[2][QT], int valid, int lane) {
   const int g = lane >> 4;
 #pragma unroll
   for (int k2 = 0; k2 < 2; ++k2)
 #pragma unroll
     for (int r = 0; r < 4; ++r)
       if (k2 * 16 + 4 * g + r >= valid) {
-        sacc[k2][0][r] = -INFINITY;
-        sacc[k2][1][r] = -INFINITY;
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) sacc[k2][qt][r] = -INFINITY;
       }
 }
 
@@ -110,9 +113,10 @@ __device__ __forceinline__ float quad_sum(float x) {
 
 // the reference maximum (log2 units) of each query tile from a chunk that
 // holds a valid key
-__device__ __forceinline__ void chunk_reference16(const f32x4 (&sacc)[2][2], float sl2, float (&m_ref)[2]) {
+template <int QT>
+__device__ __forceinline__ void chunk_reference16(const f32x4 (&sacc)[2][QT], float sl2, float (&m_ref)[QT]) {
 #pragma unroll
-  for (int qt = 0; qt < 2; ++qt) {
+  for (int qt = 0; qt < QT; ++qt) {
     float mx = sacc[0][qt][0];
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2)
@@ -122,11 +126,12 @@ __device__ __forceinline__ void chunk_reference16(const f32x4 (&sacc)[2][2], flo
   }
 }
 
-__device__ __forceinline__ void softmax16(const f32x4 (&sacc)[2][2], bf16x8 (&pop)[2], float (&l_part)[2],
-                                          const float (&m_ref)[2], float sl2) {
+template <int QT>
+__device__ __forceinline__ void softmax16(const f32x4 (&sacc)[2][QT], bf16x8 (&pop)[QT], float (&l_part)[QT],
+                                          const float (&m_ref)[QT], float sl2) {
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 #pragma unroll
-  for (int qt = 0; qt < 2; ++qt) {
+  for (int qt = 0; qt < QT; ++qt) {
     u32x4 wv;
     float lsum = l_part[qt];
 #pragma unroll
@@ -158,14 +163,14 @@ __device__ __forceinline__ bf16x8 tr_operand16(const unsigned char* tile, int vo
   return __builtin_bit_cast(bf16x8, vw);
 }
 
-template <int D>
-__device__ __forceinline__ void pv16(const bf16x8 (&pop)[2], const unsigned char* vt, const int (&voff)[Geo16<D>::DT],
-                                     f32x4 (&oacc)[Geo16<D>::DT][2]) {
+template <int D, int QT>
+__device__ __forceinline__ void pv16(const bf16x8 (&pop)[QT], const unsigned char* vt, const int (&voff)[Geo16<D>::DT],
+                                     f32x4 (&oacc)[Geo16<D>::DT][QT]) {
 #pragma unroll
   for (int dt = 0; dt < Geo16<D>::DT; ++dt) {
     const bf16x8 vop = tr_operand16<D>(vt, voff[dt]);
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt)
+    for (int qt = 0; qt < QT; ++qt)
       oacc[dt][qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop[qt], oacc[dt][qt], 0, 0, 0);
   }
 }
@@ -175,13 +180,16 @@ __device__ __forceinline__ void pv16(const bf16x8 (&pop)[2], const unsigned char
 // power of two (exact).  Rows never come near 2^64 in practice, so this is one
 // compare and a branch per block; a row that still overflows inside one block
 // is caught by overflowed16 at the end.
-template <int D>
-__device__ __forceinline__ void rescale_if_large16(float (&l_part)[2], float (&m_ref)[2],
-                                                   f32x4 (&oacc)[Geo16<D>::DT][2]) {
-  if (__builtin_amdgcn_ballot_w64(l_part[0] > 0x1p64f || l_part[1] > 0x1p64f) != 0) {
+template <int D, int QT>
+__device__ __forceinline__ void rescale_if_large16(float (&l_part)[QT], float (&m_ref)[QT],
+                                                   f32x4 (&oacc)[Geo16<D>::DT][QT]) {
+  bool big = false;
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) big |= l_part[qt] > 0x1p64f;
+  if (__builtin_amdgcn_ballot_w64(big) != 0) {
     asm volatile("");
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt) {
+    for (int qt = 0; qt < QT; ++qt) {
       const float l_tot = quad_sum(l_part[qt]);
       const int e = l_tot > 0x1p64f ? __builtin_amdgcn_frexp_expf(l_tot) : 0;
       const float f = __builtin_amdgcn_ldexpf(1.0f, -e);
@@ -197,13 +205,15 @@ __device__ __forceinline__ void rescale_if_large16(float (&l_part)[2], float (&m
 
 // a query that would need the per-iteration rescaling: sum past 2^100 or a
 // non-finite accumulator
-template <int D>
-__device__ __forceinline__ bool overflowed16(const float (&l_tot)[2], const f32x4 (&oacc)[Geo16<D>::DT][2]) {
-  bool bad = !(l_tot[0] < 0x1p100f) || !(l_tot[1] < 0x1p100f);
+template <int D, int QT>
+__device__ __forceinline__ bool overflowed16(const float (&l_tot)[QT], const f32x4 (&oacc)[Geo16<D>::DT][QT]) {
+  bool bad = false;
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) bad |= !(l_tot[qt] < 0x1p100f);
 #pragma unroll
   for (int dt = 0; dt < Geo16<D>::DT; ++dt)
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt)
+    for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) bad |= !__builtin_isfinite(oacc[dt][qt][r]);
   return bad;
@@ -212,13 +222,13 @@ __device__ __forceinline__ bool overflowed16(const float (&l_tot)[2], const f32x
 // O = O^T / l of the lane's two queries (qbase + qt*16 + i, those below N) at
 // d = 16dt + 4g .. +4, and their LSE; zeros and -inf for a query that attended
 // to nothing (has[qt] false)
-template <int D, bool OUT_F32>
+template <int D, bool OUT_F32, int QT>
 __device__ __forceinline__ void store_query16(void* out, float* lse, size_t head, size_t lse_head, int qbase, int N,
-                                              const f32x4 (&oacc)[Geo16<D>::DT][2], const float (&l_tot)[2],
-                                              const float (&m_ref)[2], const bool (&has)[2], int lane) {
+                                              const f32x4 (&oacc)[Geo16<D>::DT][QT], const float (&l_tot)[QT],
+                                              const float (&m_ref)[QT], const bool (&has)[QT], int lane) {
   const int g = lane >> 4, i = lane & 15;
 #pragma unroll
-  for (int qt = 0; qt < 2; ++qt) {
+  for (int qt = 0; qt < QT; ++qt) {
     const int q = qbase + qt * 16 + i;
     if (q >= N) continue;
     const float inv = has[qt] ? 1.0f / l_tot[qt] : 0.0f;
