@@ -177,7 +177,14 @@ int sva_select_blocks(const sva_problem* prob, const sva_select_params* sel,
  *   lse       : float32 [B, H, N] device or NULL; natural-log log-sum-exp of
  *               the scaled logits of each query (-inf for an empty row)
  * bf16 MFMA products with float32 accumulation and an online softmax in
- * float32.  Duplicate entries in a row are attended twice. */
+ * float32.  Duplicate entries in a row are attended twice.
+ * Performance: the fast kernels finish a query block in one pass; a block
+ * whose row sums would overflow float32 (logits rising by more than about
+ * 2^63 within one kept block), whose inputs hold Inf or NaN, or, at block 64
+ * with D = 128 and long rows, whose pair of lists is not strictly increasing
+ * and in range, is marked through its output and redone by a per-block
+ * rescaling kernel on a small grid (correct, but many times slower per
+ * block).  Lists as sva_select_blocks writes them never take that path. */
 int sva_sparse_attention(const sva_problem* prob, const void* q, const void* k,
                          const void* v, const int32_t* kv_idx,
                          const int32_t* kv_count, int32_t kmax, void* out,
