@@ -56,9 +56,12 @@ void attn_pair_kernel(AttnArgs a, int n_pairs) {
   const float sl2 = a.scale_log2;
 
   const int npb = (nB + 1) / 2;              // pairs per (b, h)
-  const int pr = __builtin_amdgcn_readfirstlane(xcd_remap(blockIdx.x, n_pairs));
+  // segments of 8 x 64 pairs (the eight XCDs on one head at a time), and
+  // inside a head frame tiles of 2 pairs x 8 frames
+  const int pr = __builtin_amdgcn_readfirstlane(xcd_remap_segments(blockIdx.x, n_pairs, 64));
   const int bh = pr / npb;
-  const int p = pr - bh * npb;
+  const int pairs_per_frame = max(1, (a.frame_blocks + 1) / 2);
+  const int p = frame_tile_order(pr - bh * npb, npb, pairs_per_frame, 8, 2);
   const int qsel = w >> 1;                   // 0: block 2p, 1: block 2p+1
   const int qb = 2 * p + qsel;               // this wave's query block (may be nB: none)
   const bool has_b = 2 * p + 1 < nB;

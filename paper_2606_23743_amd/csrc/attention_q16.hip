@@ -27,12 +27,13 @@
 // inside one block) is marked (NaN first element) and recomputed by the
 // per-iteration rescaling kernel that runs next.
 //
-// Workgroup order: sparse lists at S = 128 run in segments of 8 x 128 rows
-// (xcd_remap_segments: the eight XCDs work through one head at a time) and,
-// inside a head, in frame tiles of 4 consecutive query blocks x 8 frames
-// (frame_tile_order), so the query blocks an XCD runs at once are neighbours
-// in (t, y, x) and keep mostly the same key blocks; the rest run whole ranges
-// of rows per XCD (xcd_remap).
+// Workgroup order: sparse lists run, inside a head, in frame tiles of 4
+// consecutive query blocks x 8 frames (frame_tile_order), so the query blocks
+// an XCD runs at once are neighbours in (t, y, x) and keep mostly the same key
+// blocks.  At S = 128 the rows are also cut into segments of 8 x 128
+// (xcd_remap_segments: the eight XCDs work through one head at a time); at
+// S = 64, and for dense walks, each XCD takes a whole range of rows
+// (xcd_remap).
 #include "attn_w16.h"
 
 namespace sva {
@@ -64,11 +65,11 @@ void attn_q16_kernel(AttnArgs a) {
   const int N = a.N, nB = a.nB;
   const float sl2 = a.scale_log2;
 
-  constexpr bool kTiled = SPARSE && S == 128;
-  const int wg = kTiled ? xcd_remap_segments(blockIdx.x, a.n_rows, 128) : xcd_remap(blockIdx.x, a.n_rows);
+  constexpr bool kSegments = SPARSE && S == 128;
+  const int wg = kSegments ? xcd_remap_segments(blockIdx.x, a.n_rows, 128) : xcd_remap(blockIdx.x, a.n_rows);
   const int rowl = __builtin_amdgcn_readfirstlane(wg);   // (b*H + h)*nB + logical block
   const int bh = rowl / nB;
-  const int i = kTiled ? frame_tile_order(rowl - bh * nB, nB, a.frame_blocks, 8, 4) : rowl - bh * nB;
+  const int i = SPARSE ? frame_tile_order(rowl - bh * nB, nB, a.frame_blocks, 8, 4) : rowl - bh * nB;
   const int row = bh * nB + i;
   const size_t head = (size_t)bh * N * D;
   const uint16_t* Qh = a.q + head;
