@@ -103,9 +103,15 @@ void attn_fp8_kernel(Fp8AttnArgs a) {
   const int l32 = lane & 31;
   const int N = a.N, nB = a.nB, Np = a.Np;
 
-  const int row = __builtin_amdgcn_readfirstlane(xcd_remap(blockIdx.x, a.n_rows));  // (b*H + h)*nB + i
-  const int bh = row / nB;
-  const int i = row - bh * nB;
+  // workgroup order as in the bf16 kernel: sparse lists in frame tiles of 4
+  // query blocks x 8 frames inside a head, at S = 128 also in segments of
+  // 8 x 128 rows (the eight XCDs on one head at a time)
+  constexpr bool kSegments = SPARSE && S == 128;
+  const int wg = kSegments ? xcd_remap_segments(blockIdx.x, a.n_rows, 128) : xcd_remap(blockIdx.x, a.n_rows);
+  const int rowl = __builtin_amdgcn_readfirstlane(wg);   // (b*H + h)*nB + logical block
+  const int bh = rowl / nB;
+  const int i = SPARSE ? frame_tile_order(rowl - bh * nB, nB, a.frame_blocks, 8, 4) : rowl - bh * nB;
+  const int row = bh * nB + i;
   const size_t head = (size_t)bh * Np * DP;
 
   // ---- the block list: compacted, with each block's K exponent ----
@@ -447,6 +453,8 @@ hipError_t launch_attention_fp8(const Dims& d, bool sparse, const Fp8AttnArgs& a
   a.nB = d.nB;
   a.Np = d.nB * d.S;
   a.n_rows = d.B * d.H * d.nB;
+  const int64_t fb = ((int64_t)d.frame_tokens + d.S / 2) / d.S;
+  a.frame_blocks = fb < 1 ? 1 : (fb > d.nB ? d.nB : (int)fb);
   switch (d.D * 1000 + d.S) {
     case 64064: return launch_fp8_ds<64, 64>(d, sparse, a, stream);
     case 64128: return launch_fp8_ds<64, 128>(d, sparse, a, stream);

@@ -71,6 +71,7 @@ struct Fp8AttnArgs {
   void* out;
   float* lse;
   int N, nB, Np, kmax, n_rows;
+  int frame_blocks;   // query blocks per frame of the latent grid, rounded (>= 1)
 };
 // Largest kept-block list (and nB for the dense form) the fp8 kernel holds.
 constexpr int kFp8MaxList = 2047;
