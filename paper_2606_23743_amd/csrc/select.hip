@@ -33,8 +33,9 @@ struct SelectArgs {
 // the float64 scores of blocks j = t*64 + l (t < NT) for each of its rows.
 // kbar is staged through LDS 64 blocks at a time (the next chunk is loaded
 // into registers while this one is used), so every kbar row is read once per
-// R query rows.  Each score is one sequential float64 fma chain over d: the
-// fp32 products are exact in float64, so only the running sum rounds.
+// R query rows.  The scores of a chunk are float64 matrix products (16 rows x
+// 64 keys, one 16-key tile per wave), passed through LDS to the lane-per-key
+// layout of the rows' owners.
 //
 // Both rules end in a threshold key T and a quota: keys above T are kept, and
 // of the keys equal to T the `quota` lowest block indices.
@@ -90,11 +91,14 @@ __device__ __forceinline__ void kth_key(const uint64_t (&key)[NT], uint32_t k, u
 
 template <int NT, int RW, bool MASS>
 __global__ __launch_bounds__(kThreads) void select_reg_kernel(SelectArgs a) {
-  constexpr int R = 4 * RW;
+  constexpr int R = 4 * RW;          // rows of the workgroup
   constexpr int KP = 132;            // kbar row pitch in LDS (floats): conflict-free b128 reads
-  constexpr int QP = 128;            // qbar row pitch in LDS (doubles)
-  __shared__ __attribute__((aligned(16))) double qs[R * QP];
+  constexpr int QP = 132;            // qbar row pitch in LDS (doubles)
+  constexpr int SP = 66;             // score staging row pitch (doubles)
+  typedef double f64x4 __attribute__((ext_vector_type(4)));
+  __shared__ __attribute__((aligned(16))) double qs[16 * QP];
   __shared__ __attribute__((aligned(16))) float ks[64 * KP];
+  __shared__ __attribute__((aligned(16))) double ss[16 * SP];
 
   const int nB = a.nB, D = a.D;
   const int lane = threadIdx.x & 63;
@@ -105,9 +109,10 @@ __global__ __launch_bounds__(kThreads) void select_reg_kernel(SelectArgs a) {
   const float* qsrc = a.q_pool + (size_t)bh * nB * D;
   const float* ksrc = a.k_pool + (size_t)bh * nB * D;
 
-  for (int t = threadIdx.x; t < R * D; t += kThreads) {
+  // qbar of the R rows in float64 (rows R..15 of the score tiles are zero)
+  for (int t = threadIdx.x; t < 16 * D; t += kThreads) {
     const int g = t / D, d = t - g * D;
-    qs[g * QP + d] = (i0 + g < nB) ? (double)qsrc[(size_t)(i0 + g) * D + d] : 0.0;
+    qs[g * QP + d] = (g < R && i0 + g < nB) ? (double)qsrc[(size_t)(i0 + g) * D + d] : 0.0;
   }
 
   // kbar chunk: 64 rows x D floats = 16*D float4, at most 8 per thread (D <= 128)
@@ -133,36 +138,43 @@ __global__ __launch_bounds__(kThreads) void select_reg_kernel(SelectArgs a) {
     }
   };
 
+  // Scores on mfma_f64_16x16x4f64: wave w forms the 16 x 16 tile of keys
+  // c*64 + 16w + 0..15 against the 16 rows, S^T = Kbar Qbar^T.  Lane
+  // l = 16g + j feeds key j (A) and row j (B) at d = g*DG + s for step s, so
+  // the four lane groups split d into four runs of DG; the result puts key
+  // g + 4r of row j in its register r.  The fp32 products are exact in
+  // float64, so only the sums round (in an order free of consequence: the
+  // oracle's scores are a library matrix product).
+  const int DG = D >> 2;             // 16, 28 or 32: a multiple of 4
+  const int j16 = lane & 15, g4 = lane >> 4;
+  const float* ka = ks + (w * 16 + j16) * KP + g4 * DG;
+  const double* qb = qs + j16 * QP + g4 * DG;
+
   double sc[RW][NT];
   load_chunk(0);
 #pragma unroll
   for (int c = 0; c < NT; ++c) {
-    __syncthreads();                   // the previous chunk is consumed (q rows written)
+    __syncthreads();                   // the previous chunk and its scores are consumed (q rows written)
     store_chunk();
     __syncthreads();
     if (c + 1 < NT && (c + 1) * 64 < nB) load_chunk(c + 1);
-    double acc[RW];
-#pragma unroll
-    for (int r = 0; r < RW; ++r) acc[r] = 0.0;
     if (c * 64 < nB) {
-      const float* krow = ks + lane * KP;
-      const double* qrow = qs + (w * RW) * QP;
-      for (int d = 0; d < D; d += 4) {
-        const float4 kv = *reinterpret_cast<const float4*>(krow + d);
-        const double k0 = kv.x, k1 = kv.y, k2 = kv.z, k3 = kv.w;
-#pragma unroll
-        for (int r = 0; r < RW; ++r) {
-          const double2 qa = *reinterpret_cast<const double2*>(qrow + r * QP + d);
-          const double2 qb = *reinterpret_cast<const double2*>(qrow + r * QP + d + 2);
-          double x = fma(qa.x, k0, acc[r]);
-          x = fma(qa.y, k1, x);
-          x = fma(qb.x, k2, x);
-          acc[r] = fma(qb.y, k3, x);
-        }
+      f64x4 acc0 = {0.0, 0.0, 0.0, 0.0}, acc1 = {0.0, 0.0, 0.0, 0.0};
+      for (int s = 0; s < DG; s += 4) {
+        const float4 kv = *reinterpret_cast<const float4*>(ka + s);
+        const double2 q01 = *reinterpret_cast<const double2*>(qb + s);
+        const double2 q23 = *reinterpret_cast<const double2*>(qb + s + 2);
+        acc0 = __builtin_amdgcn_mfma_f64_16x16x4f64((double)kv.x, q01.x, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f64_16x16x4f64((double)kv.y, q01.y, acc1, 0, 0, 0);
+        acc0 = __builtin_amdgcn_mfma_f64_16x16x4f64((double)kv.z, q23.x, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f64_16x16x4f64((double)kv.w, q23.y, acc1, 0, 0, 0);
       }
-    }
 #pragma unroll
-    for (int r = 0; r < RW; ++r) sc[r][c] = a.scale * acc[r];
+      for (int r = 0; r < 4; ++r) ss[j16 * SP + w * 16 + g4 + 4 * r] = acc0[r] + acc1[r];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < RW; ++r) sc[r][c] = (c * 64 < nB) ? a.scale * ss[(w * RW + r) * SP + lane] : 0.0;
   }
 
   // one row at a time: the row index must be a compile-time constant so the
