@@ -7,8 +7,6 @@
 namespace sva {
 namespace {
 
-constexpr int kThreads = 256;
-
 __device__ __forceinline__ uint64_t order_key(double s) {
   if (s == 0.0) s = 0.0;          // -0 and +0 compare equal: give them one key
   const uint64_t b = (uint64_t)__double_as_longlong(s);
@@ -28,8 +26,9 @@ struct SelectArgs {
 };
 
 // ---------------------------------------------------------------------------
-// Selection with the scores in registers.  A workgroup (4 waves) takes R = 4*RW
-// query-block rows of one (b, h); each wave owns RW of them, and lane l holds
+// Selection with the scores in registers.  A workgroup (NW = 4 or 8 waves)
+// takes R = NW*RW = 16 query-block rows of one (b, h); each wave owns RW of
+// them (4, or 2 when nB > 1024 leaves no registers for four), and lane l holds
 // the float64 scores of blocks j = t*64 + l (t < NT) for each of its rows.
 // kbar is staged through LDS 64 blocks at a time (the next chunk is loaded
 // into registers while this one is used), so every kbar row is read once per
@@ -89,9 +88,11 @@ __device__ __forceinline__ void kth_key(const uint64_t (&key)[NT], uint32_t k, u
   quota = k - above;
 }
 
-template <int NT, int RW, bool MASS>
-__global__ __launch_bounds__(kThreads) void select_reg_kernel(SelectArgs a) {
-  constexpr int R = 4 * RW;          // rows of the workgroup
+template <int NT, int RW, int NW, bool MASS>
+__global__ __launch_bounds__(NW * 64) void select_reg_kernel(SelectArgs a) {
+  constexpr int NTH = NW * 64;       // threads
+  constexpr int R = NW * RW;         // rows of the workgroup (16)
+  static_assert(R == 16, "the score tiles hold 16 rows");
   constexpr int KP = 132;            // kbar row pitch in LDS (floats): conflict-free b128 reads
   constexpr int QP = 132;            // qbar row pitch in LDS (doubles)
   constexpr int SP = 66;             // score staging row pitch (doubles)
@@ -109,20 +110,21 @@ __global__ __launch_bounds__(kThreads) void select_reg_kernel(SelectArgs a) {
   const float* qsrc = a.q_pool + (size_t)bh * nB * D;
   const float* ksrc = a.k_pool + (size_t)bh * nB * D;
 
-  // qbar of the R rows in float64 (rows R..15 of the score tiles are zero)
-  for (int t = threadIdx.x; t < 16 * D; t += kThreads) {
+  // qbar of the 16 rows in float64
+  for (int t = threadIdx.x; t < 16 * D; t += NTH) {
     const int g = t / D, d = t - g * D;
-    qs[g * QP + d] = (g < R && i0 + g < nB) ? (double)qsrc[(size_t)(i0 + g) * D + d] : 0.0;
+    qs[g * QP + d] = (i0 + g < nB) ? (double)qsrc[(size_t)(i0 + g) * D + d] : 0.0;
   }
 
-  // kbar chunk: 64 rows x D floats = 16*D float4, at most 8 per thread (D <= 128)
+  // kbar chunk: 64 rows x D floats = 16*D float4, at most NPRE per thread (D <= 128)
+  constexpr int NPRE = 2048 / NTH;
   const int nf4 = 16 * D;
   const int d4 = D / 4;
-  float4 pre[8];
+  float4 pre[NPRE];
   auto load_chunk = [&](int c) {
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int e = threadIdx.x + u * kThreads;
+    for (int u = 0; u < NPRE; ++u) {
+      const int e = threadIdx.x + u * NTH;
       const int r = e / d4, c4 = e - r * d4;
       const int j = c * 64 + r;
       pre[u] = (e < nf4 && j < nB) ? *reinterpret_cast<const float4*>(ksrc + (size_t)j * D + c4 * 4)
@@ -131,15 +133,16 @@ __global__ __launch_bounds__(kThreads) void select_reg_kernel(SelectArgs a) {
   };
   auto store_chunk = [&]() {
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int e = threadIdx.x + u * kThreads;
+    for (int u = 0; u < NPRE; ++u) {
+      const int e = threadIdx.x + u * NTH;
       const int r = e / d4, c4 = e - r * d4;
       if (e < nf4) *reinterpret_cast<float4*>(ks + r * KP + c4 * 4) = pre[u];
     }
   };
 
-  // Scores on mfma_f64_16x16x4f64: wave w forms the 16 x 16 tile of keys
-  // c*64 + 16w + 0..15 against the 16 rows, S^T = Kbar Qbar^T.  Lane
+  // Scores on mfma_f64_16x16x4f64: wave w < 4 forms the 16 x 16 tile of keys
+  // c*64 + 16w + 0..15 against the 16 rows, S^T = Kbar Qbar^T (with eight
+  // waves the other four share the SIMDs and wait).    Lane
   // l = 16g + j feeds key j (A) and row j (B) at d = g*DG + s for step s, so
   // the four lane groups split d into four runs of DG; the result puts key
   // g + 4r of row j in its register r.  The fp32 products are exact in
@@ -147,7 +150,7 @@ __global__ __launch_bounds__(kThreads) void select_reg_kernel(SelectArgs a) {
   // oracle's scores are a library matrix product).
   const int DG = D >> 2;             // 16, 28 or 32: a multiple of 4
   const int j16 = lane & 15, g4 = lane >> 4;
-  const float* ka = ks + (w * 16 + j16) * KP + g4 * DG;
+  const float* ka = ks + ((w & 3) * 16 + j16) * KP + g4 * DG;
   const double* qb = qs + j16 * QP + g4 * DG;
 
   double sc[RW][NT];
@@ -158,7 +161,7 @@ __global__ __launch_bounds__(kThreads) void select_reg_kernel(SelectArgs a) {
     store_chunk();
     __syncthreads();
     if (c + 1 < NT && (c + 1) * 64 < nB) load_chunk(c + 1);
-    if (c * 64 < nB) {
+    if (c * 64 < nB && w < 4) {
       f64x4 acc0 = {0.0, 0.0, 0.0, 0.0}, acc1 = {0.0, 0.0, 0.0, 0.0};
       for (int s = 0; s < DG; s += 4) {
         const float4 kv = *reinterpret_cast<const float4*>(ka + s);
@@ -335,12 +338,14 @@ __global__ __launch_bounds__(kThreads) void select_reg_kernel(SelectArgs a) {
   if constexpr (RW > 3) select_row(std::integral_constant<int, 3>{});
 }
 
-template <int NT, int RW>
+template <int NT, int RW, int NW>
 hipError_t launch_reg(SelectArgs a, int B, int H, hipStream_t stream) {
-  a.n_groups = (a.nB + 4 * RW - 1) / (4 * RW);
+  a.n_groups = (a.nB + NW * RW - 1) / (NW * RW);
   a.n_work = B * H * a.n_groups;
-  if (a.mode == 0) hipLaunchKernelGGL((select_reg_kernel<NT, RW, false>), dim3(a.n_work), dim3(kThreads), 0, stream, a);
-  else hipLaunchKernelGGL((select_reg_kernel<NT, RW, true>), dim3(a.n_work), dim3(kThreads), 0, stream, a);
+  if (a.mode == 0)
+    hipLaunchKernelGGL((select_reg_kernel<NT, RW, NW, false>), dim3(a.n_work), dim3(NW * 64), 0, stream, a);
+  else
+    hipLaunchKernelGGL((select_reg_kernel<NT, RW, NW, true>), dim3(a.n_work), dim3(NW * 64), 0, stream, a);
   return hipGetLastError();
 }
 
@@ -366,13 +371,13 @@ hipError_t launch_select(const Dims& d, const SelectRule& r, const float* q_pool
   a.tau = r.tau;
   // nB <= SVA_SELECT_MAX_BLOCKS (2048) and D <= 128 are checked by the caller
   const int nt = (d.nB + 63) / 64;
-  if (nt <= 1) return launch_reg<1, 4>(a, d.B, d.H, stream);
-  if (nt <= 2) return launch_reg<2, 4>(a, d.B, d.H, stream);
-  if (nt <= 4) return launch_reg<4, 4>(a, d.B, d.H, stream);
-  if (nt <= 8) return launch_reg<8, 4>(a, d.B, d.H, stream);
-  if (nt <= 16) return launch_reg<16, 4>(a, d.B, d.H, stream);
-  if (nt <= 24) return launch_reg<24, 2>(a, d.B, d.H, stream);
-  if (nt <= 32) return launch_reg<32, 2>(a, d.B, d.H, stream);
+  if (nt <= 1) return launch_reg<1, 4, 4>(a, d.B, d.H, stream);
+  if (nt <= 2) return launch_reg<2, 4, 4>(a, d.B, d.H, stream);
+  if (nt <= 4) return launch_reg<4, 4, 4>(a, d.B, d.H, stream);
+  if (nt <= 8) return launch_reg<8, 4, 4>(a, d.B, d.H, stream);
+  if (nt <= 16) return launch_reg<16, 4, 4>(a, d.B, d.H, stream);
+  if (nt <= 24) return launch_reg<24, 2, 8>(a, d.B, d.H, stream);
+  if (nt <= 32) return launch_reg<32, 2, 8>(a, d.B, d.H, stream);
   return hipErrorInvalidValue;
 }
 
