@@ -28,6 +28,40 @@ LIMIT_CASES = [
 ]
 
 
+SELECT_CASES = [
+    SC("d112_nb1536_topk", 1, 2, 112, (6, 64, 256), 64, "topk", keep_ratio=0.1, seed=213),
+    SC("d112_nb1536_mass", 1, 2, 112, (6, 64, 256), 64, "mass", mass_threshold=0.9, max_keep_ratio=0.3,
+       force_first_frame=True, seed=214),
+]
+
+
+@pytest.mark.parametrize("wl", SELECT_CASES, ids=[c.name for c in SELECT_CASES])
+def test_selection_head_dim_112_past_1024_blocks(wl):
+    """Selection with D = 112 (score steps of 28 channels per lane group) at
+    1536 blocks per row, where a lane holds 24 registers of scores: every
+    row's kept list against the oracle's."""
+    say(f"[limits {wl.name}] N={wl.seq_len} nB={wl.seq_len // wl.block}")
+    bits = inputs.generate(wl)
+    dev = device_inputs(bits)
+    prob = sva.problem_for(wl)
+    sel = sva.select_for(wl)
+    nb = sva.num_blocks(prob)
+    assert nb == 1536
+    qp, kp = sva.pool_blocks(prob, dev["q"], dev["k"])
+    idx, cnt, _ = sva.select_blocks(prob, sel, qp, kp)
+    torch.cuda.synchronize()
+    f64 = {n: oracle.bf16_bits_to_f64(bits[n]) for n in ("q", "k")}
+    scores = oracle.block_scores(oracle.pool_blocks(f64["q"], wl.block), oracle.pool_blocks(f64["k"], wl.block),
+                                 scale_of(wl))
+    kept, info = oracle_select(wl, scores)
+    idx_np, cnt_np = idx.cpu().numpy(), cnt.cpu().numpy()
+    parity.check_idx_layout(idx_np, cnt_np, nb)
+    n, same, problems = parity.compare_masks(flat_rows(kept), parity.gpu_rows(idx_np, cnt_np), scores,
+                                             info["mode"], k=info["k"], tau=info["tau"], forced=info["forced"])
+    assert not problems, problems[:5]
+    say(f"[limits {wl.name}] selection rows={n} identical={same}")
+
+
 def _kept_arrays(kept, nb):
     kmax = max(1, max(len(r) for b in kept for h in b for r in h))
     idx, cnt = oracle.kept_to_arrays(kept, nb, kmax)
