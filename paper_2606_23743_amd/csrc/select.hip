@@ -377,6 +377,10 @@ hipError_t launch_select(const Dims& d, const SelectRule& r, const float* q_pool
   if (nt <= 2) return launch_reg<2, 2, 8>(a, d.B, d.H, stream);
   if (nt <= 4) return launch_reg<4, 2, 8>(a, d.B, d.H, stream);
   if (nt <= 8) return launch_reg<8, 2, 8>(a, d.B, d.H, stream);
+  // the mass rule's search (a wave sum per candidate bit) gains from one row
+  // per wave: 0.597 -> 0.533 ms at the 22B-class layer; the top-k search
+  // loses (0.339 -> 0.395 ms at the 64B-class layer)
+  if (nt <= 16 && a.mode != 0) return launch_reg<16, 1, 16>(a, d.B, d.H, stream);
   if (nt <= 16) return launch_reg<16, 2, 8>(a, d.B, d.H, stream);
   if (nt <= 24) return launch_reg<24, 2, 8>(a, d.B, d.H, stream);
   if (nt <= 32) return launch_reg<32, 2, 8>(a, d.B, d.H, stream);
