@@ -94,7 +94,7 @@ __global__ __launch_bounds__(NW * 64) void select_reg_kernel(SelectArgs a) {
   constexpr int R = NW * RW;         // rows of the workgroup (16)
   static_assert(R == 16, "the score tiles hold 16 rows");
   constexpr int KP = 132;            // kbar row pitch in LDS (floats): conflict-free b128 reads
-  constexpr int QP = 132;            // qbar row pitch in LDS (doubles)
+  constexpr int QP = 130;            // qbar row pitch in LDS (doubles): the 16 rows of a read group on distinct banks
   constexpr int SP = 66;             // score staging row pitch (doubles)
   typedef double f64x4 __attribute__((ext_vector_type(4)));
   __shared__ __attribute__((aligned(16))) double qs[16 * QP];
