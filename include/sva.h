@@ -219,10 +219,18 @@ int sva_dense_attention(const sva_problem* prob, const void* q, const void* k,
  * Requires nB <= SVA_REMAINDER_MAX_BLOCKS. ---- */
 #define SVA_REMAINDER_MAX_BLOCKS 4096
 
-/* Device workspace that sva_sparse_attention_remainder needs, in bytes
- * (about B*H*(N*D*4 + nB*D*D*4) + smaller parts; 5.7 GB for B=1, H=48,
- * N=111600, D=128, S=128).  Host only. */
+/* Device workspace that sva_sparse_attention_remainder needs to process all
+ * B*H (batch, head) pairs in one pass, in bytes (about B*H*(N*D*4 +
+ * nB*D*D*4) + smaller parts; 5.7 GB for B=1, H=48, N=111600, D=128, S=128).
+ * Host only. */
 int sva_remainder_workspace(const sva_problem* prob, size_t* bytes);
+
+/* The workspace for passes of `heads` consecutive (batch, head) pairs
+ * (1 <= heads <= B*H; heads = B*H gives sva_remainder_workspace).  A
+ * smaller workspace makes sva_sparse_attention_remainder process the pairs
+ * in groups, with the same results; 119 MB per pair at the sizes above.
+ * SVA_ERR_SHAPE for heads out of range.  Host only. */
+int sva_remainder_workspace_heads(const sva_problem* prob, int32_t heads, size_t* bytes);
 
 /* The block means and moments of the remainder.
  *   k, v     : bf16 [B, H, N, D] device
@@ -241,9 +249,14 @@ int sva_block_moments(const sva_problem* prob, const void* k, const void* v, voi
  * ones.  Arguments as for sva_sparse_attention, plus:
  *   q_pool, k_pool : float32 [B, H, nB, D] device, the block means from
  *                    sva_pool_blocks (or sva_qknorm_rope_pool); 16-byte aligned
- *   workspace      : device memory of at least sva_remainder_workspace bytes,
- *                    256-byte aligned, owned by the caller; its contents on
- *                    entry do not matter and on return are unspecified
+ *   workspace      : device memory, 256-byte aligned, owned by the caller;
+ *                    its contents on entry do not matter and on return are
+ *                    unspecified.  With sva_remainder_workspace bytes every
+ *                    (batch, head) pair is done in one pass; with less (at
+ *                    least sva_remainder_workspace_heads(prob, 1)) the pairs
+ *                    are done in consecutive groups of as many as fit, each
+ *                    group's kernels one after the other on `stream`, with
+ *                    the same results; SVA_ERR_SHAPE below one pair's size
  *   out, lse       : the compensated output and its log-sum-exp (lse may be
  *                    NULL), written for every valid token
  * Steps (all on `stream`): the kept blocks exactly with a float32 output into

@@ -77,6 +77,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "sva_sparse_attention": [P, vp, vp, vp, vp, vp, ctypes.c_int32, vp, vp, vp],
         "sva_dense_attention": [P, vp, vp, vp, vp, vp, vp],
         "sva_remainder_workspace": [P, ctypes.POINTER(ctypes.c_size_t)],
+        "sva_remainder_workspace_heads": [P, ctypes.c_int32, ctypes.POINTER(ctypes.c_size_t)],
         "sva_block_moments": [P, vp, vp, vp, vp, vp, vp],
         "sva_sparse_attention_remainder": [P, vp, vp, vp, vp, vp, vp, vp, ctypes.c_int32, vp,
                                            ctypes.c_size_t, vp, vp, vp],
@@ -340,9 +341,16 @@ def sparse_attention(prob: Problem, q, k, v, kv_idx, kv_count, out=None, want_ls
     return out, lse
 
 
-def remainder_workspace(prob: Problem) -> int:
+def remainder_workspace(prob: Problem, heads: Optional[int] = None) -> int:
+    """Workspace bytes of sparse_attention_remainder: for all (batch, head)
+    pairs in one pass (sva_remainder_workspace), or for passes of `heads`
+    pairs (sva_remainder_workspace_heads)."""
     out = ctypes.c_size_t(0)
-    _check(load().sva_remainder_workspace(ctypes.byref(prob), ctypes.byref(out)), "sva_remainder_workspace")
+    if heads is None:
+        _check(load().sva_remainder_workspace(ctypes.byref(prob), ctypes.byref(out)), "sva_remainder_workspace")
+    else:
+        _check(load().sva_remainder_workspace_heads(ctypes.byref(prob), int(heads), ctypes.byref(out)),
+               "sva_remainder_workspace_heads")
     return out.value
 
 
@@ -374,7 +382,9 @@ def sparse_attention_remainder(prob: Problem, q, k, v, q_pool, k_pool, kv_idx, k
                                want_lse: bool = False, lse=None, workspace=None, stream=None) -> Tuple:
     """sva_sparse_attention_remainder: the kept blocks exactly plus the
     first-order remainder of the dropped ones.  workspace: a uint8 device
-    tensor of remainder_workspace bytes (allocated when None)."""
+    tensor of remainder_workspace bytes (allocated when None), or of at least
+    remainder_workspace(prob, 1), with which the (batch, head) pairs are done
+    in groups of as many as fit."""
     torch = _torch()
     nb = num_blocks(prob)
     shp = _qkv_shape(prob)
@@ -390,11 +400,11 @@ def sparse_attention_remainder(prob: Problem, q, k, v, q_pool, k_pool, kv_idx, k
         lse = torch.empty(shp[:3], dtype=torch.float32, device=q.device)
     if lse is not None:
         _need(lse, torch.float32, shp[:3], "lse")
-    ws_bytes = remainder_workspace(prob)
     if workspace is None:
-        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
-    if workspace.dtype != torch.uint8 or not workspace.is_cuda or workspace.numel() < ws_bytes:
-        raise ValueError(f"workspace must be a uint8 device tensor of at least {ws_bytes} bytes")
+        workspace = torch.empty(remainder_workspace(prob), dtype=torch.uint8, device=q.device)
+    ws_min = remainder_workspace(prob, 1)
+    if workspace.dtype != torch.uint8 or not workspace.is_cuda or workspace.numel() < ws_min:
+        raise ValueError(f"workspace must be a uint8 device tensor of at least {ws_min} bytes")
     _check(load().sva_sparse_attention_remainder(
         ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(q_pool), _ptr(k_pool), _ptr(kv_idx), _ptr(kv_count),
         int(kmax), _ptr(workspace), int(workspace.numel()), _ptr(out), _ptr(lse), _stream(stream)),

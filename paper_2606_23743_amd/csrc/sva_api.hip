@@ -5,6 +5,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 #include "../../include/sva.h"
 #include "sva_internal.h"
 
@@ -122,6 +124,15 @@ RemLayout rem_layout(const Dims& d) {
   L.T = off;    off += up(bh * nbp * D * D * 2);
   L.total = off;
   return L;
+}
+
+// The dims of a run of `heads` consecutive (b, h) pairs of d, taken as one
+// batch entry of `heads` heads (the kernels index the flattened b*H + h).
+Dims group_dims(const Dims& d, int heads) {
+  Dims g = d;
+  g.B = 1;
+  g.H = heads;
+  return g;
 }
 
 int check_remainder(const sva_problem* prob, Dims* d) {
@@ -399,6 +410,16 @@ int sva_remainder_workspace(const sva_problem* prob, size_t* bytes) {
   return SVA_OK;
 }
 
+int sva_remainder_workspace_heads(const sva_problem* prob, int32_t heads, size_t* bytes) {
+  if (!bytes) return SVA_ERR_INVALID_ARG;
+  Dims d;
+  const int st = check_remainder(prob, &d);
+  if (st != SVA_OK) return st;
+  if (heads < 1 || (int64_t)heads > (int64_t)d.B * d.H) return SVA_ERR_SHAPE;
+  *bytes = rem_layout(group_dims(d, heads)).total;
+  return SVA_OK;
+}
+
 int sva_block_moments(const sva_problem* prob, const void* k, const void* v, void* kbar, void* vbar,
                       void* moments, void* stream) {
   Dims d;
@@ -419,25 +440,14 @@ int sva_block_moments(const sva_problem* prob, const void* k, const void* v, voi
   return hip_status(sva::launch_block_moments(d, a, static_cast<hipStream_t>(stream)));
 }
 
-int sva_sparse_attention_remainder(const sva_problem* prob, const void* q, const void* k, const void* v,
-                                   const float* q_pool, const float* k_pool, const int32_t* kv_idx,
-                                   const int32_t* kv_count, int32_t kmax, void* workspace,
-                                   size_t workspace_bytes, void* out, float* lse, void* stream) {
-  Dims d;
-  const int st = check_remainder(prob, &d);
-  if (st != SVA_OK) return st;
-  if (!q || !k || !v || !q_pool || !k_pool || !kv_idx || !kv_count || !workspace || !out)
-    return SVA_ERR_INVALID_ARG;
-  if (kmax < 1) return SVA_ERR_SHAPE;
-  if ((int64_t)d.B * d.H * d.nB * kmax > ((int64_t)1 << 40)) return SVA_ERR_SHAPE;
+namespace {
+
+// One pass of the remainder over the (b, h) pairs that d describes, its
+// intermediates in the workspace laid out by rem_layout(d).
+hipError_t remainder_pass(const Dims& d, const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                          const float* q_pool, const float* k_pool, const int32_t* kv_idx, const int32_t* kv_count,
+                          int32_t kmax, unsigned char* ws, void* out, float* lse, hipStream_t s) {
   const RemLayout L = rem_layout(d);
-  if (workspace_bytes < L.total) return SVA_ERR_SHAPE;
-  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) || !aligned(q_pool, 16) ||
-      !aligned(k_pool, 16) || !aligned(kv_idx, 4) || !aligned(kv_count, 4) || (lse && !aligned(lse, 4)) ||
-      !aligned(workspace, 256))
-    return SVA_ERR_ALIGNMENT;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  unsigned char* ws = static_cast<unsigned char*>(workspace);
   float* oa = reinterpret_cast<float*>(ws + L.oa);
   float* lsea = reinterpret_cast<float*>(ws + L.lsea);
   uint16_t* kbar = reinterpret_cast<uint16_t*>(ws + L.kbar);
@@ -448,20 +458,19 @@ int sva_sparse_attention_remainder(const sva_problem* prob, const void* q, const
   // the kept blocks exactly, in float32 (merged once, at the end)
   Dims df = d;
   df.out_f32 = true;
-  hipError_t e = sva::launch_attention(df, true, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
-                                       static_cast<const uint16_t*>(v), kv_idx, kv_count, kmax, oa, lsea, s);
-  if (e != hipSuccess) return SVA_ERR_HIP;
+  hipError_t e = sva::launch_attention(df, true, q, k, v, kv_idx, kv_count, kmax, oa, lsea, s);
+  if (e != hipSuccess) return e;
 
   sva::RemMomentArgs ma{};
-  ma.k = static_cast<const uint16_t*>(k);
-  ma.v = static_cast<const uint16_t*>(v);
+  ma.k = k;
+  ma.v = v;
   ma.kbar = kbar;
   ma.vbar = vbar;
   ma.mom = mom;
   ma.N = d.N;
   ma.nB = d.nB;
   ma.rows = nbp;
-  if ((e = sva::launch_block_moments(d, ma, s)) != hipSuccess) return SVA_ERR_HIP;
+  if ((e = sva::launch_block_moments(d, ma, s)) != hipSuccess) return e;
 
   sva::RemWeightArgs wa{};
   wa.q_pool = q_pool;
@@ -487,7 +496,7 @@ int sva_sparse_attention_remainder(const sva_problem* prob, const void* q, const
   ga.n_wg = 0;                      // set by the launcher
 
   sva::RemAttnArgs aa{};
-  aa.q = static_cast<const uint16_t*>(q);
+  aa.q = q;
   aa.kbar = kbar;
   aa.vbar = vbar;
   aa.kv_idx = kv_idx;
@@ -505,7 +514,49 @@ int sva_sparse_attention_remainder(const sva_problem* prob, const void* q, const
   aa.n_rows = 0;                    // set by the launcher
   aa.scale = (float)d.scale;
   aa.scale_log2 = (float)(d.scale * 1.4426950408889634);
-  return hip_status(sva::launch_remainder(d, wa, ga, aa, s));
+  return sva::launch_remainder(d, wa, ga, aa, s);
+}
+
+}  // namespace
+
+int sva_sparse_attention_remainder(const sva_problem* prob, const void* q, const void* k, const void* v,
+                                   const float* q_pool, const float* k_pool, const int32_t* kv_idx,
+                                   const int32_t* kv_count, int32_t kmax, void* workspace,
+                                   size_t workspace_bytes, void* out, float* lse, void* stream) {
+  Dims d;
+  const int st = check_remainder(prob, &d);
+  if (st != SVA_OK) return st;
+  if (!q || !k || !v || !q_pool || !k_pool || !kv_idx || !kv_count || !workspace || !out)
+    return SVA_ERR_INVALID_ARG;
+  if (kmax < 1) return SVA_ERR_SHAPE;
+  if ((int64_t)d.B * d.H * d.nB * kmax > ((int64_t)1 << 40)) return SVA_ERR_SHAPE;
+  // as many (b, h) pairs per pass as the workspace holds: all of them with
+  // sva_remainder_workspace bytes, at least one
+  const int bh = d.B * d.H;
+  int group = bh;
+  if (workspace_bytes < rem_layout(d).total) {
+    group = (int)std::min<size_t>((size_t)bh, workspace_bytes / std::max<size_t>(1, rem_layout(group_dims(d, 1)).total));
+    while (group > 0 && rem_layout(group_dims(d, group)).total > workspace_bytes) --group;
+    if (group < 1) return SVA_ERR_SHAPE;
+  }
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) || !aligned(q_pool, 16) ||
+      !aligned(k_pool, 16) || !aligned(kv_idx, 4) || !aligned(kv_count, 4) || (lse && !aligned(lse, 4)) ||
+      !aligned(workspace, 256))
+    return SVA_ERR_ALIGNMENT;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  const size_t nd = (size_t)d.N * d.D, nbd = (size_t)d.nB * d.D;
+  const size_t out_elem = d.out_f32 ? 4 : 2;
+  for (int h0 = 0; h0 < bh; h0 += group) {
+    const int g = std::min(group, bh - h0);
+    const hipError_t e = remainder_pass(
+        group_dims(d, g), static_cast<const uint16_t*>(q) + h0 * nd, static_cast<const uint16_t*>(k) + h0 * nd,
+        static_cast<const uint16_t*>(v) + h0 * nd, q_pool + h0 * nbd, k_pool + h0 * nbd,
+        kv_idx + (size_t)h0 * d.nB * kmax, kv_count + (size_t)h0 * d.nB, kmax, ws,
+        static_cast<unsigned char*>(out) + h0 * nd * out_elem, lse ? lse + (size_t)h0 * d.N : nullptr, s);
+    if (e != hipSuccess) return SVA_ERR_HIP;
+  }
+  return SVA_OK;
 }
 
 int sva_dense_attention(const sva_problem* prob, const void* q, const void* k, const void* v,

@@ -28,7 +28,8 @@ def test_every_declared_symbol_is_exported(lib):
                           "sva_token_select_workspace", "sva_fp8_padded_len", "sva_fp8_code_dim", "sva_quantize_fp8",
                           "sva_sparse_attention_fp8", "sva_dense_attention_fp8",
                           "sva_token_gather", "sva_token_scatter", "sva_status_string",
-                          "sva_remainder_workspace", "sva_block_moments", "sva_sparse_attention_remainder",
+                          "sva_remainder_workspace", "sva_remainder_workspace_heads", "sva_block_moments",
+                          "sva_sparse_attention_remainder",
                           "sva_version"}
     for n in names:
         assert hasattr(lib, n), n
@@ -153,9 +154,16 @@ def test_remainder_workspace_and_rejects_before_launch(lib):
         ws = ctypes.c_size_t(0)
         assert lib.sva_remainder_workspace(ctypes.byref(p), ctypes.byref(ws)) == _lib.SVA_OK
         assert ws.value == _remainder_bytes(wl.batch, wl.heads, wl.seq_len, wl.head_dim, wl.block)
+        # passes of fewer (batch, head) pairs: the same layout for that many
+        for g in (1, 2, wl.batch * wl.heads):
+            assert lib.sva_remainder_workspace_heads(ctypes.byref(p), g, ctypes.byref(ws)) == _lib.SVA_OK
+            assert ws.value == _remainder_bytes(1, g, wl.seq_len, wl.head_dim, wl.block), (wl.name, g)
+        for g in (0, -1, wl.batch * wl.heads + 1):
+            assert lib.sva_remainder_workspace_heads(ctypes.byref(p), g, ctypes.byref(ws)) == _lib.SVA_ERR_SHAPE
+        assert lib.sva_remainder_workspace_heads(ctypes.byref(p), 1, None) == _lib.SVA_ERR_INVALID_ARG
     p = sva.problem_for(workloads.TINY)
     need = ctypes.c_size_t(0)
-    lib.sva_remainder_workspace(ctypes.byref(p), ctypes.byref(need))
+    lib.sva_remainder_workspace_heads(ctypes.byref(p), 1, ctypes.byref(need))   # the least the call takes
     A = 1 << 20
     f = lib.sva_sparse_attention_remainder
     assert lib.sva_remainder_workspace(ctypes.byref(p), None) == _lib.SVA_ERR_INVALID_ARG

@@ -190,6 +190,37 @@ def test_workspace_is_reusable_and_sized_by_the_call():
     assert outs[1].shape[2] == wl2.seq_len
 
 
+@pytest.mark.parametrize("out_dtype", ["bf16", "f32"])
+def test_smaller_workspace_runs_head_groups(out_dtype):
+    """A workspace for fewer (batch, head) pairs than the problem has: the call
+    does the pairs in groups of as many as fit (here 2, 2, 2; 4, 2; 1 x 6) and
+    must give exactly the one-pass result, output and LSE, whichever output
+    type; below one pair's size the binding refuses."""
+    wl = SC("rem_groups", 2, 3, 128, (2, 6, 11), 64, "topk", keep_ratio=0.3, seed=311)
+    prob = sva.problem_for(wl)
+    if out_dtype == "f32":
+        prob.out_dtype = 1
+    bits = inputs.generate(wl)
+    dev = device_inputs(bits)
+    nb = sva.num_blocks(prob)
+    kept = _oracle_lists(wl, bits)
+    idx, cnt = _arrays(kept, nb)
+    qp, kp = sva.pool_blocks(prob, dev["q"], dev["k"])
+    full, full_lse = sva.sparse_attention_remainder(prob, dev["q"], dev["k"], dev["v"], qp, kp, idx, cnt,
+                                                    want_lse=True)
+    for heads in (2, 4, 1):
+        ws = torch.empty(sva.remainder_workspace(prob, heads), dtype=torch.uint8, device="cuda")
+        ws.fill_(0xFF)                                   # leftovers must not matter
+        o, lse = sva.sparse_attention_remainder(prob, dev["q"], dev["k"], dev["v"], qp, kp, idx, cnt,
+                                                want_lse=True, workspace=ws)
+        torch.cuda.synchronize()
+        say(f"[remainder groups] {out_dtype} {heads} pairs per pass")
+        assert torch.equal(o, full) and torch.equal(lse, full_lse), heads
+    small = torch.empty(sva.remainder_workspace(prob, 1) - 256, dtype=torch.uint8, device="cuda")
+    with pytest.raises(ValueError):
+        sva.sparse_attention_remainder(prob, dev["q"], dev["k"], dev["v"], qp, kp, idx, cnt, workspace=small)
+
+
 def test_custom_softmax_scale():
     """A softmax scale other than 1/sqrt(D) reaches every place the remainder
     uses it: the first-order weights, the pooled-key logits and the c M q
