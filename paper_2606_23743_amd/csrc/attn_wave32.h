@@ -1,9 +1,10 @@
-// Building blocks of the bf16 attention kernels with 32 queries per wave (one
-// query per lane pair): the direct global -> LDS chunk loads, the per-lane LDS
-// offsets of the operand reads, S^T = K Q^T and O^T += V^T P^T on
-// mfma_f32_32x32x16_bf16, the fixed-reference softmax and the output store.
-// The chunk loader also serves the 16x16 attention kernels (attn_w16.h); the
-// 32x32 arithmetic serves the remainder kernels (remainder.hip).
+// Building blocks of the bf16 attention kernels: the direct global -> LDS
+// chunk loads every kernel uses, the NaN mark of a block left to the
+// recompute pass, and the 32x32 form of the per-chunk arithmetic (one query
+// per lane pair: the per-lane LDS offsets of the operand reads, S^T = K Q^T
+// and O^T += V^T P^T on mfma_f32_32x32x16_bf16, the softmax step) that the
+// remainder's kernels (remainder.hip) use.  The attention kernels' own
+// arithmetic is the 16x16 form (attn_w16.h).
 #pragma once
 
 #include "attn_common.h"
@@ -161,22 +162,6 @@ __device__ __forceinline__ void qk_chunk(f32x16& sacc, const unsigned char* kt, 
   }
 }
 
-__device__ __forceinline__ void mask_tail(f32x16& sacc, int valid, int hf) {
-#pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int key = (r >> 2) * 8 + hf * 4 + (r & 3);
-    if (key >= valid) sacc[r] = -INFINITY;
-  }
-}
-
-// the reference maximum (log2 units) from a chunk that holds a valid key
-__device__ __forceinline__ float chunk_reference(const f32x16& sacc, float sl2) {
-  float mx = sacc[0];
-#pragma unroll
-  for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[r]);
-  return swap_halves_max(mx) * sl2;
-}
-
 // p = exp2(c*log2e*s - m) rounded to bf16; l sums the rounded weights
 __device__ __forceinline__ void softmax_chunk(const f32x16& sacc, bf16x8 (&pop)[2], float& l_part, float m_ref,
                                               float sl2) {
@@ -209,73 +194,11 @@ __device__ __forceinline__ void pv_chunk(const bf16x8 (&pop)[2], const unsigned 
       oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand<D>(vt, voff[dt], kk), pop[kk], oacc[dt], 0, 0, 0);
 }
 
-// After every kept block: if a row sum has grown past 2^64 (the reference
-// maximum was far below this row's logits), move the reference up by the
-// sum's binary exponent and scale that query's O and l by the same power of
-// two (exact).  p = exp2(s - m) can then only overflow if one block raises the
-// logits by more than ~2^63 over the running sum; that rare case is caught by
-// the final check.  Rows never come near 2^64 in practice, so this is one
-// compare and a branch per block.
-template <int D>
-__device__ __forceinline__ void rescale_if_large(float& l_part, float& m_ref, f32x16 (&oacc)[Geo<D>::DT]) {
-  if (__builtin_amdgcn_ballot_w64(l_part > 0x1p64f) != 0) {
-    asm volatile("");
-    const float l_tot = swap_halves_sum(l_part);
-    const int e = l_tot > 0x1p64f ? __builtin_amdgcn_frexp_expf(l_tot) : 0;
-    const float f = __builtin_amdgcn_ldexpf(1.0f, -e);
-    l_part *= f;
-#pragma unroll
-    for (int dt = 0; dt < Geo<D>::DT; ++dt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) oacc[dt][r] *= f;
-    m_ref += (float)e;
-  }
-}
-
-// a row that would need the per-iteration rescaling: sum past 2^100 or a
-// non-finite accumulator
-template <int D>
-__device__ __forceinline__ bool overflowed(float l_tot, const f32x16 (&oacc)[Geo<D>::DT]) {
-  bool bad = !(l_tot < 0x1p100f);
-#pragma unroll
-  for (int dt = 0; dt < Geo<D>::DT; ++dt)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) bad |= !__builtin_isfinite(oacc[dt][r]);
-  return bad;
-}
-
 // the NaN mark on a query block's first output element (recomputed later)
 template <bool OUT_F32>
 __device__ __forceinline__ void mark_block(void* out, size_t first) {
   if constexpr (OUT_F32) static_cast<float*>(out)[first] = __builtin_nanf("");
   else static_cast<uint16_t*>(out)[first] = 0x7FC0;
-}
-
-// O = O^T / l of query qr (row base obase) and its LSE; zeros and -inf when
-// the row attended to nothing
-template <int D, bool OUT_F32>
-__device__ __forceinline__ void store_query(void* out, float* lse, size_t obase, size_t lse_at,
-                                            const f32x16 (&oacc)[Geo<D>::DT], float l_tot, float m_ref, bool has,
-                                            int hf) {
-  const float inv = has ? 1.0f / l_tot : 0.0f;
-#pragma unroll
-  for (int dt = 0; dt < Geo<D>::DT; ++dt)
-#pragma unroll
-    for (int r4 = 0; r4 < 4; ++r4) {
-      const int d = dt * 32 + r4 * 8 + hf * 4;
-      if (d < D) {
-        const float o0 = oacc[dt][r4 * 4 + 0] * inv, o1 = oacc[dt][r4 * 4 + 1] * inv;
-        const float o2 = oacc[dt][r4 * 4 + 2] * inv, o3 = oacc[dt][r4 * 4 + 3] * inv;
-        if constexpr (OUT_F32) {
-          *reinterpret_cast<float4*>(static_cast<float*>(out) + obase + d) = make_float4(o0, o1, o2, o3);
-        } else {
-          const bf16x2 x = cvt2(o0, o1), y = cvt2(o2, o3);
-          const bf16x4 o = {x[0], x[1], y[0], y[1]};
-          *reinterpret_cast<bf16x4*>(static_cast<uint16_t*>(out) + obase + d) = o;
-        }
-      }
-    }
-  if (lse && hf == 0) lse[lse_at] = has ? (m_ref + __log2f(l_tot)) * 0.69314718055994530942f : -INFINITY;
 }
 
 }  // namespace attn
