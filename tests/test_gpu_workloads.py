@@ -171,9 +171,11 @@ def _run(wl, ratios, dense=False):
                 d = np.abs(got - ref[0, 0, a:e])
                 rworst, rsum, rn = max(rworst, float(d.max())), rsum + float(d.sum()), rn + d.size
             del f, ref, ref0, rlse
-        # per element the derived bound (bf16 weights, moments and T); over the
-        # sample the mean error is held to the plain attention bar as well
+        # per element the derived bound (bf16 weights, moments and T); at these
+        # sizes the first-order parts stay small, and the sample is held to the
+        # plain attention bars as well: max |err| <= 2e-2, mean <= 2e-3
         assert rsum / rn <= parity.MEAN_ABS, rsum / rn
+        assert rworst <= parity.MAX_ABS, rworst
         say(f"[workload {wl.name} r={r}] remainder ok on {len(rem_rows)} sampled query blocks: "
             f"max |err| {rworst:.2e}, mean {rsum / rn:.2e} (within the derived bounds)")
         del rem, rem_lse
