@@ -27,8 +27,9 @@ struct SelectArgs {
 
 // ---------------------------------------------------------------------------
 // Selection with the scores in registers.  A workgroup of NW waves takes
-// R = NW*RW = 16 query-block rows of one (b, h) (launched as eight waves of
-// two rows); each wave owns RW of them, and lane l holds
+// R = NW*RW = 16 query-block rows of one (b, h) (eight waves of two rows, or
+// sixteen of one; launch_select picks by block count and rule); each wave
+// owns RW of them, and lane l holds
 // the float64 scores of blocks j = t*64 + l (t < NT) for each of its rows.
 // kbar is staged through LDS 64 blocks at a time (the next chunk is loaded
 // into registers while this one is used), so every kbar row is read once per
@@ -88,8 +89,11 @@ __device__ __forceinline__ void kth_key(const uint64_t (&key)[NT], uint32_t k, u
   quota = k - above;
 }
 
-template <int NT, int RW, int NW, bool MASS>
-__global__ __launch_bounds__(NW * 64) void select_reg_kernel(SelectArgs a) {
+// OCC: waves per SIMD the register allocation must allow (4: two workgroups
+// of eight waves per CU, which overlaps one workgroup's scores with the
+// other's searches)
+template <int NT, int RW, int NW, bool MASS, int OCC>
+__global__ __launch_bounds__(NW * 64, OCC) void select_reg_kernel(SelectArgs a) {
   constexpr int NTH = NW * 64;       // threads
   constexpr int R = NW * RW;         // rows of the workgroup (16)
   static_assert(R == 16, "the score tiles hold 16 rows");
@@ -338,14 +342,11 @@ __global__ __launch_bounds__(NW * 64) void select_reg_kernel(SelectArgs a) {
   if constexpr (RW > 3) select_row(std::integral_constant<int, 3>{});
 }
 
-template <int NT, int RW, int NW>
+template <int NT, int RW, int NW, bool MASS, int OCC = 1>
 hipError_t launch_reg(SelectArgs a, int B, int H, hipStream_t stream) {
   a.n_groups = (a.nB + NW * RW - 1) / (NW * RW);
   a.n_work = B * H * a.n_groups;
-  if (a.mode == 0)
-    hipLaunchKernelGGL((select_reg_kernel<NT, RW, NW, false>), dim3(a.n_work), dim3(NW * 64), 0, stream, a);
-  else
-    hipLaunchKernelGGL((select_reg_kernel<NT, RW, NW, true>), dim3(a.n_work), dim3(NW * 64), 0, stream, a);
+  hipLaunchKernelGGL((select_reg_kernel<NT, RW, NW, MASS, OCC>), dim3(a.n_work), dim3(NW * 64), 0, stream, a);
   return hipGetLastError();
 }
 
@@ -371,19 +372,37 @@ hipError_t launch_select(const Dims& d, const SelectRule& r, const float* q_pool
   a.tau = r.tau;
   // nB <= SVA_SELECT_MAX_BLOCKS (2048) and D <= 128 are checked by the caller
   const int nt = (d.nB + 63) / 64;
-  // eight waves of two rows: measured 7-37% faster than four of four rows
-  // at every block count (more waves for the latency-bound threshold search)
-  if (nt <= 1) return launch_reg<1, 2, 8>(a, d.B, d.H, stream);
-  if (nt <= 2) return launch_reg<2, 2, 8>(a, d.B, d.H, stream);
-  if (nt <= 4) return launch_reg<4, 2, 8>(a, d.B, d.H, stream);
-  if (nt <= 8) return launch_reg<8, 2, 8>(a, d.B, d.H, stream);
-  // the mass rule's search (a wave sum per candidate bit) gains from one row
-  // per wave: 0.597 -> 0.533 ms at the 22B-class layer; the top-k search
-  // loses (0.339 -> 0.395 ms at the 64B-class layer)
-  if (nt <= 16 && a.mode != 0) return launch_reg<16, 1, 16>(a, d.B, d.H, stream);
-  if (nt <= 16) return launch_reg<16, 2, 8>(a, d.B, d.H, stream);
-  if (nt <= 24) return launch_reg<24, 2, 8>(a, d.B, d.H, stream);
-  if (nt <= 32) return launch_reg<32, 2, 8>(a, d.B, d.H, stream);
+  // Shapes by block count (chunks of 64 blocks, nt) and rule, each measured
+  // against its neighbours:
+  // - eight waves of two rows: 7-37% faster than four of four rows at every
+  //   block count (more waves for the latency-bound threshold search);
+  // - a chunk count fitted to nt: 0.339 -> 0.326 ms at the 64B-class layer
+  //   (14 chunks instead of 16);
+  // - the mass rule's search (a wave sum per candidate bit) gains from one
+  //   row per wave: 0.597 -> 0.533 ms at the 22B-class layer; the top-k
+  //   search loses (0.339 -> 0.395 ms at the 64B-class layer);
+  // - at 17-20 chunks, top-k holds two workgroups per CU only with the
+  //   registers capped at 128 (a few values spill): 0.83 -> 0.555 ms on the
+  //   CFG-sweep layer (19 chunks), against 0.646 ms for sixteen waves of one
+  //   row and one workgroup per CU.
+  const bool mass = a.mode != 0;
+  if (nt <= 1) return mass ? launch_reg<1, 2, 8, true>(a, d.B, d.H, stream) : launch_reg<1, 2, 8, false>(a, d.B, d.H, stream);
+  if (nt <= 2) return mass ? launch_reg<2, 2, 8, true>(a, d.B, d.H, stream) : launch_reg<2, 2, 8, false>(a, d.B, d.H, stream);
+  if (nt <= 4) return mass ? launch_reg<4, 2, 8, true>(a, d.B, d.H, stream) : launch_reg<4, 2, 8, false>(a, d.B, d.H, stream);
+  if (nt <= 8) return mass ? launch_reg<8, 2, 8, true>(a, d.B, d.H, stream) : launch_reg<8, 2, 8, false>(a, d.B, d.H, stream);
+  if (mass) {
+    if (nt <= 16) return launch_reg<16, 1, 16, true>(a, d.B, d.H, stream);
+    if (nt <= 20) return launch_reg<20, 1, 16, true>(a, d.B, d.H, stream);
+    if (nt <= 24) return launch_reg<24, 2, 8, true>(a, d.B, d.H, stream);
+    if (nt <= 32) return launch_reg<32, 2, 8, true>(a, d.B, d.H, stream);
+  } else {
+    if (nt <= 12) return launch_reg<12, 2, 8, false>(a, d.B, d.H, stream);
+    if (nt <= 14) return launch_reg<14, 2, 8, false>(a, d.B, d.H, stream);
+    if (nt <= 16) return launch_reg<16, 2, 8, false>(a, d.B, d.H, stream);
+    if (nt <= 20) return launch_reg<20, 2, 8, false, 4>(a, d.B, d.H, stream);
+    if (nt <= 24) return launch_reg<24, 1, 16, false>(a, d.B, d.H, stream);
+    if (nt <= 32) return launch_reg<32, 2, 8, false>(a, d.B, d.H, stream);
+  }
   return hipErrorInvalidValue;
 }
 

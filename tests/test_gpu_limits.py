@@ -1,5 +1,6 @@
 """GPU parity at the size limits of the boundary: 2048 key blocks per row (the
-most the selection kernel holds in registers) in both selection modes, with
+most the selection kernel holds in registers) in both selection modes (and
+every kernel shape the selection launch picks on the way there), with
 attention on sampled query blocks in bf16 and fp8, fp8 dense attention at
 2047 blocks (the longest kept-block list the fp8 kernel holds in LDS), and
 4096 blocks for the block-pair kernel and the first-order remainder."""
@@ -35,18 +36,45 @@ SELECT_CASES = [
 ]
 
 
+# one case per kernel shape the selection launch picks between 9 and 20
+# chunks of 64 blocks (12, 14, 16 and 20 registers of scores per lane; eight
+# waves of two rows or sixteen of one; the 20-chunk top-k shape with its
+# registers capped), in both rules
+SHAPE_CASES = [
+    SC("nb700_topk", 1, 2, 64, (5, 80, 112), 64, "topk", keep_ratio=0.2, seed=215),
+    SC("nb870_topk", 1, 2, 128, (5, 96, 116), 64, "topk", keep_ratio=0.15, seed=216),
+    SC("nb1100_topk", 1, 2, 64, (5, 80, 176), 64, "topk", keep_ratio=0.25, seed=217),
+    SC("nb1280_topk", 1, 1, 128, (5, 64, 256), 64, "topk", keep_ratio=0.1, seed=218),
+    SC("nb1100_mass", 1, 2, 64, (5, 80, 176), 64, "mass", mass_threshold=0.9, max_keep_ratio=0.3,
+       force_first_frame=True, seed=219),
+    SC("nb1280_mass", 1, 1, 128, (5, 64, 256), 64, "mass", mass_threshold=0.8, max_keep_ratio=0.2,
+       force_first_frame=False, seed=220),
+]
+
+
 @pytest.mark.parametrize("wl", SELECT_CASES, ids=[c.name for c in SELECT_CASES])
 def test_selection_head_dim_112_past_1024_blocks(wl):
     """Selection with D = 112 (score steps of 28 channels per lane group) at
     1536 blocks per row, where a lane holds 24 registers of scores: every
     row's kept list against the oracle's."""
+    _selection_every_row(wl, 1536)
+
+
+@pytest.mark.parametrize("wl", SHAPE_CASES, ids=[c.name for c in SHAPE_CASES])
+def test_selection_kernel_shapes(wl):
+    """Every row's kept list against the oracle's at block counts that select
+    each of the selection kernel's shapes from 9 to 20 chunks."""
+    _selection_every_row(wl, wl.seq_len // wl.block)
+
+
+def _selection_every_row(wl, nb_expected):
     say(f"[limits {wl.name}] N={wl.seq_len} nB={wl.seq_len // wl.block}")
     bits = inputs.generate(wl)
     dev = device_inputs(bits)
     prob = sva.problem_for(wl)
     sel = sva.select_for(wl)
     nb = sva.num_blocks(prob)
-    assert nb == 1536
+    assert nb == nb_expected
     qp, kp = sva.pool_blocks(prob, dev["q"], dev["k"])
     idx, cnt, _ = sva.select_blocks(prob, sel, qp, kp)
     torch.cuda.synchronize()
