@@ -24,7 +24,7 @@
 //                       then an online softmax over the nB pooled keys kbar_j
 //                       with weight n_j (kept and padding blocks masked),
 //                       values vbar_j
-#include "attn_wave32.h"
+#include "attn_w16.h"
 
 namespace sva {
 namespace {
@@ -32,7 +32,6 @@ namespace {
 using namespace attn;
 
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kLn2 = 0.69314718055994530942f;
 
 __device__ __forceinline__ uint16_t bf16_bits(float x) { return __builtin_bit_cast(uint16_t, (__bf16)x); }
 
@@ -467,37 +466,55 @@ void rem_gemm_kernel(RemGemmArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Remainder attention and merge.  One workgroup of four waves (32 queries
-// each) per 128 queries: one query block at S = 128, two at S = 64 (the
-// pooled keys are the same for every query block of a head; only the masks
-// differ).  The pooled keys kbar_j of the head are walked in 32-row chunks
-// (four LDS stages): S^T = Kbar Q^T, logit + log2 n_j in log2 units (-inf for
-// kept and padding blocks), P rounded to bf16 with l summed from it,
-// O^T += Vbar^T P^T.  The reference starts at max(LSE of the kept part, r_i)
-// (log2 units) and moves up only when a chunk's maximum passes it by more
-// than 8, so it is rarely moved.  The first-order term exp(r_i) c T_i q (the
-// rows of T_i staged as the first chunks of the pipeline, S step against
-// Q^T) and the kept-block result (O and LSE in float32, weight exp(LSE)) are
-// the starting numerator and row sum, so the end is one division.
+// Remainder attention and merge, on mfma_f32_16x16x32_bf16 with the per-chunk
+// arithmetic of the kept-block kernels (attn_w16.h).  One workgroup of four
+// waves (32 queries each, two 16-query tiles) per 128 queries: one query block
+// at S = 128, two at S = 64 (the pooled keys are the same for every query
+// block of a head; only the masks differ).  The pooled keys kbar_j of the head
+// are walked in 32-row chunks (four LDS stages, loads three chunks ahead):
+//   x   = c*log2e * (q.kbar_j) + log2 n_j - m        (log2 units)
+//   p   = exp2(x), rounded to bf16, then ANDed with the chunk's 16-bit masks
+//         (zero for kept and padding blocks), l summed from the masked p
+//   O^T += Vbar^T P^T
+// The masks are tabulated once per workgroup in LDS, four 32-bit words per
+// lane group and chunk (two keys each), so a chunk costs one LDS read of them
+// and one AND per two keys.  A kept block's x is at most about 0 (the pooled
+// logit plus log2 n_j is at most the block's log-sum-exp, which the reference
+// m >= LSE of the kept part bounds), so only dropped blocks can move the
+// reference: m starts at max(LSE of the kept part, r_i) and moves up only
+// when a chunk's x passes 8, which is rare.  The last chunk (the last block's
+// n_j, padding blocks) takes the general form.  The first-order term
+// exp(r_i) c T_i q (the rows of T_i staged as the first chunks of the
+// pipeline: the S step with T's rows as keys puts (T_i q)[e] where O^T keeps
+// d = e) and the kept-block result (O and LSE in float32, weight exp(LSE))
+// are the starting numerator and row sum, so the end is one division.
 // ---------------------------------------------------------------------------
 template <int D, int S, bool OUT_F32>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void rem_attn_kernel(RemAttnArgs a) {
   using G = Geo<D>;
+  using G16 = Geo16<D>;
   constexpr int NW = 4;                      // waves: 128 queries
   constexpr int NQB = 128 / S;               // query blocks per workgroup
   constexpr int CT = 32 * G::RB;
   constexpr int NUW = CT / 1024 / NW;
-  constexpr int kWords = kRemMaxBlocks / 32;
+  constexpr int NTT = G::DT;                 // 32-row tiles of T_i
+  constexpr int NTC = NQB * NTT;             // T chunks ahead of the pooled chunks
+  constexpr int kChunks = kRemMaxBlocks / 32;
+  constexpr int NST = 4, PD = 3;
   static_assert(NUW >= 1, "tile split");
-  __shared__ __attribute__((aligned(1024))) unsigned char Ks[4][CT];
-  __shared__ __attribute__((aligned(1024))) unsigned char Vs[4][CT];
-  __shared__ uint32_t bms[NQB][kWords];
+  __shared__ __attribute__((aligned(1024))) unsigned char Ks[NST][CT];
+  __shared__ __attribute__((aligned(1024))) unsigned char Vs[NST][CT];
+  // pm[b][ch][4g + 2k2 + e]: the masks of keys 16k2 + 4g + 2e (low half) and
+  // + 1 (high half) of chunk ch for query block b: 0xffff where the key's
+  // block is dropped (it takes part), 0 where kept or padding
+  __shared__ __attribute__((aligned(16))) uint32_t pm[NQB][kChunks][16];
 
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int hf = lane >> 5, l32 = lane & 31;
+  const int g = lane >> 4;
   const int N = a.N, nB = a.nB, nBp = a.nBp;
+  const int nch = nBp / 32;
   const int groups = (nB + NQB - 1) / NQB;
   const int item = __builtin_amdgcn_readfirstlane(xcd_remap(blockIdx.x, a.n_rows));
   const int bh = item / groups;
@@ -505,12 +522,12 @@ void rem_attn_kernel(RemAttnArgs a) {
   const int qb = w * 32 / S;                 // this wave's query block within the workgroup
   const int i_raw = ib0 + qb;                // may be nB (no such block: the wave only helps load)
   const int i = min(i_raw, nB - 1);
-  const uint32_t* bm = bms[qb];
 
-  // padding blocks j in [nB, nBp) are masked like kept ones
-  for (int t = threadIdx.x; t < NQB * kWords; t += 256) {
-    const int j0 = (t % kWords) * 32;
-    (&bms[0][0])[t] = j0 + 32 <= nB ? 0u : (j0 >= nB ? ~0u : ~0u << (nB - j0));
+  for (int t = threadIdx.x; t < NQB * nch * 16; t += 256) {
+    const int b2 = t / (nch * 16), rest = t - b2 * (nch * 16);
+    const int ch = rest >> 4, slot = rest & 15;
+    const int j0 = ch * 32 + ((slot >> 1) & 1) * 16 + (slot >> 2) * 4 + (slot & 1) * 2;
+    pm[b2][ch][slot] = (j0 < nB ? 0x0000ffffu : 0u) | (j0 + 1 < nB ? 0xffff0000u : 0u);
   }
   __syncthreads();
 #pragma unroll
@@ -521,147 +538,150 @@ void rem_attn_kernel(RemAttnArgs a) {
     const int32_t* idx = a.kv_idx + (size_t)row * a.kmax;
     for (int t = threadIdx.x; t < cnt; t += 256) {
       const int j = idx[t];
-      if (j >= 0 && j < nB) atomicOr(&bms[b2][j >> 5], 1u << (j & 31));
+      if (j >= 0 && j < nB) {
+        const int jj = j & 31;
+        const int slot = ((jj >> 2) & 3) * 4 + (jj >> 4) * 2 + ((jj >> 1) & 1);
+        atomicAnd(&pm[b2][j >> 5][slot], (jj & 1) ? 0x0000ffffu : 0xffff0000u);
+      }
     }
   }
   __syncthreads();
 
-  const int qr = i_raw * S + (w * 32) % S + l32;
-  const bool present = i_raw < nB && qr < N;
-  bf16x8 qop[G::DQ];
-  load_q<D>(qop, a.q + (size_t)bh * N * D, qr, present, hf);
+  const int qbase = i_raw * S + (w * 32) % S;
+  bf16x8 qop[2][G16::KS];
+  load_q16<D>(qop, a.q + (size_t)bh * N * D, qbase, N, lane);
 
-  ChunkLoader<D, NUW, CT> ld;
+  ChunkLoader<D, NUW, CT, true> ld;
   loader_init(ld, a.kbar + (size_t)bh * nBp * D, a.vbar + (size_t)bh * nBp * D, nBp, &Ks[0][0], &Vs[0][0], w,
               lane);
-  int koff[G::DQ], voff[G::DT];
-  operand_offsets<D>(lane, koff, voff);
+  int koff[G16::KS], voff[G16::DT];
+  operand_offsets16<D>(lane, koff, voff);
 
   const float sl2 = a.scale_log2;
   const float r2 = a.r[(size_t)bh * nBp + i] * kLog2e;   // block-score maximum, log2 units
-  const float lse_a = present ? a.lse_a[(size_t)bh * N + qr] : -INFINITY;
-  float m_ref = fmaxf(lse_a * kLog2e, r2);
-  float l_part = 0.0f;
-  f32x16 oacc[G::DT];
+  float m_ref[2], l_part[2], f1[2], l_a[2];
+  f32x4 oacc[G16::DT][2];
 #pragma unroll
-  for (int dt = 0; dt < G::DT; ++dt) oacc[dt] = f32x16{};
+  for (int qt = 0; qt < 2; ++qt) {
+    const int q = qbase + qt * 16 + (lane & 15);
+    const float lse_a = q < N ? a.lse_a[(size_t)bh * N + q] : -INFINITY;
+    m_ref[qt] = fmaxf(lse_a * kLog2e, r2);
+    l_a[qt] = __builtin_amdgcn_exp2f(lse_a * kLog2e - m_ref[qt]);   // 0 without a kept part
+    f1[qt] = a.scale * __builtin_amdgcn_exp2f(r2 - m_ref[qt]);
+    l_part[qt] = g == 0 ? l_a[qt] : 0.0f;
+    const size_t ob = ((size_t)bh * N + (q < N ? q : 0)) * D;
+#pragma unroll
+    for (int dt = 0; dt < G16::DT; ++dt) {
+      const float4 o = q < N ? *reinterpret_cast<const float4*>(a.o_a + ob + dt * 16 + 4 * g)
+                             : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      oacc[dt][qt] = f32x4{l_a[qt] * o.x, l_a[qt] * o.y, l_a[qt] * o.z, l_a[qt] * o.w};
+    }
+  }
   const float log2_s = S == 128 ? 7.0f : 6.0f;
   const float log2_last = __log2f((float)(N - (nB - 1) * S));
 
-  // Pipeline over one sequence of 32-row chunks: first the G::DT row tiles of
-  // T_i of each query block of the workgroup (the S step with T's rows as
-  // keys gives T_i q in the numerator's layout; a wave computes only on its
-  // own block's tiles), then the nch pooled-key chunks.  Four LDS stages
-  // (chunk g in stage g % 4), loads three chunks ahead by direct loads, and
-  // in the pooled part the S products of the next chunk issued alongside
-  // this chunk's softmax, as in the 32-query kernel.  Each chunk issues one
-  // load group (a T tile with a dummy V tile; chunk 0 again past the end), so
-  // the wait counts are constants.
-  constexpr int NST = 4, PD = 3;
-  constexpr int NTC = NQB * G::DT;           // T tiles ahead of the pooled chunks
-  const int nch = nBp / 32;
-  ChunkLoader<D, NUW, CT> tl[NQB];           // T_i of each block: D rows of D, like a K tile
+  // T tiles (with a dummy V tile), then the pooled chunks; chunk 0 again past
+  // the end, so each chunk issues one load group and the wait counts are
+  // constants.
+  ChunkLoader<D, NUW, CT, true> tl[NQB];     // T_i of each block: D rows of D, like a K tile
 #pragma unroll
   for (int b2 = 0; b2 < NQB; ++b2) {
     const uint16_t* Tb = a.T + ((size_t)bh * nBp + min(ib0 + b2, nB - 1)) * D * D;
     loader_init(tl[b2], Tb, Tb, D, &Ks[0][0], &Vs[0][0], w, lane);
   }
-  auto fetch_pooled = [&](int st, int g) {
-    const int ch = g - NTC;
+  auto fetch_pooled = [&](int st, int gc) {
+    const int ch = gc - NTC;
     load_chunk(ld, st, ch < nch ? ch * 32 : 0);
   };
-  // chunk g with g a compile-time constant (the T part, fully unrolled)
-  auto fetch_const = [&](int st, int g) {
-    if (g < NTC) {
-      load_tile<true>(tl[g / G::DT], st, (g % G::DT) * 32);
+  auto fetch_const = [&](int st, int gc) {
+    if (gc < NTC) {
+      load_tile<true>(tl[gc / NTT], st, (gc % NTT) * 32);
       load_tile<false>(ld, st, 0);
     } else {
-      fetch_pooled(st, g);
+      fetch_pooled(st, gc);
     }
   };
-  // x = logit in log2 units + log2 n_j - m_ref (-inf for kept and padding
-  // blocks), so the exponential takes x as it is.  The chunk's mask word is
-  // the same for the whole wave (one query block per wave): the condition of
-  // register r -- bit jj of the word for lanes 0..31, bit jj + 4 for lanes
-  // 32..63 -- is a scalar lane mask, and each logit costs a select, an FMA
-  // and a max.  Every block but the last has n_j = S; the last block's chunk
-  // takes the general form.
-  const int last_ch = (nB - 1) / 32;
-  auto masked = [&](f32x16& x, int ch) {
-    const uint32_t word = __builtin_amdgcn_readfirstlane(bm[ch]);
-    float mx = -INFINITY;
-    if (ch != last_ch) {
-      const float bias = log2_s - m_ref;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int jj = (r >> 2) * 8 + (r & 3);           // key within the chunk, less hf*4
-        const uint64_t lanes = (((word >> jj) & 1u) ? 0x00000000FFFFFFFFull : 0ull) |
-                               (((word >> (jj + 4)) & 1u) ? 0xFFFFFFFF00000000ull : 0ull);
-        const float y = __builtin_fmaf(x[r], sl2, bias);
-        x[r] = __builtin_amdgcn_inverse_ballot_w64(lanes) ? -INFINITY : y;
-        mx = fmaxf(mx, x[r]);
+  for (int gc = 0; gc < PD; ++gc) fetch_const(gc, gc);
+#pragma unroll
+  for (int gc = 0; gc < NTC; ++gc) {         // chunk gc: T rows 32*(gc % NTT) .. of block gc / NTT
+    wait_vmcnt_lds_idle<2 * NUW * (PD - 1)>();       // chunk gc landed
+    wg_barrier();                                   // every wave's; the stage of chunk gc-1 is free
+    fetch_const((gc + PD) % NST, gc + PD);
+    if (gc / NTT == qb) {
+      f32x4 tacc[2][2];
+      qk16<D>(tacc, &Ks[gc % NST][0], koff, qop);
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2) {
+        const int dt = 2 * (gc % NTT) + k2;          // rows 16*dt + 4g + r of T_i: d = e
+        if (dt < G16::DT) {
+#pragma unroll
+          for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) oacc[dt][qt][r] = __builtin_fmaf(f1[qt], tacc[k2][qt][r], oacc[dt][qt][r]);
+        }
       }
-    } else {
-      const uint32_t mine = word >> (hf * 4);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int jj = (r >> 2) * 8 + (r & 3);
-        const int j = ch * 32 + hf * 4 + jj;
-        const float b = ((mine >> jj) & 1u) ? -INFINITY : (j == nB - 1 ? log2_last : log2_s) - m_ref;
-        x[r] = __builtin_fmaf(x[r], sl2, b);
-        mx = fmaxf(mx, x[r]);
-      }
-    }
-    return swap_halves_max(mx);
-  };
-  // The kept part and the first-order term enter as the starting numerator
-  // and row sum at the starting reference; the rescaling below moves them
-  // with the pooled keys' sums.  Numerator: exp2(LSE - m) O_kept (its loads
-  // issued first) + c exp2(r - m) T_i q (the T tiles); row sum:
-  // exp2(LSE - m), on one half of the lane pair.
-  const float l_a = __builtin_amdgcn_exp2f(lse_a * kLog2e - m_ref);   // 0 without a kept part
-  const float f1 = a.scale * __builtin_amdgcn_exp2f(r2 - m_ref);
-  float4 oa[G::DT][4];
-  {
-    const size_t obase = ((size_t)bh * N + (present ? qr : 0)) * D;
-#pragma unroll
-    for (int dt = 0; dt < G::DT; ++dt)
-#pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        const int d = dt * 32 + r4 * 8 + hf * 4;
-        oa[dt][r4] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-        if (present && d < D) oa[dt][r4] = *reinterpret_cast<const float4*>(a.o_a + obase + d);
-      }
-  }
-#pragma unroll
-  for (int g = 0; g < PD; ++g) fetch_const(g, g);
-#pragma unroll
-  for (int dt = 0; dt < G::DT; ++dt)
-#pragma unroll
-    for (int r4 = 0; r4 < 4; ++r4) {
-      oacc[dt][r4 * 4 + 0] = l_a * oa[dt][r4].x;
-      oacc[dt][r4 * 4 + 1] = l_a * oa[dt][r4].y;
-      oacc[dt][r4 * 4 + 2] = l_a * oa[dt][r4].z;
-      oacc[dt][r4 * 4 + 3] = l_a * oa[dt][r4].w;
-    }
-  l_part = hf == 0 ? l_a : 0.0f;
-#pragma unroll
-  for (int g = 0; g < NTC; ++g) {            // chunk g: T tile g % DT of block g / DT
-    wait_vmcnt_lds_idle<2 * NUW * (PD - 1)>();       // chunk g landed
-    wg_barrier();                                   // every wave's; the stage of chunk g-1 is free
-    fetch_const((g + PD) % NST, g + PD);
-    if (g / G::DT == qb) {
-      f32x16 tacc;
-      qk_chunk<D>(tacc, &Ks[g % NST][0], koff, qop);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) oacc[g % G::DT][r] = __builtin_fmaf(f1, tacc[r], oacc[g % G::DT][r]);
     }
   }
 
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  const int last_ch = (nB - 1) / 32;
+  // x in place of s (log2 units, relative to m_ref); returns this lane's max
+  auto logits = [&](f32x4 (&x)[2][2], int ch) {
+    float mx = -INFINITY;
+    if (ch != last_ch) {
+#pragma unroll
+      for (int qt = 0; qt < 2; ++qt) {
+        const float bias = log2_s - m_ref[qt];
+#pragma unroll
+        for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            x[k2][qt][r] = __builtin_fmaf(x[k2][qt][r], sl2, bias);
+            mx = fmaxf(mx, x[k2][qt][r]);
+          }
+      }
+    } else {
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int j = ch * 32 + k2 * 16 + 4 * g + r;
+          const float lj = j >= nB ? -INFINITY : (j == nB - 1 ? log2_last : log2_s);
+#pragma unroll
+          for (int qt = 0; qt < 2; ++qt) {
+            x[k2][qt][r] = __builtin_fmaf(x[k2][qt][r], sl2, lj - m_ref[qt]);
+            mx = fmaxf(mx, x[k2][qt][r]);
+          }
+        }
+    }
+    return mx;
+  };
+  auto softmax_masked = [&](const f32x4 (&x)[2][2], const u32x4& mk, bf16x8 (&pop)[2]) {
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+      u32x4 wv;
+      float lsum = l_part[qt];
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const float p0 = __builtin_amdgcn_exp2f(x[k2][qt][2 * e]);
+          const float p1 = __builtin_amdgcn_exp2f(x[k2][qt][2 * e + 1]);
+          const unsigned u = __builtin_bit_cast(unsigned, cvt2(p0, p1)) & mk[k2 * 2 + e];
+          lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, u), ones, lsum, false);
+          wv[k2 * 2 + e] = u;
+        }
+      pop[qt] = __builtin_bit_cast(bf16x8, wv);
+      l_part[qt] = lsum;
+    }
+  };
+
   wait_vmcnt_lds_idle<2 * NUW * (PD - 1)>();         // pooled chunk 0 landed
   wg_barrier();
-  f32x16 sacc;
-  qk_chunk<D>(sacc, &Ks[NTC % NST][0], koff, qop);
+  f32x4 sacc[2][2];
+  qk16<D>(sacc, &Ks[NTC % NST][0], koff, qop);
+  const uint32_t* pmw = &pm[qb][0][4 * g];
   for (int ch0 = 0; ch0 < nch; ch0 += NST) {
 #pragma unroll
     for (int c = 0; c < NST; ++c) {
@@ -670,52 +690,53 @@ void rem_attn_kernel(RemAttnArgs a) {
       wait_vmcnt_lds_idle<2 * NUW * (PD - 2)>();     // chunk ch+1 landed
       wg_barrier();
       fetch_pooled((NTC + c + PD) % NST, NTC + ch + PD);
-      f32x16 snext;
-      qk_chunk<D>(snext, &Ks[(NTC + c + 1) % NST][0], koff, qop);
-      const float mx = masked(sacc, ch);             // relative to m_ref
-      if (__builtin_amdgcn_ballot_w64(mx > 8.0f) != 0) {
-        if (mx > 8.0f) {
-          const float f = __builtin_amdgcn_exp2f(-mx);
-          l_part *= f;
+      f32x4 snext[2][2];
+      qk16<D>(snext, &Ks[(NTC + c + 1) % NST][0], koff, qop);
+      const u32x4 mk = *reinterpret_cast<const u32x4*>(pmw + ch * 16);
+      const float mxl = logits(sacc, ch);
+      if (__builtin_amdgcn_ballot_w64(mxl > 8.0f) != 0) {
+        // a dropped block's logit passed the reference by more than 8: move it
 #pragma unroll
-          for (int dt = 0; dt < G::DT; ++dt)
+        for (int qt = 0; qt < 2; ++qt) {
+          float mx = -INFINITY;
 #pragma unroll
-            for (int r = 0; r < 16; ++r) oacc[dt][r] *= f;
+          for (int k2 = 0; k2 < 2; ++k2)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) sacc[r] -= mx;
-          m_ref += mx;
+            for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sacc[k2][qt][r]);
+          mx = quad_max(mx);
+          if (mx > 8.0f) {
+            const float f = __builtin_amdgcn_exp2f(-mx);
+            l_part[qt] *= f;
+#pragma unroll
+            for (int dt = 0; dt < G16::DT; ++dt)
+#pragma unroll
+              for (int r = 0; r < 4; ++r) oacc[dt][qt][r] *= f;
+#pragma unroll
+            for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+              for (int r = 0; r < 4; ++r) sacc[k2][qt][r] -= mx;
+            m_ref[qt] += mx;
+          }
         }
       }
       bf16x8 pop[2];
-      softmax_chunk(sacc, pop, l_part, 0.0f, 1.0f);
-      pv_chunk<D>(pop, &Vs[(NTC + c) % NST][0], voff, oacc);
-      sacc = snext;
+      softmax_masked(sacc, mk, pop);
+      pv16<D>(pop, &Vs[(NTC + c) % NST][0], voff, oacc);
+#pragma unroll
+      for (int x = 0; x < 2; ++x) {
+        sacc[x][0] = snext[x][0];
+        sacc[x][1] = snext[x][1];
+      }
     }
   }
   wait_vmcnt<0>();
 
-  const float l_tot = swap_halves_sum(l_part);
-  const float inv = 1.0f / l_tot;
-  if (!present) return;
-  const size_t obase = ((size_t)bh * N + qr) * D;
-#pragma unroll
-  for (int dt = 0; dt < G::DT; ++dt)
-#pragma unroll
-    for (int r4 = 0; r4 < 4; ++r4) {
-      const int d = dt * 32 + r4 * 8 + hf * 4;
-      if (d < D) {
-        const float o0 = oacc[dt][r4 * 4 + 0] * inv, o1 = oacc[dt][r4 * 4 + 1] * inv;
-        const float o2 = oacc[dt][r4 * 4 + 2] * inv, o3 = oacc[dt][r4 * 4 + 3] * inv;
-        if constexpr (OUT_F32) {
-          *reinterpret_cast<float4*>(static_cast<float*>(a.out) + obase + d) = make_float4(o0, o1, o2, o3);
-        } else {
-          const bf16x2 x = cvt2(o0, o1), y = cvt2(o2, o3);
-          const bf16x4 o = {x[0], x[1], y[0], y[1]};
-          *reinterpret_cast<bf16x4*>(static_cast<uint16_t*>(a.out) + obase + d) = o;
-        }
-      }
-    }
-  if (a.lse && hf == 0) a.lse[(size_t)bh * N + qr] = (m_ref + __log2f(l_tot)) * kLn2;
+  float l_tot[2];
+  l_tot[0] = quad_sum(l_part[0]);
+  l_tot[1] = quad_sum(l_part[1]);
+  const bool has[2] = {l_tot[0] > 0.0f, l_tot[1] > 0.0f};
+  store_query16<D, OUT_F32>(a.out, a.lse, (size_t)bh * N * D, (size_t)bh * N, qbase, N, oacc, l_tot, m_ref, has,
+                            lane);
 }
 
 template <int D, int S>
