@@ -1,10 +1,9 @@
 // Building blocks of the bf16 attention kernels: the direct global -> LDS
 // chunk loads every kernel uses, the NaN mark of a block left to the
-// recompute pass, and the 32x32 form of the per-chunk arithmetic (one query
-// per lane pair: the per-lane LDS offsets of the operand reads, S^T = K Q^T
-// and O^T += V^T P^T on mfma_f32_32x32x16_bf16, the softmax step) that the
-// remainder's kernels (remainder.hip) use.  The attention kernels' own
-// arithmetic is the 16x16 form (attn_w16.h).
+// recompute pass, and the operand reads of the 32x32x16 form (per-lane LDS
+// offsets of the K operand and of the V transpose reads) that the
+// remainder's moment, weight and GEMM kernels (remainder.hip) use.  The
+// attention kernels' own arithmetic is the 16x16 form (attn_w16.h).
 #pragma once
 
 #include "attn_common.h"
@@ -123,8 +122,8 @@ __device__ __forceinline__ void operand_offsets(int lane, int (&koff)[Geo<D>::DQ
 
 // Transpose read of a V-swizzled [32 rows][RB] tile: lane l gets column
 // dt*32 + l%32 (through voff = tr_offset(lane, dt)) at the 8 rows of key half
-// kk in the order of a softmax_chunk register group (rows kk*16 + hf*4 + 0..3,
-// then kk*16 + 8 + hf*4 + 0..3).  The same register serves as the A operand
+// kk in the order rows kk*16 + hf*4 + 0..3, then kk*16 + 8 + hf*4 + 0..3 (the
+// key order of a 32x32x16 S^T register group).  The same register serves as the A operand
 // (row m = the column) or the B operand (column n = the column) of an MFMA
 // whose contraction runs over the tile's rows.
 template <int D>
@@ -138,60 +137,6 @@ __device__ __forceinline__ bf16x8 tr_operand(const unsigned char* tile, int voff
   const u32x2 hw = __builtin_bit_cast(u32x2, hi);
   const u32x4 vw = {lw[0], lw[1], hw[0], hw[1]};
   return __builtin_bit_cast(bf16x8, vw);
-}
-
-// Q^T operand of query qr: d = s*16 + hf*8 + 0..7 (zero when the query is absent)
-template <int D>
-__device__ __forceinline__ void load_q(bf16x8 (&qop)[Geo<D>::DQ], const uint16_t* Qh, int qr, bool present, int hf) {
-#pragma unroll
-  for (int s = 0; s < Geo<D>::DQ; ++s) {
-    if (present) qop[s] = *reinterpret_cast<const bf16x8*>(Qh + (size_t)qr * D + s * 16 + hf * 8);
-    else qop[s] = bf16x8{};
-  }
-}
-
-// S^T of a chunk: lane (query) l32, register r holds key (r/4)*8 + hf*4 + r%4
-template <int D>
-__device__ __forceinline__ void qk_chunk(f32x16& sacc, const unsigned char* kt, const int (&koff)[Geo<D>::DQ],
-                                         const bf16x8 (&qop)[Geo<D>::DQ]) {
-  sacc = f32x16{};
-#pragma unroll
-  for (int s = 0; s < Geo<D>::DQ; ++s) {
-    const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kt + koff[s]);
-    sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[s], sacc, 0, 0, 0);
-  }
-}
-
-// p = exp2(c*log2e*s - m) rounded to bf16; l sums the rounded weights
-__device__ __forceinline__ void softmax_chunk(const f32x16& sacc, bf16x8 (&pop)[2], float& l_part, float m_ref,
-                                              float sl2) {
-  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-  float lsum = l_part;
-#pragma unroll
-  for (int kk = 0; kk < 2; ++kk) {
-    u32x4 wv;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kk * 8 + 2 * e], sl2, -m_ref));
-      const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kk * 8 + 2 * e + 1], sl2, -m_ref));
-      const bf16x2 pb = cvt2(p0, p1);
-      lsum = __builtin_amdgcn_fdot2_f32_bf16(pb, ones, lsum, false);
-      wv[e] = __builtin_bit_cast(unsigned, pb);
-    }
-    pop[kk] = __builtin_bit_cast(bf16x8, wv);
-  }
-  l_part = lsum;
-}
-
-// O^T += V^T P^T: P from the S^T registers, V^T by transpose reads
-template <int D>
-__device__ __forceinline__ void pv_chunk(const bf16x8 (&pop)[2], const unsigned char* vt, const int (&voff)[Geo<D>::DT],
-                                         f32x16 (&oacc)[Geo<D>::DT]) {
-#pragma unroll
-  for (int dt = 0; dt < Geo<D>::DT; ++dt)
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk)
-      oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand<D>(vt, voff[dt], kk), pop[kk], oacc[dt], 0, 0, 0);
 }
 
 // the NaN mark on a query block's first output element (recomputed later)

@@ -201,7 +201,7 @@ constexpr int kRemRows = 128;              // query blocks per workgroup
 
 // Position of key jj (0..31) of a chunk in a row of E: the eight keys one MFMA
 // lane takes for (kk, hf) -- kk*16 + hf*4 + 0..3, then kk*16 + 8 + hf*4 + 0..3,
-// the order of a softmax_chunk register group -- are the 16-byte piece
+// the key order of a 32x32x16 S^T register group -- are the 16-byte piece
 // kk*2 + hf.
 __host__ __device__ __forceinline__ int e_position(int jj) {
   const int kk = jj >> 4, r = jj & 15;
