@@ -43,6 +43,7 @@ SELECT_CASES = [
 SHAPE_CASES = [
     SC("nb700_topk", 1, 2, 64, (5, 80, 112), 64, "topk", keep_ratio=0.2, seed=215),
     SC("nb870_topk", 1, 2, 128, (5, 96, 116), 64, "topk", keep_ratio=0.15, seed=216),
+    SC("nb1000_topk", 1, 2, 64, (5, 80, 160), 64, "topk", keep_ratio=0.2, seed=221),
     SC("nb1100_topk", 1, 2, 64, (5, 80, 176), 64, "topk", keep_ratio=0.25, seed=217),
     SC("nb1280_topk", 1, 1, 128, (5, 64, 256), 64, "topk", keep_ratio=0.1, seed=218),
     SC("nb1100_mass", 1, 2, 64, (5, 80, 176), 64, "mass", mass_threshold=0.9, max_keep_ratio=0.3,
