@@ -56,16 +56,44 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t m) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
 }
 
+// Wave reductions of doubles on DPP lane moves (each half of the double moved
+// by the same pattern): within rows of 16 lanes by quad and mirror
+// permutations, then across the four rows by the row broadcasts; lane 63 ends
+// with the result, which every lane then reads (so all lanes hold the same
+// bits and control flow on it stays uniform).
+template <int CTRL, int ROWS>
+__device__ __forceinline__ double dpp_d(double x, double ident) {
+  const long long xi = __double_as_longlong(x), ii = __double_as_longlong(ident);
+  const int lo = __builtin_amdgcn_update_dpp((int)ii, (int)xi, CTRL, ROWS, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp((int)(ii >> 32), (int)(xi >> 32), CTRL, ROWS, 0xf, false);
+  return __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo));
+}
+
+__device__ __forceinline__ double lane63_d(double x) {
+  const long long xi = __double_as_longlong(x);
+  const int lo = __builtin_amdgcn_readlane((int)xi, 63);
+  const int hi = __builtin_amdgcn_readlane((int)(xi >> 32), 63);
+  return __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo));
+}
+
 __device__ __forceinline__ double wave_sum_d(double v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-  return v;
+  v += dpp_d<0xB1, 0xf>(v, 0.0);     // quad_perm 1,0,3,2
+  v += dpp_d<0x4E, 0xf>(v, 0.0);     // quad_perm 2,3,0,1
+  v += dpp_d<0x141, 0xf>(v, 0.0);    // row_half_mirror
+  v += dpp_d<0x140, 0xf>(v, 0.0);    // row_mirror
+  v += dpp_d<0x142, 0xa>(v, 0.0);    // row_bcast:15
+  v += dpp_d<0x143, 0xc>(v, 0.0);    // row_bcast:31
+  return lane63_d(v);
 }
 
 __device__ __forceinline__ double wave_max_d(double v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v = fmax(v, __shfl_xor(v, off, 64));
-  return v;
+  v = fmax(v, dpp_d<0xB1, 0xf>(v, -INFINITY));
+  v = fmax(v, dpp_d<0x4E, 0xf>(v, -INFINITY));
+  v = fmax(v, dpp_d<0x141, 0xf>(v, -INFINITY));
+  v = fmax(v, dpp_d<0x140, 0xf>(v, -INFINITY));
+  v = fmax(v, dpp_d<0x142, 0xa>(v, -INFINITY));
+  v = fmax(v, dpp_d<0x143, 0xc>(v, -INFINITY));
+  return lane63_d(v);
 }
 
 // k-th largest key (k >= 1, at least k keys > 0); returns T and the number of
