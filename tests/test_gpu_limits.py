@@ -77,7 +77,7 @@ def _selection_every_row(wl, nb_expected):
     nb = sva.num_blocks(prob)
     assert nb == nb_expected
     qp, kp = sva.pool_blocks(prob, dev["q"], dev["k"])
-    idx, cnt, _ = sva.select_blocks(prob, sel, qp, kp)
+    idx, cnt, mask = sva.select_blocks(prob, sel, qp, kp, want_mask=True)
     torch.cuda.synchronize()
     f64 = {n: oracle.bf16_bits_to_f64(bits[n]) for n in ("q", "k")}
     scores = oracle.block_scores(oracle.pool_blocks(f64["q"], wl.block), oracle.pool_blocks(f64["k"], wl.block),
@@ -85,6 +85,12 @@ def _selection_every_row(wl, nb_expected):
     kept, info = oracle_select(wl, scores)
     idx_np, cnt_np = idx.cpu().numpy(), cnt.cpu().numpy()
     parity.check_idx_layout(idx_np, cnt_np, nb)
+    # the optional mask says exactly what the lists say
+    m_np = mask.cpu().numpy().reshape(-1, nb)
+    want = np.zeros_like(m_np)
+    for r, (row, c) in enumerate(zip(idx_np.reshape(-1, idx_np.shape[-1]), cnt_np.reshape(-1))):
+        want[r, row[:c]] = 1
+    assert np.array_equal(m_np, want)
     n, same, problems = parity.compare_masks(flat_rows(kept), parity.gpu_rows(idx_np, cnt_np), scores,
                                              info["mode"], k=info["k"], tau=info["tau"], forced=info["forced"])
     assert not problems, problems[:5]
